@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Benchmark: one step = the whole hot path on the ResNet-50-shaped workload.
+
+Step = sparsify of the 161-tensor, 25,557,032-element gradient set (x = g + r,
+exact global top-k at rho = 0.001, ascending (idx, val), residual written
+back), followed by the sparse aggregate + SGD update of P = 128 workers' lists
+(this GPU's own 25,558 pairs plus 127 seeded lists of 25,600 pairs) into
+ResNet-50-shaped parameters with momentum 0.9, weight decay 5e-5, lr 0.1.
+
+Inputs are synthetic and resident in HBM before timing: ten seeded gradient
+steps and three replicas of (residual, parameters, momentum, gathered lists),
+rotated so that consecutive steps never reuse a buffer and a step's inputs are
+not left in the 256 MB last-level cache by the step before. The residual of
+each replica is carried across steps.
+
+Prints one JSON line. `value` = sparsify throughput in Gelem/s (d / mean
+sparsify time); the update's rate is reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "top-k sparsify Gelem/s at d=25.6M rho=0.001 (% of HBM peak); update GB/s"
+HBM_PEAK_GBPS = 8000.0
+RHO = 0.001
+P_WORKERS = 128
+K_LIST = 25_600
+LR, MU, WD = 0.1, 0.9, 5e-5
+GRAD_STEPS = 10
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--replicas", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip timing the CPU oracle")
+    ap.add_argument("--kernel-events", type=int, default=1,
+                    help="record HIP events around every kernel (1) or only per phase (0)")
+    return ap.parse_args()
+
+
+def log(msg: str) -> None:
+    sys.stderr.write(f"[bench] {msg}\n")
+    sys.stderr.flush()
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2010_10458_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel: str, digest: str):
+    """HBM bytes per launch measured by rocprofv3 counters, if a summary for
+    this kernel exists and was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_resnet50.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line:
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("source_digest") != digest:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(sizes, d):
+    """The CPU oracle on one step of the same workload (bounded sample)."""
+    import numpy as np
+
+    import gen
+    import oracle
+    orc = oracle.Oracle()
+    grads = gen.resnet_grads(0)
+    res = [np.zeros(n, np.float32) for n in sizes]
+    t0 = time.perf_counter()
+    idx, val, _, ks = orc.sparsify(grads, res, rho=RHO)
+    t_sp = time.perf_counter() - t0
+    lists_i, lists_v = gen.sparse_lists(d, P_WORKERS, K_LIST, step=0)
+    w = gen.concat(gen.params_like(sizes, config=5))
+    b = np.zeros(d, np.float32)
+    t0 = time.perf_counter()
+    orc.update(w, b, lists_i, lists_v, lr=LR, mu=MU, wd=WD)
+    t_up = time.perf_counter() - t0
+    upd_bytes = 16 * d + 8 * P_WORKERS * K_LIST
+    return {"value": round(d / t_sp / 1e9, 6), "unit": "Gelem/s", "cores": 1, "kind": "oracle",
+            "sample": f"one ResNet-50-shaped sparsify step (d={d}, k={ks[0]}, full comparison "
+                      f"sort) plus one P={P_WORKERS} x {K_LIST} momentum update, single thread",
+            "sparsify_s": round(t_sp, 3), "update_s": round(t_up, 3),
+            "update_GBps": round(upd_bytes / t_up / 1e9, 3),
+            "host_cpus": os.cpu_count()}
+
+
+def main() -> int:
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (this build has no multi-GPU path); "
+              f"got --gpus {args.gpus}", file=sys.stderr)
+        return 2
+    import numpy as np
+    import torch
+
+    import gen
+    import paper_2010_10458_amd as tk
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sizes = gen.numels(gen.resnet50_shapes())
+    d = sum(sizes)
+    R = args.replicas
+
+    log(f"generating inputs: d={d}, {GRAD_STEPS} gradient steps, {R} replicas")
+    bank = []
+    for s in range(GRAD_STEPS):
+        bank.append([torch.from_numpy(a).to(dev) for a in gen.resnet_grads(s)])
+    resid = [[torch.zeros(n, device=dev) for n in sizes] for _ in range(R)]
+    w0 = gen.params_like(sizes, config=5)
+    params = [[torch.from_numpy(a).to(dev) for a in w0] for _ in range(R)]
+    mom = [[torch.zeros(n, device=dev) for n in sizes] for _ in range(R)]
+    idx_all, val_all = [], []
+    for j in range(R):
+        li, lv = gen.sparse_lists(d, P_WORKERS, K_LIST, step=100 + j)
+        idx_all.append(torch.from_numpy(li).to(dev))
+        val_all.append(torch.from_numpy(lv).to(dev))
+
+    plans = [[tk.SparsifyPlan(sizes, rho=RHO) for _ in range(R)] for _ in range(GRAD_STEPS)]
+    for s in range(GRAD_STEPS):
+        for j in range(R):
+            plans[s][j].bind(bank[s], resid[j])
+    k_total = plans[0][0].k_total
+    uplans = [tk.UpdatePlan(sizes, P=P_WORKERS, stride=K_LIST).bind(params[j], mom[j])
+              for j in range(R)]
+    nnz = torch.tensor([k_total] + [K_LIST] * (P_WORKERS - 1), dtype=torch.int32, device=dev)
+    sp_names = plans[0][0].launch_names()
+    up_names = uplans[0].launch_names()
+    n_sp, n_up = len(sp_names) + 1, len(up_names) + 1
+    if not args.kernel_events:
+        n_sp = n_up = 1
+
+    def make_events(n):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in evs:
+            e.record()
+        return evs
+
+    K, W = args.steps, args.warmup
+    ev_sp = [make_events(max(n_sp, 2)) for _ in range(K)]
+    ev_up = [make_events(max(n_up, 2)) for _ in range(K)]
+    torch.cuda.synchronize()
+
+    def step(i, t=None):
+        s, j = i % GRAD_STEPS, i % R
+        sp, up = plans[s][j], uplans[j]
+        if t is not None and args.kernel_events:
+            sp.set_events(ev_sp[t])
+            up.set_events(ev_up[t])
+        elif t is not None:
+            ev_sp[t][0].record()
+        sp.execute(idx_out=idx_all[j][0], val_out=val_all[j][0])
+        if t is not None and not args.kernel_events:
+            ev_sp[t][1].record()
+            ev_up[t][0].record()
+        up.execute(idx_all[j], val_all[j], lr=LR, mu=MU, wd=WD, nnz=nnz)
+        if t is not None and not args.kernel_events:
+            ev_up[t][1].record()
+        if t is not None and args.kernel_events:
+            sp.set_events(None)
+            up.set_events(None)
+
+    log(f"warmup {W} steps")
+    for i in range(W):
+        step(i)
+    torch.cuda.synchronize()
+    log(f"timing {K} steps")
+    t0 = time.perf_counter()
+    for t in range(K):
+        step(W + t, t)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    log("timed region done")
+
+    sp_ms = np.array([ev_sp[t][0].elapsed_time(ev_sp[t][-1]) for t in range(K)])
+    up_ms = np.array([ev_up[t][0].elapsed_time(ev_up[t][-1]) for t in range(K)])
+    kern = {}
+    if args.kernel_events:
+        for names, evs in ((sp_names, ev_sp), (up_names, ev_up)):
+            for i, name in enumerate(names):
+                kern[name] = float(np.mean([evs[t][i].elapsed_time(evs[t][i + 1])
+                                            for t in range(K)]))
+
+    sp_s = float(sp_ms.mean()) / 1e3
+    up_s = float(up_ms.mean()) / 1e3
+    sp_bytes = 12 * d + 8 * k_total
+    total_pairs = k_total + (P_WORKERS - 1) * K_LIST
+    up_bytes = 16 * d + 8 * total_pairs
+    algo = {"stream": 12 * d, "update": 16 * d + 8 * total_pairs, "emit": 8 * k_total}
+
+    roofline = None
+    if kern:
+        dom = max(kern, key=kern.get)
+        bytes_per_launch = algo.get(dom, 0)
+        achieved = bytes_per_launch / (kern[dom] / 1e3) / 1e9
+        digest = kernel_source_digest()
+        roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                    "traffic": read_traffic(dom, digest),
+                    "algorithmic_bytes_per_launch": bytes_per_launch,
+                    "mean_launch_us": round(kern[dom] * 1e3, 2),
+                    "source_digest": digest}
+
+    out = {
+        "metric": METRIC,
+        "value": round(d / sp_s / 1e9, 3),
+        "unit": "Gelem/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(wall / K * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "resnet50-shaped gradient set: 161 fp32 tensors, d=25557032, "
+                               "N(0,1e-2) with 1% x100 outliers, residual carried; global top-k "
+                               "rho=0.001; then P=128 aggregate-update (25,600-pair lists), "
+                               "momentum 0.9, wd 5e-5, lr 0.1",
+                   "d": d, "k": k_total, "rho": RHO, "P": P_WORKERS, "replicas": R},
+        "sparsify_us": round(sp_s * 1e6, 2),
+        "sparsify_GBps": round(sp_bytes / sp_s / 1e9, 1),
+        "sparsify_frac_hbm_peak": round(sp_bytes / sp_s / 1e9 / HBM_PEAK_GBPS, 4),
+        "update_us": round(up_s * 1e6, 2),
+        "update_GBps": round(up_bytes / up_s / 1e9, 1),
+        "update_frac_hbm_peak": round(up_bytes / up_s / 1e9 / HBM_PEAK_GBPS, 4),
+        "kernels_us": {k: round(v * 1e3, 2) for k, v in kern.items()},
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on one step (bounded sample)")
+        out["cpu_baseline"] = cpu_baseline(sizes, d)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

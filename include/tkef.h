@@ -1,0 +1,203 @@
+/*
+ * tkef: exact top-k gradient sparsification with error feedback, and the
+ * sparse aggregate + merged multi-tensor SGD update, for AMD MI355X (gfx950).
+ *
+ * C ABI. Every pointer argument documented as "device" must point to device
+ * memory of the current HIP device; "host" pointers are read during the call
+ * only. The caller owns every buffer. The library allocates no device memory:
+ * all scratch space lives in a caller-provided workspace ("ws"), whose size is
+ * reported by the *_info / *_workspace queries. All GPU work of a call is
+ * enqueued on the caller's stream and is asynchronous with respect to the
+ * host, except where a function says it synchronizes.
+ *
+ * Return codes: TKEF_OK (0) or a negative TKEF_E* code. A call that returns
+ * an error has enqueued no GPU work, except TKEF_EHIP, which reports a HIP
+ * runtime failure (launch or copy) after work may have been enqueued.
+ * Problems that only the GPU can see (a NaN in the data, an unsorted or
+ * out-of-range index list) set bits in an optional caller-owned device status
+ * word (uint32, zeroed by the caller, bits OR-ed in by the library).
+ *
+ * Thread safety: plans are not shared between threads without external
+ * locking; distinct plans may be used concurrently. Calls that share a
+ * workspace must be ordered on one stream.
+ */
+#ifndef TKEF_H
+#define TKEF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TKEF_VERSION 10000 /* major * 10000 + minor * 100 + patch */
+
+/* return codes */
+#define TKEF_OK 0
+#define TKEF_EINVAL (-1)     /* null pointer, bad mode, bad count, aliasing */
+#define TKEF_ERANGE (-2)     /* size >= 2^31, k outside [1, d], rho outside (0, 1] */
+#define TKEF_EWORKSPACE (-3) /* workspace missing, too small or not 256-B aligned */
+#define TKEF_EHIP (-4)       /* HIP runtime error */
+#define TKEF_ESTATE (-5)     /* plan not bound, or bound to another workspace */
+#define TKEF_ENOMEM (-6)     /* host allocation failed */
+
+/* selection modes */
+#define TKEF_GLOBAL 0     /* one selection over the concatenated tensor list */
+#define TKEF_PER_TENSOR 1 /* one selection per tensor, k_t from rho per tensor */
+
+/* device status bits */
+#define TKEF_STATUS_NAN 1u         /* sparsify saw a NaN in g + r */
+#define TKEF_STATUS_UNSORTED 2u    /* an update index list is not ascending */
+#define TKEF_STATUS_INDEX_RANGE 4u /* an update index lies outside [0, d) */
+
+int tkef_version(void);
+const char *tkef_strerror(int code);
+
+/*
+ * k = ceil(rho * d) evaluated in double precision, clamped to [1, d]; the
+ * paper writes k = rho * d for a density 0 < rho < 1 (Sec. 3.2, sparse
+ * format) without a rounding rule. Returns 0 for d == 0 and a negative code
+ * for rho outside (0, 1] or d < 0.
+ */
+int64_t tkef_k_from_rho(int64_t d, double rho);
+
+/* ========================================================================
+ * Sparsify (Sec. 3.1, TopK operator; Alg. 1 output format; error feedback)
+ *
+ * For a list of T float32 gradient tensors g_t and residual tensors r_t
+ * (same sizes), with global position i = offset_t + j in the concatenation:
+ *   x_i = g_i + r_i                       (one binary32 add, round-to-nearest)
+ *   S   = the k positions first in the order (|x| descending, i ascending)
+ *   idx = S in ascending order (int32), val_j = x[idx_j] (bitwise, sign kept)
+ *   r_i = x_i for i not in S, +0.0f for i in S     (residuals updated in place)
+ * TKEF_GLOBAL selects once over all positions (k from rho over the total
+ * size, or an explicit k). TKEF_PER_TENSOR selects k_t = tkef_k_from_rho(n_t,
+ * rho) within each tensor; outputs are concatenated in tensor order and still
+ * carry global positions. Magnitudes compare as IEEE values: -0 equals +0,
+ * infinities rank above every finite value. A NaN in x sets
+ * TKEF_STATUS_NAN; the selection is then unspecified (but every output is
+ * still written within bounds).
+ * ====================================================================== */
+
+typedef struct tkef_sparsify_plan_s *tkef_sparsify_plan;
+
+/* Host only. numels: host array of T sizes (each >= 0, total in [1, 2^31-1]).
+ * k > 0 gives an explicit k (TKEF_GLOBAL only, k <= total); k == 0 takes k
+ * from rho. */
+int tkef_sparsify_plan_create(const int64_t *numels, int32_t ntensors, int32_t mode,
+                              double rho, int64_t k, tkef_sparsify_plan *plan_out);
+int tkef_sparsify_plan_destroy(tkef_sparsify_plan plan);
+
+/* Host only. workspace_bytes: device workspace the plan needs; k_total: number
+ * of (idx, val) pairs an execution writes; d_total: total positions;
+ * ngroups: 1 (global) or T (per tensor); nlaunch: kernels per execution. */
+int tkef_sparsify_plan_info(tkef_sparsify_plan plan, size_t *workspace_bytes,
+                            int64_t *k_total, int64_t *d_total, int32_t *ngroups,
+                            int32_t *nlaunch);
+
+/* Host only: k of each selection group (ngroups entries). */
+int tkef_sparsify_plan_group_k(tkef_sparsify_plan plan, int64_t *k_out, int32_t n);
+
+/* Binds device tensors to the plan and writes the plan's descriptor tables
+ * into ws (device, >= workspace_bytes, 256-B aligned). grads[t], residuals[t]:
+ * host arrays of device pointers (non-null when numel > 0; g and r must not
+ * overlap). Copies host -> device on `stream` and synchronizes that stream.
+ * The ws then belongs to the plan until the next bind. */
+int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float *const *grads,
+                            float *const *residuals, void *ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* Runs one sparsify on the bound tensors: reads g, updates r in place, writes
+ * k_total pairs to idx_out (device int32) and val_out (device float32). ws
+ * must be the bound workspace. status: optional device word. Asynchronous. */
+int tkef_sparsify_execute(tkef_sparsify_plan plan, void *ws, size_t ws_bytes,
+                          int32_t *idx_out, float *val_out, uint32_t *status,
+                          hipStream_t stream);
+
+/* Optional timing hook: with n_events >= nlaunch + 1, each execution records
+ * events[0] before its first kernel and events[i + 1] after kernel i (HIP
+ * events created by the caller). Pass NULL to switch it off. Names of the
+ * kernels in launch order are available from tkef_sparsify_plan_launch_name. */
+int tkef_sparsify_plan_set_events(tkef_sparsify_plan plan, hipEvent_t *events,
+                                  int32_t n_events);
+const char *tkef_sparsify_plan_launch_name(tkef_sparsify_plan plan, int32_t i);
+
+/* One-shot convenience: create + bind + execute + destroy. Synchronizes
+ * `stream` once (during bind). */
+int tkef_sparsify_workspace(const int64_t *numels, int32_t ntensors, int32_t mode,
+                            double rho, int64_t k, size_t *workspace_bytes,
+                            int64_t *k_total);
+int tkef_sparsify(const float *const *grads, float *const *residuals,
+                  const int64_t *numels, int32_t ntensors, int32_t mode, double rho,
+                  int64_t k, int32_t *idx_out, float *val_out, void *ws,
+                  size_t ws_bytes, uint32_t *status, hipStream_t stream);
+
+/* ========================================================================
+ * Sparse aggregate + merged multi-tensor SGD update
+ * (Alg. 2, accumulation of the gathered lists; Eq. (1) update)
+ *
+ * P workers' sparse gradients in the gathered layout that an All-Gather of
+ * fixed-size lists produces: worker p's entries are idx[p*stride + j],
+ * val[p*stride + j] for j < nnz_p (nnz_p = nnz[p] if an nnz array is given,
+ * else stride). Indices are global positions in the concatenation of the T
+ * parameter tensors; each worker's list must be ascending (repeats allowed and
+ * summed). With G = sum over workers of their values at each position:
+ *   mu == 0 and wd == 0:  w_i -= lr * G_i at every position some list names
+ *                         (all other parameters are left untouched)
+ *   otherwise, at every position:
+ *       D = G_i + wd * w_i;  if mu != 0: b_i = mu * b_i + D, U = b_i; else U = D
+ *       w_i -= lr * U
+ * Each step is a binary32 operation with round-to-nearest (no fused
+ * multiply-add). G is accumulated in binary32; where three or more workers
+ * name one position, the order of its additions is unspecified.
+ * ====================================================================== */
+
+typedef struct tkef_update_plan_s *tkef_update_plan;
+
+/* Host only. numels: T parameter sizes (total in [1, 2^31-1]); P workers
+ * (1 <= P <= 65535); stride: entries reserved per worker in the gathered
+ * arrays (0 <= stride <= 2^31-1). */
+int tkef_update_plan_create(const int64_t *numels, int32_t ntensors, int32_t P,
+                            int64_t stride, tkef_update_plan *plan_out);
+int tkef_update_plan_destroy(tkef_update_plan plan);
+int tkef_update_plan_info(tkef_update_plan plan, size_t *workspace_bytes,
+                          int64_t *d_total, int32_t *nlaunch);
+
+/* Binds parameter tensors (host array of T device pointers) and optional
+ * momentum buffers (host array of T device pointers, or NULL) and writes the
+ * descriptor tables into ws. Copies host -> device and synchronizes `stream`. */
+int tkef_update_plan_bind(tkef_update_plan plan, float *const *params,
+                          float *const *momentum, void *ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+/* Applies one aggregate + update. idx (device int32) and val (device float32)
+ * hold P * stride entries; nnz: optional device int32 array of P counts
+ * (each clamped to [0, stride]). mu != 0 needs momentum buffers at bind.
+ * lr, mu, wd must be finite. Asynchronous. */
+int tkef_update_execute(tkef_update_plan plan, const int32_t *idx, const float *val,
+                        const int32_t *nnz, float lr, float mu, float wd, void *ws,
+                        size_t ws_bytes, uint32_t *status, hipStream_t stream);
+
+int tkef_update_plan_set_events(tkef_update_plan plan, hipEvent_t *events,
+                                int32_t n_events);
+const char *tkef_update_plan_launch_name(tkef_update_plan plan, int32_t i);
+
+/* One-shot convenience: create + bind + execute + destroy (synchronizes
+ * `stream` once, during bind). */
+int tkef_update_workspace(const int64_t *numels, int32_t ntensors, int32_t P,
+                          int64_t stride, size_t *workspace_bytes);
+int tkef_sparse_aggregate_update(float *const *params, float *const *momentum,
+                                 const int64_t *numels, int32_t ntensors,
+                                 const int32_t *idx, const float *val, int32_t P,
+                                 int64_t stride, const int32_t *nnz, float lr,
+                                 float mu, float wd, void *ws, size_t ws_bytes,
+                                 uint32_t *status, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TKEF_H */

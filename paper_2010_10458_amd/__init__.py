@@ -1,0 +1,320 @@
+"""Exact top-k gradient sparsification with error feedback and the sparse
+aggregate + multi-tensor SGD update on AMD MI355X (gfx950).
+
+Thin ctypes binding over ``lib/libtkef.so`` (C ABI in ``include/tkef.h``).
+This module only marshals arguments: every step of the computation runs in
+the library's HIP kernels. PyTorch supplies device memory and streams.
+
+    plan = SparsifyPlan(numels, mode=GLOBAL, rho=0.001)
+    plan.bind(grads, residuals)            # once per set of buffers
+    idx, val = plan.execute()              # every step
+
+    up = UpdatePlan(numels, P=128, stride=k)
+    up.bind(params, momentum)              # once
+    up.execute(idx_all, val_all, lr=0.1, mu=0.9, wd=5e-5)
+"""
+from __future__ import annotations
+
+# torch first: it loads the HIP runtime that this library must share
+import torch  # noqa: E402
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "lib", "libtkef.so")
+
+GLOBAL = 0
+PER_TENSOR = 1
+STATUS_NAN = 1
+STATUS_UNSORTED = 2
+STATUS_INDEX_RANGE = 4
+
+OK, EINVAL, ERANGE, EWORKSPACE, EHIP, ESTATE, ENOMEM = 0, -1, -2, -3, -4, -5, -6
+
+
+class TkefError(RuntimeError):
+    def __init__(self, fn: str, code: int, msg: str):
+        super().__init__(f"{fn}: {msg} ({code})")
+        self.code = code
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
+    vp, i32, i64, f32, f64, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                  ctypes.c_float, ctypes.c_double, ctypes.c_size_t)
+    P = ctypes.POINTER
+    sig = {
+        "tkef_version": ([], ctypes.c_int),
+        "tkef_strerror": ([ctypes.c_int], ctypes.c_char_p),
+        "tkef_k_from_rho": ([i64, f64], i64),
+        "tkef_sparsify_plan_create": ([P(i64), i32, i32, f64, i64, P(vp)], ctypes.c_int),
+        "tkef_sparsify_plan_destroy": ([vp], ctypes.c_int),
+        "tkef_sparsify_plan_info": ([vp, P(sz), P(i64), P(i64), P(i32), P(i32)], ctypes.c_int),
+        "tkef_sparsify_plan_group_k": ([vp, P(i64), i32], ctypes.c_int),
+        "tkef_sparsify_plan_bind": ([vp, P(vp), P(vp), vp, sz, vp], ctypes.c_int),
+        "tkef_sparsify_execute": ([vp, vp, sz, vp, vp, vp, vp], ctypes.c_int),
+        "tkef_sparsify_plan_set_events": ([vp, P(vp), i32], ctypes.c_int),
+        "tkef_sparsify_plan_launch_name": ([vp, i32], ctypes.c_char_p),
+        "tkef_sparsify_workspace": ([P(i64), i32, i32, f64, i64, P(sz), P(i64)], ctypes.c_int),
+        "tkef_sparsify": ([P(vp), P(vp), P(i64), i32, i32, f64, i64, vp, vp, vp, sz, vp, vp],
+                          ctypes.c_int),
+        "tkef_update_plan_create": ([P(i64), i32, i32, i64, P(vp)], ctypes.c_int),
+        "tkef_update_plan_destroy": ([vp], ctypes.c_int),
+        "tkef_update_plan_info": ([vp, P(sz), P(i64), P(i32)], ctypes.c_int),
+        "tkef_update_plan_bind": ([vp, P(vp), P(vp), vp, sz, vp], ctypes.c_int),
+        "tkef_update_execute": ([vp, vp, vp, vp, f32, f32, f32, vp, sz, vp, vp], ctypes.c_int),
+        "tkef_update_plan_set_events": ([vp, P(vp), i32], ctypes.c_int),
+        "tkef_update_plan_launch_name": ([vp, i32], ctypes.c_char_p),
+        "tkef_update_workspace": ([P(i64), i32, i32, i64, P(sz)], ctypes.c_int),
+        "tkef_sparse_aggregate_update": ([P(vp), P(vp), P(i64), i32, vp, vp, i32, i64, vp, f32,
+                                          f32, f32, vp, sz, vp, vp], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library. Raises if it has not been built: there is no
+    fallback implementation."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        _lib = _declare(ctypes.CDLL(LIB_PATH))
+    return _lib
+
+
+def _check(fn: str, rc: int) -> None:
+    if rc != OK:
+        raise TkefError(fn, rc, lib().tkef_strerror(rc).decode())
+
+
+def strerror(code: int) -> str:
+    return lib().tkef_strerror(code).decode()
+
+
+def k_from_rho(d: int, rho: float) -> int:
+    return int(lib().tkef_k_from_rho(d, rho))
+
+
+def _i64_array(vals: Sequence[int]):
+    return (ctypes.c_int64 * max(1, len(vals)))(*[int(v) for v in vals])
+
+
+def _ptr_array(ts: Sequence[Optional[torch.Tensor]]):
+    return (ctypes.c_void_p * max(1, len(ts)))(*[(t.data_ptr() if t is not None else None)
+                                                 for t in ts])
+
+
+def _stream_handle(stream: Optional[torch.cuda.Stream]) -> Optional[int]:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream or None
+
+
+def _check_f32_tensors(ts: Sequence[torch.Tensor], what: str) -> None:
+    for t in ts:
+        if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{what}: expected contiguous float32 CUDA tensors")
+
+
+def _events(events: Optional[Sequence[torch.cuda.Event]]):
+    """Raw event handles of torch events (each recorded once so it exists)."""
+    if not events:
+        return None, 0
+    for e in events:
+        if e.cuda_event == 0:
+            e.record()
+    arr = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+    return arr, len(events)
+
+
+# ----------------------------------------------------------------------------
+class SparsifyPlan:
+    """Plan for sparsifying a fixed list of tensor sizes (see tkef.h)."""
+
+    def __init__(self, numels: Sequence[int], mode: int = GLOBAL, rho: Optional[float] = None,
+                 k: Optional[int] = None):
+        self._numels = [int(n) for n in numels]
+        self._h = ctypes.c_void_p()
+        L = lib()
+        _check("tkef_sparsify_plan_create", L.tkef_sparsify_plan_create(
+            _i64_array(self._numels), len(self._numels), int(mode),
+            float(rho) if rho is not None else 0.0, int(k) if k else 0, ctypes.byref(self._h)))
+        ws, kt, d, ng, nl = (ctypes.c_size_t(), ctypes.c_int64(), ctypes.c_int64(),
+                             ctypes.c_int32(), ctypes.c_int32())
+        _check("tkef_sparsify_plan_info", L.tkef_sparsify_plan_info(
+            self._h, ctypes.byref(ws), ctypes.byref(kt), ctypes.byref(d), ctypes.byref(ng),
+            ctypes.byref(nl)))
+        self.ws_bytes, self.k_total, self.d = ws.value, kt.value, d.value
+        self.ngroups, self.nlaunch = ng.value, nl.value
+        self.ws: Optional[torch.Tensor] = None
+        self._bound = None
+        self._events = None
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._h.value and _lib is not None:
+            _lib.tkef_sparsify_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def group_k(self):
+        arr = (ctypes.c_int64 * self.ngroups)()
+        _check("tkef_sparsify_plan_group_k", lib().tkef_sparsify_plan_group_k(
+            self._h, arr, self.ngroups))
+        return list(arr)
+
+    def launch_names(self):
+        return [lib().tkef_sparsify_plan_launch_name(self._h, i).decode()
+                for i in range(self.nlaunch)]
+
+    def bind(self, grads: Sequence[torch.Tensor], residuals: Sequence[torch.Tensor],
+             ws: Optional[torch.Tensor] = None, stream=None) -> "SparsifyPlan":
+        if len(grads) != len(self._numels) or len(residuals) != len(self._numels):
+            raise ValueError("tensor count does not match the plan")
+        _check_f32_tensors(list(grads) + list(residuals), "bind")
+        for g, r, n in zip(grads, residuals, self._numels):
+            if g.numel() != n or r.numel() != n:
+                raise ValueError("tensor size does not match the plan")
+        dev = grads[0].device
+        if ws is None:
+            ws = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=dev)
+        self.ws = ws
+        _check("tkef_sparsify_plan_bind", lib().tkef_sparsify_plan_bind(
+            self._h, _ptr_array(grads), _ptr_array(residuals), ws.data_ptr(), ws.numel(),
+            _stream_handle(stream)))
+        self._bound = (list(grads), list(residuals))
+        return self
+
+    def set_events(self, events: Optional[Sequence[torch.cuda.Event]]) -> None:
+        arr, n = _events(events)
+        self._events = (arr, list(events) if events else None)
+        _check("tkef_sparsify_plan_set_events",
+               lib().tkef_sparsify_plan_set_events(self._h, arr, n))
+
+    def execute(self, idx_out: Optional[torch.Tensor] = None,
+                val_out: Optional[torch.Tensor] = None,
+                status: Optional[torch.Tensor] = None, stream=None
+                ) -> Tuple[torch.Tensor, torch.Tensor]:
+        if self._bound is None or self.ws is None:
+            raise RuntimeError("plan is not bound")
+        dev = self.ws.device
+        if idx_out is None:
+            idx_out = torch.empty(max(self.k_total, 1), dtype=torch.int32, device=dev)
+        if val_out is None:
+            val_out = torch.empty(max(self.k_total, 1), dtype=torch.float32, device=dev)
+        if idx_out.numel() < self.k_total or val_out.numel() < self.k_total:
+            raise ValueError("output buffers too small")
+        if idx_out.dtype != torch.int32 or val_out.dtype != torch.float32:
+            raise ValueError("idx_out must be int32 and val_out float32")
+        _check("tkef_sparsify_execute", lib().tkef_sparsify_execute(
+            self._h, self.ws.data_ptr(), self.ws.numel(), idx_out.data_ptr(),
+            val_out.data_ptr(), status.data_ptr() if status is not None else None,
+            _stream_handle(stream)))
+        return idx_out[: self.k_total], val_out[: self.k_total]
+
+
+class UpdatePlan:
+    """Plan for the sparse aggregate + SGD update of a fixed parameter list."""
+
+    def __init__(self, numels: Sequence[int], P: int, stride: int):
+        self._numels = [int(n) for n in numels]
+        self.P, self.stride = int(P), int(stride)
+        self._h = ctypes.c_void_p()
+        L = lib()
+        _check("tkef_update_plan_create", L.tkef_update_plan_create(
+            _i64_array(self._numels), len(self._numels), self.P, self.stride,
+            ctypes.byref(self._h)))
+        ws, d, nl = ctypes.c_size_t(), ctypes.c_int64(), ctypes.c_int32()
+        _check("tkef_update_plan_info", L.tkef_update_plan_info(
+            self._h, ctypes.byref(ws), ctypes.byref(d), ctypes.byref(nl)))
+        self.ws_bytes, self.d, self.nlaunch = ws.value, d.value, nl.value
+        self.ws: Optional[torch.Tensor] = None
+        self._bound = None
+        self._events = None
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._h.value and _lib is not None:
+            _lib.tkef_update_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def launch_names(self):
+        return [lib().tkef_update_plan_launch_name(self._h, i).decode()
+                for i in range(self.nlaunch)]
+
+    def bind(self, params: Sequence[torch.Tensor],
+             momentum: Optional[Sequence[torch.Tensor]] = None,
+             ws: Optional[torch.Tensor] = None, stream=None) -> "UpdatePlan":
+        if len(params) != len(self._numels):
+            raise ValueError("tensor count does not match the plan")
+        _check_f32_tensors(list(params) + list(momentum or []), "bind")
+        for i, (w, n) in enumerate(zip(params, self._numels)):
+            if w.numel() != n or (momentum is not None and momentum[i].numel() != n):
+                raise ValueError("tensor size does not match the plan")
+        if ws is None:
+            ws = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=params[0].device)
+        self.ws = ws
+        mom = _ptr_array(momentum) if momentum is not None else None
+        _check("tkef_update_plan_bind", lib().tkef_update_plan_bind(
+            self._h, _ptr_array(params), mom, ws.data_ptr(), ws.numel(),
+            _stream_handle(stream)))
+        self._bound = (list(params), list(momentum) if momentum is not None else None)
+        return self
+
+    def set_events(self, events: Optional[Sequence[torch.cuda.Event]]) -> None:
+        arr, n = _events(events)
+        self._events = (arr, list(events) if events else None)
+        _check("tkef_update_plan_set_events", lib().tkef_update_plan_set_events(self._h, arr, n))
+
+    def execute(self, idx: torch.Tensor, val: torch.Tensor, lr: float, mu: float = 0.0,
+                wd: float = 0.0, nnz: Optional[torch.Tensor] = None,
+                status: Optional[torch.Tensor] = None, stream=None) -> None:
+        if self._bound is None or self.ws is None:
+            raise RuntimeError("plan is not bound")
+        if idx.dtype != torch.int32 or val.dtype != torch.float32:
+            raise ValueError("idx must be int32 and val float32")
+        if not (idx.is_cuda and val.is_cuda and idx.is_contiguous() and val.is_contiguous()):
+            raise ValueError("idx and val must be contiguous CUDA tensors")
+        if idx.numel() < self.P * self.stride or val.numel() < self.P * self.stride:
+            raise ValueError("idx / val hold fewer than P * stride entries")
+        if nnz is not None and (nnz.dtype != torch.int32 or nnz.numel() < self.P or not nnz.is_cuda):
+            raise ValueError("nnz must be a CUDA int32 tensor of P counts")
+        _check("tkef_update_execute", lib().tkef_update_execute(
+            self._h, idx.data_ptr(), val.data_ptr(),
+            nnz.data_ptr() if nnz is not None else None, float(lr), float(mu), float(wd),
+            self.ws.data_ptr(), self.ws.numel(),
+            status.data_ptr() if status is not None else None, _stream_handle(stream)))
+
+
+# ----------------------------------------------------------------------------
+# one-shot conveniences (the spec call shapes)
+
+def sparsify(grads: Sequence[torch.Tensor], residuals: Sequence[torch.Tensor],
+             rho: Optional[float] = None, mode: int = GLOBAL, k: Optional[int] = None,
+             status: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """x = g + r; top-k of |x| (ties to the lower position); r <- x with the
+    selected entries zeroed. Returns (idx int32, val float32)."""
+    plan = SparsifyPlan([t.numel() for t in grads], mode=mode, rho=rho, k=k)
+    plan.bind(grads, residuals)
+    return plan.execute(status=status)
+
+
+def sparse_aggregate_update(params: Sequence[torch.Tensor], idx: torch.Tensor,
+                            val: torch.Tensor, lr: float,
+                            momentum: Optional[Sequence[torch.Tensor]] = None,
+                            mu: float = 0.0, wd: float = 0.0,
+                            nnz: Optional[torch.Tensor] = None,
+                            status: Optional[torch.Tensor] = None) -> None:
+    """Sum P workers' sparse gradients (idx, val: (P, stride) gathered layout)
+    and apply w -= lr * (sum [+ wd * w], through momentum if mu != 0)."""
+    if idx.dim() == 1:
+        idx, val = idx.view(1, -1), val.view(1, -1)
+    P, stride = idx.shape
+    plan = UpdatePlan([t.numel() for t in params], P=P, stride=stride)
+    plan.bind(params, momentum)
+    plan.execute(idx.contiguous(), val.contiguous(), lr=lr, mu=mu, wd=wd, nnz=nnz, status=status)

@@ -1,0 +1,517 @@
+// Host side of the tkef C ABI: argument validation, plans, workspace layout
+// and the launch sequence. No device memory is allocated here; every device
+// buffer is the caller's.
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include <hip/hip_runtime_api.h>
+
+#include "tkef.h"
+#include "tkef_internal.h"
+
+using namespace tkef;
+
+namespace {
+
+constexpr int64_t kMaxD = 2147483647LL;  // positions are int32
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+bool aligned_ws(const void* ws) {
+  return (reinterpret_cast<uintptr_t>(ws) & (kAlign - 1)) == 0;
+}
+
+int hip_rc(hipError_t e) { return e == hipSuccess ? TKEF_OK : TKEF_EHIP; }
+
+bool ranges_overlap(const void* a, const void* b, int64_t n) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  const uintptr_t bytes = static_cast<uintptr_t>(n) * sizeof(float);
+  return x < y + bytes && y < x + bytes;
+}
+
+// Validates a tensor-size list: sizes >= 0, total in [1, kMaxD].
+int check_numels(const int64_t* numels, int32_t ntensors, int64_t* total) {
+  if (!numels || ntensors <= 0) return TKEF_EINVAL;
+  int64_t d = 0;
+  for (int32_t t = 0; t < ntensors; ++t) {
+    if (numels[t] < 0) return TKEF_EINVAL;
+    if (numels[t] > kMaxD) return TKEF_ERANGE;
+    d += numels[t];
+    if (d > kMaxD) return TKEF_ERANGE;
+  }
+  if (d < 1) return TKEF_ERANGE;
+  *total = d;
+  return TKEF_OK;
+}
+
+// Records the optional timing event that follows launch `i` (or precedes
+// launch 0 when i == -1).
+struct Tracer {
+  hipEvent_t* ev;
+  int32_t n;
+  hipStream_t s;
+  void mark(int i) const {
+    if (ev && i + 1 < n) (void)hipEventRecord(ev[i + 1], s);
+  }
+};
+
+}  // namespace
+
+// ============================================================================
+// shared helpers
+
+extern "C" int tkef_version(void) { return TKEF_VERSION; }
+
+extern "C" const char* tkef_strerror(int code) {
+  switch (code) {
+    case TKEF_OK: return "ok";
+    case TKEF_EINVAL: return "invalid argument (null pointer, bad mode or count, aliasing)";
+    case TKEF_ERANGE: return "out of range (size >= 2^31, k outside [1, d], rho outside (0, 1])";
+    case TKEF_EWORKSPACE: return "workspace missing, too small or not 256-byte aligned";
+    case TKEF_EHIP: return "HIP runtime error";
+    case TKEF_ESTATE: return "plan not bound, or bound to a different workspace";
+    case TKEF_ENOMEM: return "host allocation failed";
+    default: return "unknown tkef error code";
+  }
+}
+
+extern "C" int64_t tkef_k_from_rho(int64_t d, double rho) {
+  if (d < 0 || !(rho > 0.0 && rho <= 1.0) || !std::isfinite(rho)) return TKEF_ERANGE;
+  if (d == 0) return 0;
+  const double kd = std::ceil(rho * static_cast<double>(d));
+  int64_t k = static_cast<int64_t>(kd);
+  if (k < 1) k = 1;
+  if (k > d) k = d;
+  return k;
+}
+
+// ============================================================================
+// sparsify plan
+
+static const char* const kSparsifyLaunches[] = {
+    "fill", "stream", "pick1", "refine2", "pick2", "refine3", "pick3",
+    "count", "scan", "emit"};
+constexpr int32_t kSparsifyNLaunch = 10;
+
+struct tkef_sparsify_plan_s {
+  int32_t ntensors = 0, mode = 0, ngroups = 0, ntiles = 0;
+  int64_t d = 0, k_total = 0, nlines = 0;
+  std::vector<int64_t> numels, goff, kgroup;
+  std::vector<TileDesc> tiles;   // pointers filled at bind
+  std::vector<GroupDesc> groups;
+  size_t off_tiles = 0, off_groups = 0, off_state = 0, off_hist1 = 0, off_hist2 = 0,
+         off_hist3 = 0, off_zero_end = 0, off_summ = 0, off_cnt = 0, off_pglob = 0,
+         off_prel = 0, ws_bytes = 0;
+  void* bound_ws = nullptr;
+  hipEvent_t* events = nullptr;
+  int32_t n_events = 0;
+};
+
+extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors, int32_t mode,
+                                         double rho, int64_t k, tkef_sparsify_plan* plan_out) {
+  if (!plan_out) return TKEF_EINVAL;
+  *plan_out = nullptr;
+  int64_t d = 0;
+  int rc = check_numels(numels, ntensors, &d);
+  if (rc) return rc;
+  if (mode != TKEF_GLOBAL && mode != TKEF_PER_TENSOR) return TKEF_EINVAL;
+  if (k < 0) return TKEF_ERANGE;
+  if (k > 0) {
+    if (mode != TKEF_GLOBAL) return TKEF_EINVAL;
+    if (k > d) return TKEF_ERANGE;
+  } else if (!(rho > 0.0 && rho <= 1.0) || !std::isfinite(rho)) {
+    return TKEF_ERANGE;
+  }
+  tkef_sparsify_plan p = new (std::nothrow) tkef_sparsify_plan_s();
+  if (!p) return TKEF_ENOMEM;
+  try {
+    p->ntensors = ntensors;
+    p->mode = mode;
+    p->d = d;
+    p->numels.assign(numels, numels + ntensors);
+    p->goff.resize(ntensors);
+    int64_t off = 0;
+    for (int32_t t = 0; t < ntensors; ++t) {
+      p->goff[t] = off;
+      off += numels[t];
+    }
+    p->ngroups = (mode == TKEF_GLOBAL) ? 1 : ntensors;
+    p->kgroup.assign(p->ngroups, 0);
+    if (mode == TKEF_GLOBAL) {
+      p->kgroup[0] = (k > 0) ? k : tkef_k_from_rho(d, rho);
+    } else {
+      for (int32_t t = 0; t < ntensors; ++t) p->kgroup[t] = tkef_k_from_rho(numels[t], rho);
+    }
+    p->k_total = 0;
+    for (int64_t kg : p->kgroup) p->k_total += kg;
+
+    // tiles: tensor-major, kTile elements each; lines per tile
+    int64_t line = 0;
+    p->groups.assign(p->ngroups, GroupDesc{0, 0, 0, 0});
+    int64_t out = 0;
+    for (int32_t t = 0; t < ntensors; ++t) {
+      const int32_t grp = (mode == TKEF_GLOBAL) ? 0 : t;
+      if (mode == TKEF_PER_TENSOR || t == 0) {
+        p->groups[grp].k = static_cast<uint32_t>(p->kgroup[grp]);
+        p->groups[grp].tile_begin = static_cast<uint32_t>(p->tiles.size());
+        p->groups[grp].out_base = static_cast<uint32_t>(out);
+        out += p->kgroup[grp];
+      }
+      for (int64_t s = 0; s < numels[t]; s += kTile) {
+        TileDesc td;
+        td.g = nullptr;
+        td.r = nullptr;
+        td.gstart = static_cast<int32_t>(p->goff[t] + s);
+        td.len = static_cast<int32_t>(std::min<int64_t>(kTile, numels[t] - s));
+        td.group = grp;
+        td.line0 = static_cast<int32_t>(line);
+        line += (td.len + kLine - 1) / kLine;
+        p->tiles.push_back(td);
+      }
+    }
+    p->ntiles = static_cast<int32_t>(p->tiles.size());
+    p->nlines = line;
+
+    // workspace layout (every region 256-B aligned)
+    size_t o = 0;
+    p->off_tiles = o;   o = align_up(o + p->tiles.size() * sizeof(TileDesc));
+    p->off_groups = o;  o = align_up(o + p->groups.size() * sizeof(GroupDesc));
+    p->off_state = o;   o = align_up(o + p->groups.size() * sizeof(GroupState));
+    p->off_hist1 = o;   o = align_up(o + (size_t)p->ngroups * kH1Bins * 4);
+    p->off_hist2 = o;   o = align_up(o + (size_t)p->ngroups * kH2Bins * 4);
+    p->off_hist3 = o;   o = align_up(o + (size_t)p->ngroups * kH3Bins * 4);
+    p->off_zero_end = o;
+    p->off_summ = o;    o = align_up(o + (size_t)p->nlines * sizeof(uint16_t));
+    p->off_cnt = o;     o = align_up(o + (size_t)p->ntiles * 8);
+    p->off_pglob = o;   o = align_up(o + (size_t)p->ntiles * 8);
+    p->off_prel = o;    o = align_up(o + (size_t)p->ntiles * 8);
+    p->ws_bytes = o;
+  } catch (const std::bad_alloc&) {
+    delete p;
+    return TKEF_ENOMEM;
+  }
+  *plan_out = p;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_sparsify_plan_destroy(tkef_sparsify_plan plan) {
+  delete plan;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_sparsify_plan_info(tkef_sparsify_plan plan, size_t* workspace_bytes,
+                                       int64_t* k_total, int64_t* d_total, int32_t* ngroups,
+                                       int32_t* nlaunch) {
+  if (!plan) return TKEF_EINVAL;
+  if (workspace_bytes) *workspace_bytes = plan->ws_bytes;
+  if (k_total) *k_total = plan->k_total;
+  if (d_total) *d_total = plan->d;
+  if (ngroups) *ngroups = plan->ngroups;
+  if (nlaunch) *nlaunch = kSparsifyNLaunch;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_sparsify_plan_group_k(tkef_sparsify_plan plan, int64_t* k_out, int32_t n) {
+  if (!plan || !k_out || n < plan->ngroups) return TKEF_EINVAL;
+  for (int32_t g = 0; g < plan->ngroups; ++g) k_out[g] = plan->kgroup[g];
+  return TKEF_OK;
+}
+
+extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* const* grads,
+                                       float* const* residuals, void* ws, size_t ws_bytes,
+                                       hipStream_t stream) {
+  if (!plan || !grads || !residuals) return TKEF_EINVAL;
+  if (!ws || !aligned_ws(ws) || ws_bytes < plan->ws_bytes) return TKEF_EWORKSPACE;
+  for (int32_t t = 0; t < plan->ntensors; ++t) {
+    const int64_t n = plan->numels[t];
+    if (n == 0) continue;
+    if (!grads[t] || !residuals[t]) return TKEF_EINVAL;
+    if (ranges_overlap(grads[t], residuals[t], n)) return TKEF_EINVAL;
+  }
+  size_t i = 0;
+  for (int32_t t = 0; t < plan->ntensors; ++t) {
+    for (int64_t s = 0; s < plan->numels[t]; s += kTile, ++i) {
+      plan->tiles[i].g = grads[t] + s;
+      plan->tiles[i].r = residuals[t] + s;
+    }
+  }
+  char* base = static_cast<char*>(ws);
+  hipError_t e = hipMemcpyAsync(base + plan->off_tiles, plan->tiles.data(),
+                                plan->tiles.size() * sizeof(TileDesc), hipMemcpyHostToDevice,
+                                stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(base + plan->off_groups, plan->groups.data(),
+                       plan->groups.size() * sizeof(GroupDesc), hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    plan->bound_ws = nullptr;
+    return TKEF_EHIP;
+  }
+  plan->bound_ws = ws;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_sparsify_plan_set_events(tkef_sparsify_plan plan, hipEvent_t* events,
+                                             int32_t n_events) {
+  if (!plan || n_events < 0 || (events && n_events == 0)) return TKEF_EINVAL;
+  plan->events = events;
+  plan->n_events = events ? n_events : 0;
+  return TKEF_OK;
+}
+
+extern "C" const char* tkef_sparsify_plan_launch_name(tkef_sparsify_plan plan, int32_t i) {
+  if (!plan || i < 0 || i >= kSparsifyNLaunch) return nullptr;
+  return kSparsifyLaunches[i];
+}
+
+extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t ws_bytes,
+                                     int32_t* idx_out, float* val_out, uint32_t* status,
+                                     hipStream_t s) {
+  if (!plan) return TKEF_EINVAL;
+  if (!ws || ws_bytes < plan->ws_bytes || !aligned_ws(ws)) return TKEF_EWORKSPACE;
+  if (plan->bound_ws != ws) return TKEF_ESTATE;
+  if (plan->k_total > 0 && (!idx_out || !val_out)) return TKEF_EINVAL;
+  char* base = static_cast<char*>(ws);
+  const TileDesc* tiles = reinterpret_cast<const TileDesc*>(base + plan->off_tiles);
+  const GroupDesc* groups = reinterpret_cast<const GroupDesc*>(base + plan->off_groups);
+  GroupState* st = reinterpret_cast<GroupState*>(base + plan->off_state);
+  uint32_t* hist1 = reinterpret_cast<uint32_t*>(base + plan->off_hist1);
+  uint32_t* hist2 = reinterpret_cast<uint32_t*>(base + plan->off_hist2);
+  uint32_t* hist3 = reinterpret_cast<uint32_t*>(base + plan->off_hist3);
+  uint16_t* summ = reinterpret_cast<uint16_t*>(base + plan->off_summ);
+  uint32_t* cnt = reinterpret_cast<uint32_t*>(base + plan->off_cnt);
+  uint32_t* pglob = reinterpret_cast<uint32_t*>(base + plan->off_pglob);
+  uint32_t* prel = reinterpret_cast<uint32_t*>(base + plan->off_prel);
+  const int32_t nt = plan->ntiles, ng = plan->ngroups;
+  const Tracer tr{plan->events, plan->n_events, s};
+  if (tr.ev && tr.n > 0) (void)hipEventRecord(tr.ev[0], s);
+
+  hipError_t e;
+  e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_state), 0u,
+                      (int64_t)((plan->off_zero_end - plan->off_state) / 4), s);
+  tr.mark(0);
+  if (e == hipSuccess) { e = launch_stream(tiles, nt, hist1, summ, status, s); tr.mark(1); }
+  if (e == hipSuccess) { e = launch_pick(1, groups, st, hist1, ng, s); tr.mark(2); }
+  if (e == hipSuccess) { e = launch_refine(2, tiles, nt, st, summ, hist2, s); tr.mark(3); }
+  if (e == hipSuccess) { e = launch_pick(2, groups, st, hist2, ng, s); tr.mark(4); }
+  if (e == hipSuccess) { e = launch_refine(3, tiles, nt, st, summ, hist3, s); tr.mark(5); }
+  if (e == hipSuccess) { e = launch_pick(3, groups, st, hist3, ng, s); tr.mark(6); }
+  if (e == hipSuccess) { e = launch_count(tiles, nt, st, summ, cnt, s); tr.mark(7); }
+  if (e == hipSuccess) { e = launch_scan(tiles, nt, groups, cnt, pglob, prel, s); tr.mark(8); }
+  if (e == hipSuccess) {
+    e = launch_emit(tiles, nt, groups, st, summ, prel, idx_out, val_out, s);
+    tr.mark(9);
+  }
+  return hip_rc(e);
+}
+
+extern "C" int tkef_sparsify_workspace(const int64_t* numels, int32_t ntensors, int32_t mode,
+                                       double rho, int64_t k, size_t* workspace_bytes,
+                                       int64_t* k_total) {
+  tkef_sparsify_plan p = nullptr;
+  int rc = tkef_sparsify_plan_create(numels, ntensors, mode, rho, k, &p);
+  if (rc) return rc;
+  rc = tkef_sparsify_plan_info(p, workspace_bytes, k_total, nullptr, nullptr, nullptr);
+  tkef_sparsify_plan_destroy(p);
+  return rc;
+}
+
+extern "C" int tkef_sparsify(const float* const* grads, float* const* residuals,
+                             const int64_t* numels, int32_t ntensors, int32_t mode, double rho,
+                             int64_t k, int32_t* idx_out, float* val_out, void* ws,
+                             size_t ws_bytes, uint32_t* status, hipStream_t stream) {
+  tkef_sparsify_plan p = nullptr;
+  int rc = tkef_sparsify_plan_create(numels, ntensors, mode, rho, k, &p);
+  if (rc) return rc;
+  rc = tkef_sparsify_plan_bind(p, grads, residuals, ws, ws_bytes, stream);
+  if (!rc) rc = tkef_sparsify_execute(p, ws, ws_bytes, idx_out, val_out, status, stream);
+  tkef_sparsify_plan_destroy(p);
+  return rc;
+}
+
+// ============================================================================
+// update plan
+
+static const char* const kUpdateLaunches[] = {"seg", "update"};
+constexpr int32_t kUpdateNLaunch = 2;
+
+struct tkef_update_plan_s {
+  int32_t ntensors = 0, P = 0, ntiles_u = 0;
+  int64_t d = 0, stride = 0;
+  std::vector<int64_t> numels, goff;
+  std::vector<UpdTensor> tens;
+  std::vector<int32_t> tile_first;
+  size_t off_tens = 0, off_first = 0, off_seg = 0, ws_bytes = 0;
+  void* bound_ws = nullptr;
+  bool has_mom = false;
+  hipEvent_t* events = nullptr;
+  int32_t n_events = 0;
+};
+
+extern "C" int tkef_update_plan_create(const int64_t* numels, int32_t ntensors, int32_t P,
+                                       int64_t stride, tkef_update_plan* plan_out) {
+  if (!plan_out) return TKEF_EINVAL;
+  *plan_out = nullptr;
+  int64_t d = 0;
+  int rc = check_numels(numels, ntensors, &d);
+  if (rc) return rc;
+  if (P < 1 || P > 65535) return TKEF_EINVAL;
+  if (stride < 0 || stride > kMaxD) return TKEF_ERANGE;
+  if ((int64_t)P * stride > (int64_t)1 << 40) return TKEF_ERANGE;
+  tkef_update_plan p = new (std::nothrow) tkef_update_plan_s();
+  if (!p) return TKEF_ENOMEM;
+  try {
+    p->ntensors = ntensors;
+    p->P = P;
+    p->d = d;
+    p->stride = stride;
+    p->numels.assign(numels, numels + ntensors);
+    p->goff.resize(ntensors);
+    int64_t off = 0;
+    for (int32_t t = 0; t < ntensors; ++t) {
+      p->goff[t] = off;
+      off += numels[t];
+    }
+    p->ntiles_u = static_cast<int32_t>((d + kUTile - 1) / kUTile);
+    // tile_first[u]: the tensor holding position u * kUTile; [ntiles_u] = T
+    p->tile_first.assign(p->ntiles_u + 1, ntensors);
+    int32_t t = 0;
+    for (int32_t u = 0; u < p->ntiles_u; ++u) {
+      const int64_t pos = (int64_t)u * kUTile;
+      while (t < ntensors && p->goff[t] + numels[t] <= pos) ++t;
+      p->tile_first[u] = t;
+    }
+    p->tens.resize(ntensors);
+    size_t o = 0;
+    p->off_tens = o;   o = align_up(o + p->tens.size() * sizeof(UpdTensor));
+    p->off_first = o;  o = align_up(o + p->tile_first.size() * sizeof(int32_t));
+    p->off_seg = o;    o = align_up(o + (size_t)P * (p->ntiles_u + 1) * sizeof(int32_t));
+    p->ws_bytes = o;
+  } catch (const std::bad_alloc&) {
+    delete p;
+    return TKEF_ENOMEM;
+  }
+  *plan_out = p;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_update_plan_destroy(tkef_update_plan plan) {
+  delete plan;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_update_plan_info(tkef_update_plan plan, size_t* workspace_bytes,
+                                     int64_t* d_total, int32_t* nlaunch) {
+  if (!plan) return TKEF_EINVAL;
+  if (workspace_bytes) *workspace_bytes = plan->ws_bytes;
+  if (d_total) *d_total = plan->d;
+  if (nlaunch) *nlaunch = kUpdateNLaunch;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_update_plan_bind(tkef_update_plan plan, float* const* params,
+                                     float* const* momentum, void* ws, size_t ws_bytes,
+                                     hipStream_t stream) {
+  if (!plan || !params) return TKEF_EINVAL;
+  if (!ws || !aligned_ws(ws) || ws_bytes < plan->ws_bytes) return TKEF_EWORKSPACE;
+  for (int32_t t = 0; t < plan->ntensors; ++t) {
+    const int64_t n = plan->numels[t];
+    if (n == 0) continue;
+    if (!params[t]) return TKEF_EINVAL;
+    if (momentum) {
+      if (!momentum[t]) return TKEF_EINVAL;
+      if (ranges_overlap(params[t], momentum[t], n)) return TKEF_EINVAL;
+    }
+  }
+  for (int32_t t = 0; t < plan->ntensors; ++t) {
+    plan->tens[t].w = params[t];
+    plan->tens[t].b = momentum ? momentum[t] : nullptr;
+    plan->tens[t].goff = plan->goff[t];
+    plan->tens[t].n = plan->numels[t];
+  }
+  char* base = static_cast<char*>(ws);
+  hipError_t e = hipMemcpyAsync(base + plan->off_tens, plan->tens.data(),
+                                plan->tens.size() * sizeof(UpdTensor), hipMemcpyHostToDevice,
+                                stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(base + plan->off_first, plan->tile_first.data(),
+                       plan->tile_first.size() * sizeof(int32_t), hipMemcpyHostToDevice,
+                       stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    plan->bound_ws = nullptr;
+    return TKEF_EHIP;
+  }
+  plan->bound_ws = ws;
+  plan->has_mom = momentum != nullptr;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_update_plan_set_events(tkef_update_plan plan, hipEvent_t* events,
+                                           int32_t n_events) {
+  if (!plan || n_events < 0 || (events && n_events == 0)) return TKEF_EINVAL;
+  plan->events = events;
+  plan->n_events = events ? n_events : 0;
+  return TKEF_OK;
+}
+
+extern "C" const char* tkef_update_plan_launch_name(tkef_update_plan plan, int32_t i) {
+  if (!plan || i < 0 || i >= kUpdateNLaunch) return nullptr;
+  return kUpdateLaunches[i];
+}
+
+extern "C" int tkef_update_execute(tkef_update_plan plan, const int32_t* idx, const float* val,
+                                   const int32_t* nnz, float lr, float mu, float wd, void* ws,
+                                   size_t ws_bytes, uint32_t* status, hipStream_t s) {
+  if (!plan) return TKEF_EINVAL;
+  if (!ws || ws_bytes < plan->ws_bytes || !aligned_ws(ws)) return TKEF_EWORKSPACE;
+  if (plan->bound_ws != ws) return TKEF_ESTATE;
+  if (plan->stride > 0 && (!idx || !val)) return TKEF_EINVAL;
+  if (!std::isfinite(lr) || !std::isfinite(mu) || !std::isfinite(wd)) return TKEF_ERANGE;
+  if (mu != 0.0f && !plan->has_mom) return TKEF_EINVAL;
+  char* base = static_cast<char*>(ws);
+  const UpdTensor* tens = reinterpret_cast<const UpdTensor*>(base + plan->off_tens);
+  const int32_t* first = reinterpret_cast<const int32_t*>(base + plan->off_first);
+  int32_t* seg = reinterpret_cast<int32_t*>(base + plan->off_seg);
+  const int sparse_mode = (mu == 0.0f && wd == 0.0f) ? 1 : 0;
+  const int has_mom = (mu != 0.0f) ? 1 : 0;
+  const Tracer tr{plan->events, plan->n_events, s};
+  if (tr.ev && tr.n > 0) (void)hipEventRecord(tr.ev[0], s);
+  hipError_t e = launch_seg(idx, plan->stride, nnz, plan->P, (int32_t)plan->d, plan->ntiles_u,
+                            seg, status, s);
+  tr.mark(0);
+  if (e == hipSuccess) {
+    e = launch_update(tens, first, plan->ntensors, (int32_t)plan->d, plan->ntiles_u, idx, val,
+                      plan->stride, nnz, plan->P, seg, lr, mu, wd, sparse_mode, has_mom, s);
+    tr.mark(1);
+  }
+  return hip_rc(e);
+}
+
+extern "C" int tkef_update_workspace(const int64_t* numels, int32_t ntensors, int32_t P,
+                                     int64_t stride, size_t* workspace_bytes) {
+  tkef_update_plan p = nullptr;
+  int rc = tkef_update_plan_create(numels, ntensors, P, stride, &p);
+  if (rc) return rc;
+  rc = tkef_update_plan_info(p, workspace_bytes, nullptr, nullptr);
+  tkef_update_plan_destroy(p);
+  return rc;
+}
+
+extern "C" int tkef_sparse_aggregate_update(float* const* params, float* const* momentum,
+                                            const int64_t* numels, int32_t ntensors,
+                                            const int32_t* idx, const float* val, int32_t P,
+                                            int64_t stride, const int32_t* nnz, float lr,
+                                            float mu, float wd, void* ws, size_t ws_bytes,
+                                            uint32_t* status, hipStream_t stream) {
+  tkef_update_plan p = nullptr;
+  int rc = tkef_update_plan_create(numels, ntensors, P, stride, &p);
+  if (rc) return rc;
+  rc = tkef_update_plan_bind(p, params, momentum, ws, ws_bytes, stream);
+  if (!rc) rc = tkef_update_execute(p, idx, val, nnz, lr, mu, wd, ws, ws_bytes, status, stream);
+  tkef_update_plan_destroy(p);
+  return rc;
+}

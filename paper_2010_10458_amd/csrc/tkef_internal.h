@@ -1,0 +1,96 @@
+// Internal layout shared by the host library and the gfx950 kernels.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+namespace tkef {
+
+// ---- sparsify tiling --------------------------------------------------------
+// A tile is up to kTile consecutive elements of one tensor; one workgroup of
+// kBlock threads streams it. A line is kLine consecutive elements (one 128-B
+// cache line of float32) and gets a 16-bit summary: the top 15 bits of the
+// largest magnitude key in it.
+constexpr int kBlock = 256;
+constexpr int kTile = 8192;
+constexpr int kLine = 32;
+constexpr int kLinesPerTile = kTile / kLine;  // == kBlock: one line per thread
+static_assert(kLinesPerTile == kBlock, "one summary line per thread");
+
+// Magnitude key = float bits with the sign cleared. The threshold search is a
+// three-level radix select on it: 11 bits, then 10, then 10.
+constexpr int kH1Bins = 2048, kH1Shift = 20;
+constexpr int kH2Bins = 1024, kH2Shift = 10;
+constexpr int kH3Bins = 1024;
+
+struct TileDesc {        // 32 B, one per tile, written at bind
+  const float* g;        // gradient, first element of the tile
+  float* r;              // residual, first element of the tile
+  int32_t gstart;        // global position of the first element
+  int32_t len;           // elements in the tile, 1..kTile
+  int32_t group;         // selection group
+  int32_t line0;         // first summary line of the tile
+};
+static_assert(sizeof(TileDesc) == 32, "TileDesc layout");
+
+struct GroupDesc {       // one per selection group, written at bind
+  uint32_t k;            // pairs the group selects
+  uint32_t tile_begin;   // first tile of the group
+  uint32_t out_base;     // first output slot of the group
+  uint32_t pad;
+};
+
+struct GroupState {      // per group, rewritten by every execution
+  uint32_t need;         // still to take from the current key class
+  uint32_t prefix;       // key bits fixed so far
+  uint32_t T;            // final threshold key
+  uint32_t n_eq;         // elements with key == T
+};
+
+// ---- update tiling ------------------------------------------------------------
+// Update tiles are aligned blocks of kUTile global positions; one workgroup
+// accumulates a tile's sparse contributions in LDS and then applies the SGD
+// step to the parameters (and momentum) of that range.
+constexpr int kUBlock = 256;
+constexpr int kUShift = 13;
+constexpr int kUTile = 1 << kUShift;  // 8192 positions, 32 KB of LDS
+
+struct UpdTensor {       // 32 B, one per parameter tensor, written at bind
+  float* w;
+  float* b;              // momentum buffer or null
+  int64_t goff;          // global position of element 0
+  int64_t n;
+};
+static_assert(sizeof(UpdTensor) == 32, "UpdTensor layout");
+
+// ---- kernel launchers (tkef_kernels.hip) --------------------------------------
+// Each returns the hipError_t of its launch.
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
+hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, uint32_t* hist1,
+                         uint16_t* summ, uint32_t* status, hipStream_t s);
+hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
+                       const uint32_t* hist, int32_t ngroups, hipStream_t s);
+hipError_t launch_refine(int level, const TileDesc* tiles, int32_t ntiles,
+                         const GroupState* st, const uint16_t* summ, uint32_t* hist,
+                         hipStream_t s);
+hipError_t launch_count(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
+                        const uint16_t* summ, uint32_t* tile_cnt, hipStream_t s);
+hipError_t launch_scan(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
+                       const uint32_t* tile_cnt, uint32_t* pre_glob, uint32_t* pre_rel,
+                       hipStream_t s);
+hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
+                       const GroupState* st, const uint16_t* summ, const uint32_t* pre_rel,
+                       int32_t* idx_out, float* val_out, hipStream_t s);
+
+hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, int32_t P,
+                      int32_t d, int32_t ntiles_u, int32_t* seg, uint32_t* status,
+                      hipStream_t s);
+hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32_t ntens,
+                         int32_t d, int32_t ntiles_u, const int32_t* idx, const float* val,
+                         int64_t stride, const int32_t* nnz, int32_t P, const int32_t* seg,
+                         float lr, float mu, float wd, int sparse_mode, int has_mom,
+                         hipStream_t s);
+
+}  // namespace tkef

@@ -1,0 +1,149 @@
+"""The C ABI library on the CPU: it loads, exports every function that
+include/tkef.h declares, and validates arguments on the host before any GPU
+work (no call here reaches the GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2010_10458_amd as tk
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tkef.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tkef_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported():
+    names = declared_functions()
+    assert len(names) >= 20
+    L = tk.lib()
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in tkef.h but not exported"
+
+
+def test_version_and_strerror():
+    L = tk.lib()
+    assert L.tkef_version() == 10000
+    for code in (0, -1, -2, -3, -4, -5, -6):
+        assert L.tkef_strerror(code)
+    assert b"unknown" in L.tkef_strerror(-99)
+
+
+@pytest.mark.parametrize("d,rho,k", [(1_048_576, 0.001, 1049), (25_557_032, 0.001, 25_558),
+                                     (109_708_544, 0.01, 1_097_086), (340_000_000, 0.001, 340_000),
+                                     (0, 0.5, 0), (5, 1.0, 5), (3, 1e-9, 1)])
+def test_k_from_rho(d, rho, k):
+    assert tk.k_from_rho(d, rho) == k
+
+
+@pytest.mark.parametrize("rho", [0.0, -0.1, 1.0000001, float("nan"), float("inf")])
+def test_k_from_rho_rejects(rho):
+    assert tk.k_from_rho(10, rho) == tk.ERANGE
+
+
+def _create(numels, mode=tk.GLOBAL, rho=0.01, k=0, n=None):
+    L = tk.lib()
+    h = ctypes.c_void_p()
+    arr = (ctypes.c_int64 * max(1, len(numels)))(*numels) if numels is not None else None
+    rc = L.tkef_sparsify_plan_create(arr, len(numels) if n is None else n, mode, rho, k,
+                                     ctypes.byref(h))
+    if rc == 0:
+        L.tkef_sparsify_plan_destroy(h)
+    return rc
+
+
+def test_sparsify_plan_validation():
+    assert _create([10, 20]) == tk.OK
+    assert _create(None, n=2) == tk.EINVAL
+    assert _create([10], n=0) == tk.EINVAL
+    assert _create([10, -1]) == tk.EINVAL
+    assert _create([0, 0]) == tk.ERANGE
+    assert _create([2**31 - 1]) == tk.OK
+    assert _create([2**31]) == tk.ERANGE
+    assert _create([2**30, 2**30]) == tk.ERANGE
+    assert _create([10], mode=7) == tk.EINVAL
+    assert _create([10], rho=0.0) == tk.ERANGE
+    assert _create([10], rho=2.0) == tk.ERANGE
+    assert _create([10], k=11, rho=0.0) == tk.ERANGE
+    assert _create([10], k=10, rho=0.0) == tk.OK
+    assert _create([10], k=-1) == tk.ERANGE
+    assert _create([10, 5], mode=tk.PER_TENSOR, k=3) == tk.EINVAL
+    L = tk.lib()
+    assert L.tkef_sparsify_plan_create(None, 1, 0, 0.1, 0, None) == tk.EINVAL
+
+
+def test_sparsify_plan_sizes():
+    p = tk.SparsifyPlan([100, 8192 * 3 + 1, 0, 7], rho=0.01)
+    assert p.k_total == tk.k_from_rho(100 + 8192 * 3 + 1 + 7, 0.01) and p.ngroups == 1
+    assert p.ws_bytes % 256 == 0 and p.ws_bytes > 0
+    q = tk.SparsifyPlan([100, 8192 * 3 + 1, 0, 7], mode=tk.PER_TENSOR, rho=0.01)
+    assert q.group_k() == [1, 246, 0, 1] and q.k_total == 248
+
+
+def test_bind_and_execute_validation_without_gpu():
+    L = tk.lib()
+    p = tk.SparsifyPlan([1000], rho=0.01)
+    h = p._h
+    P = ctypes.c_void_p
+    ptrs = (P * 1)(P(0x1000))
+    rptrs = (P * 1)(P(0x100000))
+    # workspace missing / misaligned / too small
+    assert L.tkef_sparsify_plan_bind(h, ptrs, rptrs, None, 10**9, None) == tk.EWORKSPACE
+    assert L.tkef_sparsify_plan_bind(h, ptrs, rptrs, P(0x10010), 10**9, None) == tk.EWORKSPACE
+    assert L.tkef_sparsify_plan_bind(h, ptrs, rptrs, P(0x10000), 1, None) == tk.EWORKSPACE
+    # null tensor pointers, overlapping g and r
+    nul = (P * 1)(None)
+    assert L.tkef_sparsify_plan_bind(h, nul, rptrs, P(0x10000), 10**9, None) == tk.EINVAL
+    same = (P * 1)(P(0x1000 + 64))
+    assert L.tkef_sparsify_plan_bind(h, ptrs, same, P(0x10000), 10**9, None) == tk.EINVAL
+    assert L.tkef_sparsify_plan_bind(None, ptrs, rptrs, P(0x10000), 10**9, None) == tk.EINVAL
+    # execute before bind
+    assert L.tkef_sparsify_execute(h, P(0x10000), 10**9, P(0x2000), P(0x3000), None,
+                                   None) == tk.ESTATE
+    assert L.tkef_sparsify_execute(h, None, 10**9, P(0x2000), P(0x3000), None,
+                                   None) == tk.EWORKSPACE
+    assert L.tkef_sparsify_plan_set_events(h, None, 0) == tk.OK
+    assert L.tkef_sparsify_plan_set_events(h, None, -1) == tk.EINVAL
+    assert L.tkef_sparsify_plan_launch_name(h, 99) is None
+
+
+def test_update_plan_validation():
+    L = tk.lib()
+
+    def create(numels, P, stride):
+        h = ctypes.c_void_p()
+        arr = (ctypes.c_int64 * len(numels))(*numels)
+        rc = L.tkef_update_plan_create(arr, len(numels), P, stride, ctypes.byref(h))
+        if rc == 0:
+            L.tkef_update_plan_destroy(h)
+        return rc
+
+    assert create([10, 20], 1, 5) == tk.OK
+    assert create([10, 20], 0, 5) == tk.EINVAL
+    assert create([10, 20], 65536, 5) == tk.EINVAL
+    assert create([10, 20], 4, -1) == tk.ERANGE
+    assert create([10, 20], 4, 2**31) == tk.ERANGE
+    assert create([0], 4, 5) == tk.ERANGE
+    u = tk.UpdatePlan([10, 20], P=3, stride=4)
+    P = ctypes.c_void_p
+    w = (P * 2)(P(0x1000), P(0x2000))
+    b = (P * 2)(P(0x1000 + 8), P(0x3000))
+    assert L.tkef_update_plan_bind(u._h, w, b, P(0x10000), 10**9, None) == tk.EINVAL
+    assert L.tkef_update_plan_bind(u._h, None, None, P(0x10000), 10**9, None) == tk.EINVAL
+    assert L.tkef_update_plan_bind(u._h, w, None, P(0x10001), 10**9, None) == tk.EWORKSPACE
+    assert L.tkef_update_execute(u._h, P(0x10), P(0x20), None, 0.1, 0.0, 0.0, P(0x10000),
+                                 10**9, None, None) == tk.ESTATE
+
+
+def test_no_cpu_fallback_when_library_missing(tmp_path, monkeypatch):
+    """The binding raises instead of computing anything itself."""
+    monkeypatch.setattr(tk, "_lib", None)
+    monkeypatch.setattr(tk, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError):
+        tk.lib()
