@@ -48,7 +48,24 @@ def parse_args():
                     help="skip timing the CPU oracle")
     ap.add_argument("--kernel-events", type=int, default=1,
                     help="record HIP events around every kernel (1) or only per phase (0)")
+    ap.add_argument("--probe-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain elementwise copy of MIB MiB five times (the "
+                         "reference kernel for scaling HBM counter readings) and exit")
     return ap.parse_args()
+
+
+def probe_copy(mib: int) -> int:
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"probe_copy_bytes_read": n * 4, "probe_copy_bytes_written": n * 4,
+                      "launches": 5}), flush=True)
+    return 0
 
 
 def log(msg: str) -> None:
@@ -114,6 +131,8 @@ def cpu_baseline(sizes, d):
 
 def main() -> int:
     args = parse_args()
+    if args.probe_copy:
+        return probe_copy(args.probe_copy)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (this build has no multi-GPU path); "
               f"got --gpus {args.gpus}", file=sys.stderr)
