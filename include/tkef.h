@@ -52,6 +52,7 @@ extern "C" {
 #define TKEF_STATUS_NAN 1u         /* sparsify saw a NaN in g + r */
 #define TKEF_STATUS_UNSORTED 2u    /* an update index list is not ascending */
 #define TKEF_STATUS_INDEX_RANGE 4u /* an update index lies outside [0, d) */
+#define TKEF_STATUS_TIMEOUT 8u     /* a bounded wait between workgroups gave up (results invalid) */
 
 int tkef_version(void);
 const char *tkef_strerror(int code);

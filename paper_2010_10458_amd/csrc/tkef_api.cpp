@@ -1,6 +1,7 @@
 // Host side of the tkef C ABI: argument validation, plans, workspace layout
 // and the launch sequence. No device memory is allocated here; every device
 // buffer is the caller's.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -91,20 +92,26 @@ extern "C" int64_t tkef_k_from_rho(int64_t d, double rho) {
 // ============================================================================
 // sparsify plan
 
-static const char* const kSparsifyLaunches[] = {
-    "fill", "stream", "pick1", "refine2", "pick2", "refine3", "pick3",
-    "count", "scan", "emit"};
-constexpr int32_t kSparsifyNLaunch = 10;
+// Launch sequences: one selection group (global) and several (per tensor).
+static const char* const kSparsifyLaunchesOne[] = {"fill",   "stream", "pick1",
+                                                   "gather", "hist3",  "emit"};
+static const char* const kSparsifyLaunchesMany[] = {"fill",  "stream", "pick1",
+                                                    "gather", "pick2", "hist3",
+                                                    "pick3", "groupscan", "emit"};
+constexpr int32_t kSparsifyNLaunchOne = 6, kSparsifyNLaunchMany = 9;
 
 struct tkef_sparsify_plan_s {
-  int32_t ntensors = 0, mode = 0, ngroups = 0, ntiles = 0;
+  int32_t ntensors = 0, mode = 0, ngroups = 0, ntiles = 0, nslots = 1, stream_grid = 1;
   int64_t d = 0, k_total = 0, nlines = 0;
   std::vector<int64_t> numels, goff, kgroup;
   std::vector<TileDesc> tiles;   // pointers filled at bind
   std::vector<GroupDesc> groups;
+  uint32_t cand_cap = 0;  // capacity of the compacted candidate list
+  int32_t sel_lpt = 1, sel_grid = 1;  // selection kernels: lines per thread, workgroups
   size_t off_tiles = 0, off_groups = 0, off_state = 0, off_hist1 = 0, off_hist2 = 0,
-         off_hist3 = 0, off_zero_end = 0, off_summ = 0, off_cnt = 0, off_pglob = 0,
-         off_prel = 0, ws_bytes = 0;
+         off_hist3 = 0, off_flags1 = 0, off_flags2 = 0, off_meta = 0, off_zero_end = 0,
+         off_summ = 0, off_base = 0, off_cand = 0, ws_bytes = 0;
+  int32_t nlaunch() const { return ngroups == 1 ? kSparsifyNLaunchOne : kSparsifyNLaunchMany; }
   void* bound_ws = nullptr;
   hipEvent_t* events = nullptr;
   int32_t n_events = 0;
@@ -148,8 +155,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     p->k_total = 0;
     for (int64_t kg : p->kgroup) p->k_total += kg;
 
-    // tiles: tensor-major, kTile elements each; lines per tile
-    int64_t line = 0;
+    // tiles: tensor-major, kTile elements each
     p->groups.assign(p->ngroups, GroupDesc{0, 0, 0, 0});
     int64_t out = 0;
     for (int32_t t = 0; t < ntensors; ++t) {
@@ -167,27 +173,48 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
         td.gstart = static_cast<int32_t>(p->goff[t] + s);
         td.len = static_cast<int32_t>(std::min<int64_t>(kTile, numels[t] - s));
         td.group = grp;
-        td.line0 = static_cast<int32_t>(line);
-        line += (td.len + kLine - 1) / kLine;
+        td.reserved = 0;
         p->tiles.push_back(td);
       }
     }
     p->ntiles = static_cast<int32_t>(p->tiles.size());
-    p->nlines = line;
+    p->nlines = (int64_t)p->ntiles * kLinesPerTile;
+    // Candidates are the positions at or above the level-1 threshold bin:
+    // about k plus one bin's worth. Four times k plus a margin covers that
+    // for ordinary data; heavier inputs fall back to re-reading lines.
+    p->cand_cap = (uint32_t)std::min<int64_t>(d, 4 * p->k_total + 65536);
+    // selection kernels: `lpt` consecutive summary lines per thread, at most
+    // select_max_groups() workgroups of select_block() threads; enough
+    // workgroups that a candidate run per thread stays short
+    // Aim for about 256 workgroups (one per compute unit, so all are resident
+    // at once) with at least two lines per thread.
+    const int64_t sb = select_block(), sg = select_max_groups();
+    int64_t lpt = std::max<int64_t>(2, (p->nlines + sb * 256 - 1) / (sb * 256));
+    lpt = std::min<int64_t>(lpt, select_max_lpt());
+    if ((p->nlines + sb * lpt - 1) / (sb * lpt) > sg) throw std::bad_alloc();  // d < 2^31
+    p->sel_lpt = (int32_t)lpt;
+    const int64_t g_lines = (p->nlines + sb * lpt - 1) / (sb * lpt);
+    const int64_t g_cands = std::min<int64_t>(sg, ((int64_t)p->cand_cap + sb * 4 - 1) / (sb * 4));
+    p->sel_grid = (int32_t)std::max<int64_t>(1, std::max(g_lines, g_cands));
+    // level-1 histogram copies per group: many for one global selection (all
+    // workgroups add into it), a few per tensor in per-tensor mode
+    p->nslots = (p->ngroups == 1) ? 16 : 4;
 
     // workspace layout (every region 256-B aligned)
     size_t o = 0;
     p->off_tiles = o;   o = align_up(o + p->tiles.size() * sizeof(TileDesc));
     p->off_groups = o;  o = align_up(o + p->groups.size() * sizeof(GroupDesc));
     p->off_state = o;   o = align_up(o + p->groups.size() * sizeof(GroupState));
-    p->off_hist1 = o;   o = align_up(o + (size_t)p->ngroups * kH1Bins * 4);
+    p->off_hist1 = o;   o = align_up(o + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
     p->off_hist2 = o;   o = align_up(o + (size_t)p->ngroups * kH2Bins * 4);
     p->off_hist3 = o;   o = align_up(o + (size_t)p->ngroups * kH3Bins * 4);
+    p->off_flags1 = o;  o = align_up(o + (size_t)p->sel_grid * 8);
+    p->off_flags2 = o;  o = align_up(o + (size_t)p->sel_grid * 8);
+    p->off_meta = o;    o = align_up(o + 8);
     p->off_zero_end = o;
     p->off_summ = o;    o = align_up(o + (size_t)p->nlines * sizeof(uint16_t));
-    p->off_cnt = o;     o = align_up(o + (size_t)p->ntiles * 8);
-    p->off_pglob = o;   o = align_up(o + (size_t)p->ntiles * 8);
-    p->off_prel = o;    o = align_up(o + (size_t)p->ntiles * 8);
+    p->off_base = o;    o = align_up(o + (size_t)p->ngroups * 8);
+    p->off_cand = o;    o = align_up(o + (size_t)p->cand_cap * 4);
     p->ws_bytes = o;
   } catch (const std::bad_alloc&) {
     delete p;
@@ -210,7 +237,7 @@ extern "C" int tkef_sparsify_plan_info(tkef_sparsify_plan plan, size_t* workspac
   if (k_total) *k_total = plan->k_total;
   if (d_total) *d_total = plan->d;
   if (ngroups) *ngroups = plan->ngroups;
-  if (nlaunch) *nlaunch = kSparsifyNLaunch;
+  if (nlaunch) *nlaunch = plan->nlaunch();
   return TKEF_OK;
 }
 
@@ -238,6 +265,14 @@ extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* con
       plan->tiles[i].r = residuals[t] + s;
     }
   }
+  // persistent stream grid: four workgroups per compute unit
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return TKEF_EHIP;
+  const int64_t units = (int64_t)plan->ntiles * (kTile / 2048);
+  plan->stream_grid = (int32_t)std::min<int64_t>((int64_t)4 * cus, units);
   char* base = static_cast<char*>(ws);
   hipError_t e = hipMemcpyAsync(base + plan->off_tiles, plan->tiles.data(),
                                 plan->tiles.size() * sizeof(TileDesc), hipMemcpyHostToDevice,
@@ -263,8 +298,8 @@ extern "C" int tkef_sparsify_plan_set_events(tkef_sparsify_plan plan, hipEvent_t
 }
 
 extern "C" const char* tkef_sparsify_plan_launch_name(tkef_sparsify_plan plan, int32_t i) {
-  if (!plan || i < 0 || i >= kSparsifyNLaunch) return nullptr;
-  return kSparsifyLaunches[i];
+  if (!plan || i < 0 || i >= plan->nlaunch()) return nullptr;
+  return plan->ngroups == 1 ? kSparsifyLaunchesOne[i] : kSparsifyLaunchesMany[i];
 }
 
 extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t ws_bytes,
@@ -282,28 +317,54 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   uint32_t* hist2 = reinterpret_cast<uint32_t*>(base + plan->off_hist2);
   uint32_t* hist3 = reinterpret_cast<uint32_t*>(base + plan->off_hist3);
   uint16_t* summ = reinterpret_cast<uint16_t*>(base + plan->off_summ);
-  uint32_t* cnt = reinterpret_cast<uint32_t*>(base + plan->off_cnt);
-  uint32_t* pglob = reinterpret_cast<uint32_t*>(base + plan->off_pglob);
-  uint32_t* prel = reinterpret_cast<uint32_t*>(base + plan->off_prel);
+  uint64_t* flags1 = reinterpret_cast<uint64_t*>(base + plan->off_flags1);
+  uint64_t* flags2 = reinterpret_cast<uint64_t*>(base + plan->off_flags2);
+  uint32_t* meta = reinterpret_cast<uint32_t*>(base + plan->off_meta);
+  uint32_t* gbase = reinterpret_cast<uint32_t*>(base + plan->off_base);
+  int32_t* cand = reinterpret_cast<int32_t*>(base + plan->off_cand);
   const int32_t nt = plan->ntiles, ng = plan->ngroups;
+  const int single = (ng == 1) ? 1 : 0;
+  const int64_t nl = plan->nlines;
+  const int lpt = plan->sel_lpt, sg = plan->sel_grid;
   const Tracer tr{plan->events, plan->n_events, s};
   if (tr.ev && tr.n > 0) (void)hipEventRecord(tr.ev[0], s);
+  int li = 0;  // launch index, for the timing hook
 
   hipError_t e;
   e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_state), 0u,
                       (int64_t)((plan->off_zero_end - plan->off_state) / 4), s);
-  tr.mark(0);
-  if (e == hipSuccess) { e = launch_stream(tiles, nt, hist1, summ, status, s); tr.mark(1); }
-  if (e == hipSuccess) { e = launch_pick(1, groups, st, hist1, ng, s); tr.mark(2); }
-  if (e == hipSuccess) { e = launch_refine(2, tiles, nt, st, summ, hist2, s); tr.mark(3); }
-  if (e == hipSuccess) { e = launch_pick(2, groups, st, hist2, ng, s); tr.mark(4); }
-  if (e == hipSuccess) { e = launch_refine(3, tiles, nt, st, summ, hist3, s); tr.mark(5); }
-  if (e == hipSuccess) { e = launch_pick(3, groups, st, hist3, ng, s); tr.mark(6); }
-  if (e == hipSuccess) { e = launch_count(tiles, nt, st, summ, cnt, s); tr.mark(7); }
-  if (e == hipSuccess) { e = launch_scan(tiles, nt, groups, cnt, pglob, prel, s); tr.mark(8); }
+  tr.mark(li++);
   if (e == hipSuccess) {
-    e = launch_emit(tiles, nt, groups, st, summ, prel, idx_out, val_out, s);
-    tr.mark(9);
+    e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s);
+    tr.mark(li++);
+  }
+  if (e == hipSuccess) {
+    e = launch_pick(1, groups, st, hist1, plan->nslots, ng, s);
+    tr.mark(li++);
+  }
+  if (e == hipSuccess) {
+    e = launch_gather(tiles, st, single, summ, nl, lpt, sg, hist2, flags1, cand, plan->cand_cap,
+                      meta, status, s);
+    tr.mark(li++);
+  }
+  if (e == hipSuccess && !single) {
+    e = launch_pick(2, groups, st, hist2, 1, ng, s);
+    tr.mark(li++);
+  }
+  if (e == hipSuccess) {
+    e = launch_hist3(tiles, nt, st, single, summ, nl, lpt, sg, hist2, cand, meta, hist3, s);
+    tr.mark(li++);
+  }
+  if (e == hipSuccess && !single) {
+    e = launch_pick(3, groups, st, hist3, 1, ng, s);
+    tr.mark(li++);
+    if (e == hipSuccess) e = launch_groupscan(groups, st, ng, gbase, s);
+    tr.mark(li++);
+  }
+  if (e == hipSuccess) {
+    e = launch_emit(tiles, nt, groups, st, single, summ, nl, lpt, sg, hist2, hist3, cand, meta,
+                    gbase, flags2, idx_out, val_out, status, s);
+    tr.mark(li++);
   }
   return hip_rc(e);
 }

@@ -9,10 +9,10 @@
 namespace tkef {
 
 // ---- sparsify tiling --------------------------------------------------------
-// A tile is up to kTile consecutive elements of one tensor; one workgroup of
-// kBlock threads streams it. A line is kLine consecutive elements (one 128-B
-// cache line of float32) and gets a 16-bit summary: the top 15 bits of the
-// largest magnitude key in it.
+// A tile is up to kTile consecutive elements of one tensor. A line is kLine
+// consecutive elements (one 128-B cache line of float32) and gets a 16-bit
+// summary: the top 15 bits of the largest magnitude key in it. Tile i owns
+// summary entries [i * kLinesPerTile, (i + 1) * kLinesPerTile).
 constexpr int kBlock = 256;
 constexpr int kTile = 8192;
 constexpr int kLine = 32;
@@ -31,7 +31,7 @@ struct TileDesc {        // 32 B, one per tile, written at bind
   int32_t gstart;        // global position of the first element
   int32_t len;           // elements in the tile, 1..kTile
   int32_t group;         // selection group
-  int32_t line0;         // first summary line of the tile
+  int32_t reserved;
 };
 static_assert(sizeof(TileDesc) == 32, "TileDesc layout");
 
@@ -54,8 +54,8 @@ struct GroupState {      // per group, rewritten by every execution
 // accumulates a tile's sparse contributions in LDS and then applies the SGD
 // step to the parameters (and momentum) of that range.
 constexpr int kUBlock = 256;
-constexpr int kUShift = 13;
-constexpr int kUTile = 1 << kUShift;  // 8192 positions, 32 KB of LDS
+constexpr int kUShift = 12;
+constexpr int kUTile = 1 << kUShift;  // 4096 positions, 16 KB of LDS
 
 struct UpdTensor {       // 32 B, one per parameter tensor, written at bind
   float* w;
@@ -68,21 +68,30 @@ static_assert(sizeof(UpdTensor) == 32, "UpdTensor layout");
 // ---- kernel launchers (tkef_kernels.hip) --------------------------------------
 // Each returns the hipError_t of its launch.
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
-hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, uint32_t* hist1,
-                         uint16_t* summ, uint32_t* status, hipStream_t s);
+hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, uint32_t* hist1,
+                         int32_t nslots, uint16_t* summ, uint32_t* status, hipStream_t s);
 hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
-                       const uint32_t* hist, int32_t ngroups, hipStream_t s);
-hipError_t launch_refine(int level, const TileDesc* tiles, int32_t ntiles,
-                         const GroupState* st, const uint16_t* summ, uint32_t* hist,
-                         hipStream_t s);
-hipError_t launch_count(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
-                        const uint16_t* summ, uint32_t* tile_cnt, hipStream_t s);
-hipError_t launch_scan(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
-                       const uint32_t* tile_cnt, uint32_t* pre_glob, uint32_t* pre_rel,
-                       hipStream_t s);
+                       const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s);
+hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, int single,
+                         const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
+                         uint32_t* hist2, uint64_t* flags, int32_t* cand, uint32_t cap,
+                         uint32_t* meta, uint32_t* status, hipStream_t s);
+hipError_t launch_hist3(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
+                        int single, const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
+                        const uint32_t* hist2, const int32_t* cand, const uint32_t* meta,
+                        uint32_t* hist3, hipStream_t s);
+hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32_t ngroups,
+                            uint32_t* base, hipStream_t s);
 hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
-                       const GroupState* st, const uint16_t* summ, const uint32_t* pre_rel,
-                       int32_t* idx_out, float* val_out, hipStream_t s);
+                       const GroupState* st, int single, const uint16_t* summ, int64_t nlines,
+                       int lpt, int32_t grid, const uint32_t* hist2, const uint32_t* hist3,
+                       const int32_t* cand, const uint32_t* meta, const uint32_t* base,
+                       uint64_t* flags, int32_t* idx_out, float* val_out, uint32_t* status,
+                       hipStream_t s);
+// launch-shape limits of the selection kernels
+int32_t select_max_groups();
+int32_t select_block();
+int32_t select_max_lpt();
 
 hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, int32_t P,
                       int32_t d, int32_t ntiles_u, int32_t* seg, uint32_t* status,
