@@ -93,12 +93,11 @@ extern "C" int64_t tkef_k_from_rho(int64_t d, double rho) {
 // sparsify plan
 
 // Launch sequences: one selection group (global) and several (per tensor).
-static const char* const kSparsifyLaunchesOne[] = {"fill",   "stream", "pick1",
-                                                   "gather", "hist3",  "emit"};
-static const char* const kSparsifyLaunchesMany[] = {"fill",  "stream", "pick1",
-                                                    "gather", "pick2", "hist3",
-                                                    "pick3", "groupscan", "emit"};
-constexpr int32_t kSparsifyNLaunchOne = 6, kSparsifyNLaunchMany = 9;
+static const char* const kSparsifyLaunchesOne[] = {"stream", "gather", "hist3", "emit"};
+static const char* const kSparsifyLaunchesMany[] = {"stream", "pick1", "gather",
+                                                    "pick2",  "hist3", "pick3",
+                                                    "groupscan", "emit"};
+constexpr int32_t kSparsifyNLaunchOne = 4, kSparsifyNLaunchMany = 8;
 
 struct tkef_sparsify_plan_s {
   int32_t ntensors = 0, mode = 0, ngroups = 0, ntiles = 0, nslots = 1, stream_grid = 1;
@@ -108,9 +107,15 @@ struct tkef_sparsify_plan_s {
   std::vector<GroupDesc> groups;
   uint32_t cand_cap = 0;  // capacity of the compacted candidate list
   int32_t sel_lpt = 1, sel_grid = 1;  // selection kernels: lines per thread, workgroups
-  size_t off_tiles = 0, off_groups = 0, off_state = 0, off_hist1 = 0, off_hist2 = 0,
-         off_hist3 = 0, off_flags1 = 0, off_flags2 = 0, off_meta = 0, off_zero_end = 0,
-         off_summ = 0, off_base = 0, off_cand = 0, ws_bytes = 0;
+  // Scratch that must start at zero (histograms, prefix flags, overflow and
+  // count words) exists twice; execution n uses copy n % 2 and its last kernel
+  // clears the other copy for execution n + 1. Offsets below are relative to
+  // the start of a copy, which lies at off_zero[0] or off_zero[1].
+  size_t off_tiles = 0, off_groups = 0, off_state = 0, off_zero[2] = {0, 0}, zero_bytes = 0,
+         off_hist1 = 0, off_hist2 = 0, off_hist3 = 0, off_flags1 = 0, off_flags2 = 0,
+         off_meta = 0, off_summ = 0, off_base = 0, off_cand = 0, ws_bytes = 0;
+  uint64_t executions = 0;   // since the last bind
+  bool needs_clear = true;   // both copies must be cleared before the next run
   int32_t nlaunch() const { return ngroups == 1 ? kSparsifyNLaunchOne : kSparsifyNLaunchMany; }
   void* bound_ws = nullptr;
   hipEvent_t* events = nullptr;
@@ -205,13 +210,16 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     p->off_tiles = o;   o = align_up(o + p->tiles.size() * sizeof(TileDesc));
     p->off_groups = o;  o = align_up(o + p->groups.size() * sizeof(GroupDesc));
     p->off_state = o;   o = align_up(o + p->groups.size() * sizeof(GroupState));
-    p->off_hist1 = o;   o = align_up(o + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
-    p->off_hist2 = o;   o = align_up(o + (size_t)p->ngroups * kH2Bins * 4);
-    p->off_hist3 = o;   o = align_up(o + (size_t)p->ngroups * kH3Bins * 4);
-    p->off_flags1 = o;  o = align_up(o + (size_t)p->sel_grid * 8);
-    p->off_flags2 = o;  o = align_up(o + (size_t)p->sel_grid * 8);
-    p->off_meta = o;    o = align_up(o + 8);
-    p->off_zero_end = o;
+    size_t z = 0;
+    p->off_hist1 = z;   z = align_up(z + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
+    p->off_hist2 = z;   z = align_up(z + (size_t)p->ngroups * kH2Bins * 4);
+    p->off_hist3 = z;   z = align_up(z + (size_t)p->ngroups * kH3Bins * 4);
+    p->off_flags1 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
+    p->off_flags2 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
+    p->off_meta = z;    z = align_up(z + 8);
+    p->zero_bytes = z;
+    p->off_zero[0] = o; o = align_up(o + z);
+    p->off_zero[1] = o; o = align_up(o + z);
     p->off_summ = o;    o = align_up(o + (size_t)p->nlines * sizeof(uint16_t));
     p->off_base = o;    o = align_up(o + (size_t)p->ngroups * 8);
     p->off_cand = o;    o = align_up(o + (size_t)p->cand_cap * 4);
@@ -280,12 +288,19 @@ extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* con
   if (e == hipSuccess)
     e = hipMemcpyAsync(base + plan->off_groups, plan->groups.data(),
                        plan->groups.size() * sizeof(GroupDesc), hipMemcpyHostToDevice, stream);
+  // both copies of the zero-initialised scratch start cleared
+  if (e == hipSuccess)
+    e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_zero[0]), 0u,
+                        (int64_t)((plan->off_zero[1] + plan->zero_bytes - plan->off_zero[0]) / 4),
+                        stream);
   if (e == hipSuccess) e = hipStreamSynchronize(stream);
   if (e != hipSuccess) {
     plan->bound_ws = nullptr;
     return TKEF_EHIP;
   }
   plan->bound_ws = ws;
+  plan->executions = 0;
+  plan->needs_clear = false;
   return TKEF_OK;
 }
 
@@ -313,13 +328,16 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   const TileDesc* tiles = reinterpret_cast<const TileDesc*>(base + plan->off_tiles);
   const GroupDesc* groups = reinterpret_cast<const GroupDesc*>(base + plan->off_groups);
   GroupState* st = reinterpret_cast<GroupState*>(base + plan->off_state);
-  uint32_t* hist1 = reinterpret_cast<uint32_t*>(base + plan->off_hist1);
-  uint32_t* hist2 = reinterpret_cast<uint32_t*>(base + plan->off_hist2);
-  uint32_t* hist3 = reinterpret_cast<uint32_t*>(base + plan->off_hist3);
+  const int par = (int)(plan->executions & 1u);
+  char* zb = base + plan->off_zero[par];           // this execution's cleared scratch
+  char* zn = base + plan->off_zero[par ^ 1];       // cleared for the next execution
+  uint32_t* hist1 = reinterpret_cast<uint32_t*>(zb + plan->off_hist1);
+  uint32_t* hist2 = reinterpret_cast<uint32_t*>(zb + plan->off_hist2);
+  uint32_t* hist3 = reinterpret_cast<uint32_t*>(zb + plan->off_hist3);
   uint16_t* summ = reinterpret_cast<uint16_t*>(base + plan->off_summ);
-  uint64_t* flags1 = reinterpret_cast<uint64_t*>(base + plan->off_flags1);
-  uint64_t* flags2 = reinterpret_cast<uint64_t*>(base + plan->off_flags2);
-  uint32_t* meta = reinterpret_cast<uint32_t*>(base + plan->off_meta);
+  uint64_t* flags1 = reinterpret_cast<uint64_t*>(zb + plan->off_flags1);
+  uint64_t* flags2 = reinterpret_cast<uint64_t*>(zb + plan->off_flags2);
+  uint32_t* meta = reinterpret_cast<uint32_t*>(zb + plan->off_meta);
   uint32_t* gbase = reinterpret_cast<uint32_t*>(base + plan->off_base);
   int32_t* cand = reinterpret_cast<int32_t*>(base + plan->off_cand);
   const int32_t nt = plan->ntiles, ng = plan->ngroups;
@@ -327,24 +345,26 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   const int64_t nl = plan->nlines;
   const int lpt = plan->sel_lpt, sg = plan->sel_grid;
   const Tracer tr{plan->events, plan->n_events, s};
-  if (tr.ev && tr.n > 0) (void)hipEventRecord(tr.ev[0], s);
   int li = 0;  // launch index, for the timing hook
 
-  hipError_t e;
-  e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_state), 0u,
-                      (int64_t)((plan->off_zero_end - plan->off_state) / 4), s);
-  tr.mark(li++);
-  if (e == hipSuccess) {
-    e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s);
-    tr.mark(li++);
+  hipError_t e = hipSuccess;
+  if (plan->needs_clear) {  // after a failed run
+    e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_zero[0]), 0u,
+                        (int64_t)((plan->off_zero[1] + plan->zero_bytes - plan->off_zero[0]) / 4),
+                        s);
+    if (e != hipSuccess) return TKEF_EHIP;
+    plan->needs_clear = false;
   }
-  if (e == hipSuccess) {
+  if (tr.ev && tr.n > 0) (void)hipEventRecord(tr.ev[0], s);
+  e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s);
+  tr.mark(li++);
+  if (e == hipSuccess && !single) {
     e = launch_pick(1, groups, st, hist1, plan->nslots, ng, s);
     tr.mark(li++);
   }
   if (e == hipSuccess) {
-    e = launch_gather(tiles, st, single, summ, nl, lpt, sg, hist2, flags1, cand, plan->cand_cap,
-                      meta, status, s);
+    e = launch_gather(tiles, groups, st, hist1, plan->nslots, single, summ, nl, lpt, sg, hist2,
+                      flags1, cand, plan->cand_cap, meta, status, s);
     tr.mark(li++);
   }
   if (e == hipSuccess && !single) {
@@ -363,9 +383,15 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   }
   if (e == hipSuccess) {
     e = launch_emit(tiles, nt, groups, st, single, summ, nl, lpt, sg, hist2, hist3, cand, meta,
-                    gbase, flags2, idx_out, val_out, status, s);
+                    gbase, flags2, idx_out, val_out, status,
+                    reinterpret_cast<uint32_t*>(zn), (int64_t)(plan->zero_bytes / 4), s);
     tr.mark(li++);
   }
+  if (e != hipSuccess) {
+    plan->needs_clear = true;
+    return TKEF_EHIP;
+  }
+  plan->executions++;
   return hip_rc(e);
 }
 

@@ -72,10 +72,11 @@ hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, ui
                          int32_t nslots, uint16_t* summ, uint32_t* status, hipStream_t s);
 hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
                        const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s);
-hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, int single,
-                         const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
-                         uint32_t* hist2, uint64_t* flags, int32_t* cand, uint32_t cap,
-                         uint32_t* meta, uint32_t* status, hipStream_t s);
+hipError_t launch_gather(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
+                         const uint32_t* hist1, int nslots, int single, const uint16_t* summ,
+                         int64_t nlines, int lpt, int32_t grid, uint32_t* hist2,
+                         uint64_t* flags, int32_t* cand, uint32_t cap, uint32_t* meta,
+                         uint32_t* status, hipStream_t s);
 hipError_t launch_hist3(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
                         int single, const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
                         const uint32_t* hist2, const int32_t* cand, const uint32_t* meta,
@@ -87,7 +88,7 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
                        int lpt, int32_t grid, const uint32_t* hist2, const uint32_t* hist3,
                        const int32_t* cand, const uint32_t* meta, const uint32_t* base,
                        uint64_t* flags, int32_t* idx_out, float* val_out, uint32_t* status,
-                       hipStream_t s);
+                       uint32_t* clear_next, int64_t clear_words, hipStream_t s);
 // launch-shape limits of the selection kernels
 int32_t select_max_groups();
 int32_t select_block();

@@ -110,6 +110,11 @@ __device__ __forceinline__ float4 load_nt4(const float4* p) {
   return make_float4(t.x, t.y, t.z, t.w);
 }
 
+__device__ __forceinline__ void store_nt4(float4* p, float4 v) {
+  const v4f t = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(t, reinterpret_cast<v4f*>(p));
+}
+
 __device__ __forceinline__ uint32_t add_quad(float4 a, float4 b, float4& x, uint32_t* h) {
   x.x = a.x + b.x;
   x.y = a.y + b.y;
@@ -176,8 +181,8 @@ __global__ __launch_bounds__(kBlock) void k_stream(const TileDesc* __restrict__ 
       float4 x0, x1;
       uint32_t m0 = add_quad(a0, b0, x0, h);
       uint32_t m1 = add_quad(a1, b1, x1, h);
-      r4[tid] = x0;
-      r4[kBlock + tid] = x1;
+      store_nt4(r4 + tid, x0);
+      store_nt4(r4 + kBlock + tid, x1);
       tmax = max(tmax, max(m0, m1));
       m0 = max(m0, (uint32_t)__shfl_xor((int)m0, 1));
       m1 = max(m1, (uint32_t)__shfl_xor((int)m1, 1));
@@ -441,73 +446,132 @@ __device__ __forceinline__ void sblock_pick(const uint32_t* __restrict__ hist, u
   __syncthreads();
 }
 
-// Iterates over the elements a thread owns, in position order, calling
-// f(tile, TileDesc, e, x, key) for each. Line mode: the thread's `lpt`
-// consecutive summary lines starting at line0; a line is read only when its
-// summary reaches thr(group). The summaries and the (at most two) tile
-// descriptors of the thread's lines are fetched together up front.
-template <typename Thr, typename F>
-__device__ __forceinline__ void walk_lines(const TileDesc* __restrict__ tiles,
-                                           const uint16_t* __restrict__ summ, int64_t nlines,
-                                           int64_t line0, int lpt, Thr thr, F f) {
-  if (line0 >= nlines) return;
-  const int64_t last = min(line0 + lpt, nlines) - 1;
-  const int tile0 = (int)(line0 / kLinesPerTile), tile1 = (int)(last / kLinesPerTile);
+// Within one workgroup: level-1 pick over a 2048-bin histogram held in
+// `nslots` copies (two bins per thread). Returns via res[]: bin, count above
+// it, count in it. Ends with a barrier.
+__device__ __forceinline__ void sblock_pick1(const uint32_t* __restrict__ hist1, int nslots,
+                                             uint32_t need, uint32_t* wsum, uint32_t* res) {
+  static_assert(kH1Bins == 2 * kSBlock, "two bins per thread");
+  const int tid = threadIdx.x;
+  const int lo = kH1Bins - 2 * (tid + 1);  // this thread's bins: lo, lo + 1 (from the top)
+  uint32_t c0 = 0u, c1 = 0u;
+#pragma unroll 16
+  for (int sl = 0; sl < nslots; ++sl) {
+    const uint2 v = *reinterpret_cast<const uint2*>(hist1 + (size_t)sl * kH1Bins + lo);
+    c0 += v.x;
+    c1 += v.y;
+  }
+  __syncthreads();  // earlier readers of res[] are done
+  if (tid == 0) {
+    res[0] = 0u;
+    res[1] = 0u;
+    res[2] = 0u;
+  }
+  uint32_t total;
+  const uint32_t ex = sblock_scan(c0 + c1, wsum, &total);
+  if (ex < need && need <= ex + c0 + c1) {
+    if (ex + c1 >= need) {  // higher bin first
+      res[0] = (uint32_t)(lo + 1);
+      res[1] = ex;
+      res[2] = c1;
+    } else {
+      res[0] = (uint32_t)lo;
+      res[1] = ex + c1;
+      res[2] = c0;
+    }
+  }
+  __syncthreads();
+}
+
+// The thread's `lpt` consecutive summary lines starting at line0, seen
+// through the (at most two) tiles they lie in. Summaries and descriptors are
+// fetched together up front; flagged() gives the lines whose summary reaches
+// thr(group).
+struct LineSpan {
+  int64_t line0, last;
+  int tile0, tile1;
+  TileDesc tA, tB;
   uint16_t sv[kSMaxLpt];
+
+  __device__ __forceinline__ void load(const TileDesc* __restrict__ tiles,
+                                       const uint16_t* __restrict__ summ, int64_t nlines,
+                                       int64_t l0, int lpt) {
+    line0 = l0;
+    const bool has = l0 < nlines;
+    last = has ? min(l0 + lpt, nlines) - 1 : l0 - 1;
+    tile0 = has ? (int)(l0 / kLinesPerTile) : 0;
+    tile1 = has ? (int)(last / kLinesPerTile) : 0;
 #pragma unroll
-  for (int q = 0; q < kSMaxLpt; ++q)
-    sv[q] = (line0 + q <= last) ? summ[line0 + q] : (uint16_t)0;
-  const TileDesc tA = tiles[tile0];
-  const TileDesc tB = tiles[tile1];
+    for (int q = 0; q < kSMaxLpt; ++q) sv[q] = (l0 + q <= last) ? summ[l0 + q] : (uint16_t)0;
+    tA = tiles[tile0];
+    tB = tiles[tile1];
+  }
+  __device__ __forceinline__ bool in_a(int q) const {
+    return (int)((line0 + q) / kLinesPerTile) == tile0;
+  }
+  __device__ __forceinline__ const TileDesc& desc(int q) const { return in_a(q) ? tA : tB; }
+  __device__ __forceinline__ int tile(int q) const { return in_a(q) ? tile0 : tile1; }
+  __device__ __forceinline__ int e0(int q) const {
+    return (int)((line0 + q) % kLinesPerTile) * kLine;
+  }
+  template <typename Thr>
+  __device__ __forceinline__ uint32_t flagged(Thr thr) const {
+    const uint32_t ta = thr(tA.group) >> 16, tb = thr(tB.group) >> 16;
+    uint32_t m = 0u;
 #pragma unroll
-  for (int q = 0; q < kSMaxLpt; ++q) {
-    const int64_t gl = line0 + q;
-    if (gl > last) break;
-    const int tile = (int)(gl / kLinesPerTile);
-    const int lit = (int)(gl % kLinesPerTile);
-    const TileDesc& t = (tile == tile0) ? tA : tB;
-    if (lit * kLine >= t.len) continue;
-    if ((uint32_t)sv[q] < (thr(t.group) >> 16)) continue;
-    const int e0 = lit * kLine;
-    const int n = min(kLine, t.len - e0);
+    for (int q = 0; q < kSMaxLpt; ++q) {
+      const bool a = in_a(q);
+      if (line0 + q <= last && e0(q) < (a ? tA.len : tB.len) && (uint32_t)sv[q] >= (a ? ta : tb))
+        m |= 1u << q;
+    }
+    return m;
+  }
+};
+
+// For every element of the flagged lines in `mask`, in position order, for
+// which hit(group, key) holds: f(tile, TileDesc, e, x, key). The hit test runs
+// over all 32 elements of a line at once; the (few) hits are then visited one
+// by one, re-reading the element from the line just loaded.
+template <typename Hit, typename F>
+__device__ __forceinline__ void walk_mask(const LineSpan& ls, uint32_t mask, Hit hit, F f) {
+#pragma unroll 1
+  while (mask) {
+    const int q = __ffs(mask) - 1;
+    mask &= mask - 1u;
+    const TileDesc& t = ls.desc(q);
+    const int e0 = ls.e0(q), n = min(kLine, t.len - e0);
     float v[kLine];
     load_line(t.r, e0, n, v);
+    uint32_t hm = 0u;
 #pragma unroll
     for (int j = 0; j < kLine; ++j)
-      if (j < n) f(tile, t, e0 + j, v[j], mag_key(v[j]));
+      hm |= (j < n && hit(t.group, mag_key(v[j]))) ? (1u << j) : 0u;
+    const int tile = ls.tile(q);
+#pragma unroll 1
+    while (hm) {
+      const int j = __ffs(hm) - 1;
+      hm &= hm - 1u;
+      const float x = t.r[e0 + j];
+      f(tile, t, e0 + j, x, mag_key(x));
+    }
   }
 }
 
-// Candidate mode: candidates [cb, ce), fetched four at a time (codes, then
-// descriptors, then values, each batch of loads in flight together).
+// Calls f(tile, TileDesc, e, x, key) for candidates [cb, ce), in order.
 template <typename F>
 __device__ __forceinline__ void walk_cands(const TileDesc* __restrict__ tiles, int32_t ntiles,
                                            const int32_t* __restrict__ cand, uint32_t cb,
                                            uint32_t ce, F f) {
-  constexpr int B = 4;
-  for (uint32_t j0 = cb; j0 < ce; j0 += B) {
-    uint32_t c[B];
-#pragma unroll
-    for (int q = 0; q < B; ++q) c[q] = (j0 + q < ce) ? (uint32_t)cand[j0 + q] : 0xFFFFFFFFu;
-    TileDesc t[B];
-    int e[B];
-#pragma unroll
-    for (int q = 0; q < B; ++q) {
-      const int tile = (c[q] == 0xFFFFFFFFu) ? ntiles : (int)(c[q] >> kCandShift);
-      e[q] = (int)(c[q] & (kTile - 1));
-      if (tile < ntiles) {  // never false for produced candidates; keeps accesses in bounds
-        t[q] = tiles[tile];
-        if (e[q] >= t[q].len) e[q] = -1;
-      } else {
-        e[q] = -1;
-      }
-    }
-    float x[B];
-#pragma unroll
-    for (int q = 0; q < B; ++q) x[q] = (e[q] >= 0) ? t[q].r[e[q]] : 0.0f;
-#pragma unroll
-    for (int q = 0; q < B; ++q)
-      if (e[q] >= 0) f((int)(c[q] >> kCandShift), t[q], e[q], x[q], mag_key(x[q]));
+#pragma unroll 1
+  for (uint32_t j = cb; j < ce; ++j) {
+    const uint32_t c = (uint32_t)cand[j];
+    const int tile = (int)(c >> kCandShift);
+    const int e = (int)(c & (kTile - 1));
+    if (tile >= ntiles) continue;  // never produced; keeps accesses in bounds
+    const TileDesc t = tiles[tile];
+    if (e >= t.len) continue;
+    const float x = t.r[e];
+    f(tile, t, e, x, mag_key(x));
   }
 }
 
@@ -517,8 +581,12 @@ __device__ __forceinline__ void walk_cands(const TileDesc* __restrict__ tiles, i
 // elements in bin B1 (level 2); (b) ordered compaction of all elements with
 // key >= B1 << 20 into `cand`. meta[0] = overflow (the candidates did not fit
 // in `cap`; later steps then read lines), meta[1] = candidate count.
+constexpr int kStage = 8;  // candidates / items a thread stages in LDS
+
 __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__ tiles,
-                                                    const GroupState* __restrict__ st,
+                                                    const GroupDesc* __restrict__ groups,
+                                                    GroupState* __restrict__ st,
+                                                    const uint32_t* __restrict__ hist1, int nslots,
                                                     int single, const uint16_t* __restrict__ summ,
                                                     int64_t nlines, int lpt,
                                                     uint32_t* __restrict__ hist2,
@@ -529,91 +597,59 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
   __shared__ uint32_t h[kH2Bins];
   __shared__ uint32_t wsum[kSWaves];
   __shared__ uint64_t red[kSWaves];
-  __shared__ int32_t flagged[kSBlock * kSMaxLpt];  // this workgroup's flagged lines, in order
+  __shared__ uint32_t res[3];
+  __shared__ int32_t stage[kStage * kSBlock];  // [slot][thread]
   __shared__ uint32_t any;
   const int tid = threadIdx.x;
-  const GroupState s0 = st[0];
   h[tid] = 0u;
   if (tid == 0) any = 0u;
-  auto b1_of = [&](int g) -> uint32_t { return single ? s0.prefix : st[g].prefix; };
 
-  // 1. summaries of this thread's lines (and their tiles): which lines can
-  //    hold a key >= B1 << 20 (B1 = 0xFFFFFFFF for a group with nothing to
-  //    select: shifted, it lies above every key)
-  const int64_t line0 = ((int64_t)blockIdx.x * kSBlock + tid) * lpt;
-  uint32_t fmask = 0u;
-  if (line0 < nlines) {
-    const int64_t last = min(line0 + lpt, nlines) - 1;
-    const int tile0 = (int)(line0 / kLinesPerTile), tile1 = (int)(last / kLinesPerTile);
-    uint16_t sv[kSMaxLpt];
-#pragma unroll
-    for (int q = 0; q < kSMaxLpt; ++q) sv[q] = (line0 + q <= last) ? summ[line0 + q] : (uint16_t)0;
-    const TileDesc tA = tiles[tile0];
-    const TileDesc tB = tiles[tile1];
-    const uint32_t thrA = (b1_of(tA.group) << kH1Shift) >> 16;
-    const uint32_t thrB = (b1_of(tB.group) << kH1Shift) >> 16;
-#pragma unroll
-    for (int q = 0; q < kSMaxLpt; ++q) {
-      const int64_t gl = line0 + q;
-      if (gl > last) break;
-      const bool inA = (int)(gl / kLinesPerTile) == tile0;
-      const int lit = (int)(gl % kLinesPerTile);
-      const int len = inA ? tA.len : tB.len;
-      if (lit * kLine < len && (uint32_t)sv[q] >= (inA ? thrA : thrB)) fmask |= 1u << q;
-    }
+  // 1. summaries and tiles of this thread's lines (independent of the pick)
+  LineSpan ls;
+  ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
+
+  // 2. level-1 pick. One selection group: every workgroup makes it itself
+  //    from the slotted histogram and workgroup 0 records it for the later
+  //    kernels. Several groups: the pick kernel has done it.
+  GroupState s0;
+  if (single) {
+    const uint32_t k = groups[0].k;
+    sblock_pick1(hist1, nslots, k, wsum, res);
+    s0.prefix = (k == 0u) ? 0xFFFFFFFFu : res[0];
+    s0.need = (k == 0u || res[1] >= k) ? 0u : k - res[1];
+    s0.T = 0xFFFFFFFFu;
+    s0.n_eq = 0u;
+    if (blockIdx.x == 0 && tid == 0) st[0] = s0;
+  } else {
+    s0 = st[0];
   }
-  // 2. compact the flagged line numbers of the workgroup into LDS, in order
-  uint32_t nf;
-  const uint32_t fx = sblock_scan(__popc(fmask), wsum, &nf);
-  {
-    uint32_t m = fmask, j = fx;
-    while (m) {
-      const int q = __ffs(m) - 1;
-      m &= m - 1u;
-      flagged[j++] = (int32_t)(line0 + q);
-    }
-  }
-  __syncthreads();
-  // 3. each thread takes a contiguous share of the flagged lines (usually at
-  //    most one), counts its candidates and keeps the first few in registers
-  const uint32_t per = (nf + kSBlock - 1) / kSBlock;
-  const uint32_t fb = min(nf, tid * per), fe = min(nf, fb + per);
-  constexpr int kRegCands = 8;
-  int32_t rc[kRegCands];
-  uint32_t c = 0u, hit = 0u;
-  auto visit = [&](int32_t gl, bool write, uint64_t pos0) {
-    const int tile = gl / kLinesPerTile, lit = gl % kLinesPerTile;
-    const TileDesc t = tiles[tile];
-    const uint32_t b1 = b1_of(t.group);
-    const uint32_t lo = b1 << kH1Shift;
-    const int e0 = lit * kLine;
-    const int n = min(kLine, t.len - e0);
-    float v[kLine];
-    load_line(t.r, e0, n, v);
-#pragma unroll
-    for (int j = 0; j < kLine; ++j) {
-      const uint32_t k = mag_key(v[j]);
-      if (j < n && k >= lo) {
-        const int32_t code = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)(e0 + j));
-        if (write) {
-          if (c >= (uint32_t)kRegCands) cand[pos0 + c] = code;
-        } else {
-#pragma unroll
-          for (int q = 0; q < kRegCands; ++q)
-            if (c == (uint32_t)q) rc[q] = code;
-          if ((k >> kH1Shift) == b1) {
-            const uint32_t bin = (k >> kH2Shift) & (kH2Bins - 1);
-            if (single) atomicAdd(&h[bin], 1u);
-            else atomicAdd(&hist2[(size_t)t.group * kH2Bins + bin], 1u);
-            hit = 1u;
-          }
-        }
-        ++c;
-      }
-    }
+  // B1 = 0xFFFFFFFF for a group with nothing to select: shifted, it lies
+  // above every key, so such a group yields no candidates
+  auto b1_of = [&](int g) -> uint32_t { return single ? s0.prefix : st[g].prefix; };
+  const uint32_t b1A = b1_of(ls.tA.group), b1B = b1_of(ls.tB.group);
+  const uint32_t mask = ls.flagged([&](int g) -> uint32_t {
+    return (g == ls.tA.group ? b1A : b1B) << kH1Shift;
+  });
+
+  // 3. count the candidates of the flagged lines; stage the first kStage in LDS
+  auto is_cand = [&](int g, uint32_t k) -> bool {
+    return k >= ((g == ls.tA.group ? b1A : b1B) << kH1Shift);
   };
-  for (uint32_t j = fb; j < fe; ++j) visit(flagged[j], false, 0);
+  uint32_t c = 0u, hit = 0u;
+  walk_mask(ls, mask, is_cand, [&](int tile, const TileDesc& t, int e, float, uint32_t k) {
+    const uint32_t b1 = (t.group == ls.tA.group) ? b1A : b1B;
+    if (c < (uint32_t)kStage)
+      stage[c * kSBlock + tid] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
+    ++c;
+    if ((k >> kH1Shift) == b1) {
+      const uint32_t bin = (k >> kH2Shift) & (kH2Bins - 1);
+      if (single) atomicAdd(&h[bin], 1u);
+      else atomicAdd(&hist2[(size_t)t.group * kH2Bins + bin], 1u);
+      hit = 1u;
+    }
+  });
   if (hit) any = 1u;
+
   // 4. ordered positions: scan within the workgroup, prefix across workgroups
   uint32_t total;
   const uint32_t ex = sblock_scan(c, wsum, &total);
@@ -625,14 +661,16 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
   }
   if (fits && c) {
     const uint64_t pos = pre + ex;
-#pragma unroll
-    for (int q = 0; q < kRegCands; ++q)
-      if ((uint32_t)q < c) cand[pos + q] = rc[q];
-    if (c > (uint32_t)kRegCands) {  // rare: read the lines again for the rest
-      const uint32_t ctot = c;
-      c = 0u;
-      for (uint32_t j = fb; j < fe; ++j) visit(flagged[j], true, pos);
-      c = ctot;
+    const uint32_t ns = min(c, (uint32_t)kStage);
+#pragma unroll 1
+    for (uint32_t q = 0; q < ns; ++q) cand[pos + q] = stage[q * kSBlock + tid];
+    if (c > (uint32_t)kStage) {  // rare: read the lines again for the rest
+      uint32_t i = 0u;
+      walk_mask(ls, mask, is_cand, [&](int tile, const TileDesc&, int e, float, uint32_t) {
+        if (i >= (uint32_t)kStage)
+          cand[pos + i] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
+        ++i;
+      });
     }
   }
   if (single && any) {  // `any` was written before the scans' barriers
@@ -684,9 +722,9 @@ __global__ __launch_bounds__(kSBlock) void k_hist3(const TileDesc* __restrict__ 
     return sg.need ? sg.prefix : 0xFFFFFFFFu;
   };
   uint32_t hit = 0u;
+  auto in_cls = [&](int g, uint32_t k) -> bool { return (k >> kH2Shift) == cls_of(g); };
   auto body = [&](int, const TileDesc& t, int, float, uint32_t k) {
-    const uint32_t cls = cls_of(t.group);
-    if ((k >> kH2Shift) == cls) {
+    if (in_cls(t.group, k)) {
       const uint32_t bin = k & (kH3Bins - 1);
       if (single) atomicAdd(&h[bin], 1u);
       else atomicAdd(&hist3[(size_t)t.group * kH3Bins + bin], 1u);
@@ -694,12 +732,14 @@ __global__ __launch_bounds__(kSBlock) void k_hist3(const TileDesc* __restrict__ 
     }
   };
   if (ov) {
-    const int64_t line0 = ((int64_t)blockIdx.x * kSBlock + tid) * lpt;
-    walk_lines(tiles, summ, nlines, line0, lpt,
-               [&](int g) -> uint32_t { return cls_of(g) << kH2Shift; }, body);
+    LineSpan ls;
+    ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
+    walk_mask(ls, ls.flagged([&](int g) -> uint32_t { return cls_of(g) << kH2Shift; }), in_cls,
+              body);
   } else {
     const uint32_t per_wg = (C + gridDim.x - 1) / gridDim.x;
     const uint32_t wb = min(C, blockIdx.x * per_wg), we = min(C, wb + per_wg);
+#pragma unroll 1
     for (uint32_t j = wb + tid; j < we; j += kSBlock) walk_cands(tiles, ntiles, cand, j, j + 1, body);
   }
   if (hit) any = 1u;
@@ -761,11 +801,20 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
                                                   uint64_t* __restrict__ flags,
                                                   int32_t* __restrict__ idx_out,
                                                   float* __restrict__ val_out,
-                                                  uint32_t* __restrict__ status) {
+                                                  uint32_t* __restrict__ status,
+                                                  uint32_t* __restrict__ clear_next,
+                                                  int64_t clear_words) {
   __shared__ uint32_t wsum[kSWaves];
   __shared__ uint64_t red[kSWaves];
   __shared__ uint32_t res[3];
+  __shared__ int32_t stage_code[kStage * kSBlock];  // [slot][thread]: (tile << 13) | e
+  __shared__ float stage_x[kStage * kSBlock];
   const int tid = threadIdx.x;
+  // clear the other copy of the zero-initialised scratch for the next run
+#pragma unroll 1
+  for (int64_t i = (int64_t)blockIdx.x * kSBlock + tid; i < clear_words;
+       i += (int64_t)gridDim.x * kSBlock)
+    clear_next[i] = 0u;
   const uint32_t ov = meta[0], C = meta[1];
   const GroupState s0 = st[0];
   const GroupDesc gd0 = groups[0];
@@ -780,9 +829,13 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
     }
   }
   auto T_of = [&](int g) -> uint32_t { return single ? T_one : st[g].T; };
-  const int64_t line0 = ((int64_t)blockIdx.x * kSBlock + tid) * lpt;
-  uint32_t cb = 0u, ce = 0u;
-  if (!ov) {
+  // this thread's elements: a run of candidates, or (after an overflow) lines
+  LineSpan ls;
+  uint32_t mask = 0u, cb = 0u, ce = 0u;
+  if (ov) {
+    ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
+    mask = ls.flagged(T_of);
+  } else {
     const uint32_t per_wg = (C + gridDim.x - 1) / gridDim.x;
     const uint32_t wb = min(C, blockIdx.x * per_wg), we = min(C, wb + per_wg);
     const uint32_t per = (we - wb + kSBlock - 1) / kSBlock;
@@ -790,33 +843,28 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
     ce = min(we, cb + per);
   }
   // pass 1: counts of (key > T) and (key == T), in position order; the first
-  // kRegItems selected-or-tied elements are kept in registers for pass 2
-  constexpr int kRegItems = 4;
-  int rtile[kRegItems], re[kRegItems];
-  float rx[kRegItems];
-  uint32_t gt = 0u, eq = 0u, nreg = 0u;
+  // kStage elements with key >= T are staged in LDS for pass 2
+  uint32_t gt = 0u, eq = 0u, nst = 0u;
   auto count = [&](int tile, const TileDesc& t, int e, float x, uint32_t k) {
     const uint32_t T = T_of(t.group);
     if (k >= T) {
-#pragma unroll
-      for (int q = 0; q < kRegItems; ++q)
-        if (nreg == (uint32_t)q) {
-          rtile[q] = tile;
-          re[q] = e;
-          rx[q] = x;
-        }
-      ++nreg;
+      if (nst < (uint32_t)kStage) {
+        stage_code[nst * kSBlock + tid] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
+        stage_x[nst * kSBlock + tid] = x;
+      }
+      ++nst;
+      gt += (k > T) ? 1u : 0u;
+      eq += (k == T) ? 1u : 0u;
     }
-    gt += (k > T) ? 1u : 0u;
-    eq += (k == T) ? 1u : 0u;
   };
-  if (ov) walk_lines(tiles, summ, nlines, line0, lpt, T_of, count);
+  auto at_least_T = [&](int g, uint32_t k) -> bool { return k >= T_of(g); };
+  if (ov) walk_mask(ls, mask, at_least_T, count);
   else walk_cands(tiles, ntiles, cand, cb, ce, count);
   uint32_t tot_gt, tot_eq;
   const uint32_t xg = sblock_scan(gt, wsum, &tot_gt);
   const uint32_t xe = sblock_scan(eq, wsum, &tot_eq);
   const uint64_t pre = group_prefix(flags, (uint64_t)tot_gt | ((uint64_t)tot_eq << 31), red, status);
-  if (gt == 0u && eq == 0u) return;
+  if (nst == 0u) return;
   uint32_t gtr = (uint32_t)(pre & 0x7FFFFFFFu) + xg;
   uint32_t eqr = (uint32_t)((pre >> 31) & 0x7FFFFFFFu) + xe;
   // pass 2: write
@@ -841,15 +889,17 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
       t.r[e] = 0.0f;
     }
   };
-  if (nreg <= (uint32_t)kRegItems) {
-#pragma unroll
-    for (int q = 0; q < kRegItems; ++q)
-      if ((uint32_t)q < nreg) {
-        const TileDesc t = tiles[rtile[q]];
-        write(rtile[q], t, re[q], rx[q], mag_key(rx[q]));
-      }
+  if (nst <= (uint32_t)kStage) {
+#pragma unroll 1
+    for (uint32_t q = 0; q < nst; ++q) {
+      const uint32_t code = (uint32_t)stage_code[q * kSBlock + tid];
+      const int tile = (int)(code >> kCandShift);
+      const TileDesc t = tiles[tile];
+      const float x = stage_x[q * kSBlock + tid];
+      write(tile, t, (int)(code & (kTile - 1)), x, mag_key(x));
+    }
   } else if (ov) {
-    walk_lines(tiles, summ, nlines, line0, lpt, T_of, write);
+    walk_mask(ls, mask, at_least_T, write);
   } else {
     walk_cands(tiles, ntiles, cand, cb, ce, write);
   }
@@ -1026,8 +1076,8 @@ __global__ __launch_bounds__(kUBlock) void k_update(
       w.y = sgd_step(G.y, w.y, bb.y, mom, lr, mu, wd);
       w.z = sgd_step(G.z, w.z, bb.z, mom, lr, mu, wd);
       w.w = sgd_step(G.w, w.w, bb.w, mom, lr, mu, wd);
-      w4[v] = w;
-      if (mom) b4[v] = bb;
+      store_nt4(w4 + v, w);
+      if (mom) store_nt4(b4 + v, bb);
     }
     return;
   }
@@ -1121,12 +1171,13 @@ hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
   return hipGetLastError();
 }
 
-hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, int single,
-                         const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
-                         uint32_t* hist2, uint64_t* flags, int32_t* cand, uint32_t cap,
-                         uint32_t* meta, uint32_t* status, hipStream_t s) {
-  hipLaunchKernelGGL(k_gather, dim3(grid), dim3(kSBlock), 0, s, tiles, st, single, summ, nlines,
-                     lpt, hist2, flags, cand, cap, meta, status);
+hipError_t launch_gather(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
+                         const uint32_t* hist1, int nslots, int single, const uint16_t* summ,
+                         int64_t nlines, int lpt, int32_t grid, uint32_t* hist2,
+                         uint64_t* flags, int32_t* cand, uint32_t cap, uint32_t* meta,
+                         uint32_t* status, hipStream_t s) {
+  hipLaunchKernelGGL(k_gather, dim3(grid), dim3(kSBlock), 0, s, tiles, groups, st, hist1, nslots,
+                     single, summ, nlines, lpt, hist2, flags, cand, cap, meta, status);
   return hipGetLastError();
 }
 
@@ -1150,10 +1201,10 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
                        int lpt, int32_t grid, const uint32_t* hist2, const uint32_t* hist3,
                        const int32_t* cand, const uint32_t* meta, const uint32_t* base,
                        uint64_t* flags, int32_t* idx_out, float* val_out, uint32_t* status,
-                       hipStream_t s) {
+                       uint32_t* clear_next, int64_t clear_words, hipStream_t s) {
   hipLaunchKernelGGL(k_emit, dim3(grid), dim3(kSBlock), 0, s, tiles, ntiles, groups, st, single, summ,
                      nlines, lpt, hist2, hist3, cand, meta, base, flags, idx_out, val_out,
-                     status);
+                     status, clear_next, clear_words);
   return hipGetLastError();
 }
 
