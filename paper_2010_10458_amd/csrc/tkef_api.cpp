@@ -93,11 +93,11 @@ extern "C" int64_t tkef_k_from_rho(int64_t d, double rho) {
 // sparsify plan
 
 // Launch sequences: one selection group (global) and several (per tensor).
-static const char* const kSparsifyLaunchesOne[] = {"stream", "gather", "hist3", "emit"};
+static const char* const kSparsifyLaunchesOne[] = {"stream", "collect", "finish"};
 static const char* const kSparsifyLaunchesMany[] = {"stream", "pick1", "gather",
                                                     "pick2",  "hist3", "pick3",
                                                     "groupscan", "emit"};
-constexpr int32_t kSparsifyNLaunchOne = 4, kSparsifyNLaunchMany = 8;
+constexpr int32_t kSparsifyNLaunchOne = 3, kSparsifyNLaunchMany = 8;
 
 struct tkef_sparsify_plan_s {
   int32_t ntensors = 0, mode = 0, ngroups = 0, ntiles = 0, nslots = 1, stream_grid = 1;
@@ -105,7 +105,8 @@ struct tkef_sparsify_plan_s {
   std::vector<int64_t> numels, goff, kgroup;
   std::vector<TileDesc> tiles;   // pointers filled at bind
   std::vector<GroupDesc> groups;
-  uint32_t cand_cap = 0;  // capacity of the compacted candidate list
+  uint32_t cand_cap = 0;  // per-tensor path: capacity of the compacted candidate list
+  uint32_t rcap = 0;      // one-group path: candidates stored per region
   int32_t sel_lpt = 1, sel_grid = 1;  // selection kernels: lines per thread, workgroups
   // Scratch that must start at zero (histograms, prefix flags, overflow and
   // count words) exists twice; execution n uses copy n % 2 and its last kernel
@@ -113,7 +114,8 @@ struct tkef_sparsify_plan_s {
   // the start of a copy, which lies at off_zero[0] or off_zero[1].
   size_t off_tiles = 0, off_groups = 0, off_state = 0, off_zero[2] = {0, 0}, zero_bytes = 0,
          off_hist1 = 0, off_hist2 = 0, off_hist3 = 0, off_flags1 = 0, off_flags2 = 0,
-         off_meta = 0, off_summ = 0, off_base = 0, off_cand = 0, ws_bytes = 0;
+         off_meta = 0, off_summ = 0, off_base = 0, off_cand = 0, off_rcand = 0, off_rband = 0,
+         off_rsuf = 0, off_rcnt = 0, off_gcnt = 0, off_gband = 0, ws_bytes = 0;
   uint64_t executions = 0;   // since the last bind
   bool needs_clear = true;   // both copies must be cleared before the next run
   int32_t nlaunch() const { return ngroups == 1 ? kSparsifyNLaunchOne : kSparsifyNLaunchMany; }
@@ -184,26 +186,34 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     }
     p->ntiles = static_cast<int32_t>(p->tiles.size());
     p->nlines = (int64_t)p->ntiles * kLinesPerTile;
-    // Candidates are the positions at or above the level-1 threshold bin:
-    // about k plus one bin's worth. Four times k plus a margin covers that
-    // for ordinary data; heavier inputs fall back to re-reading lines.
-    p->cand_cap = (uint32_t)std::min<int64_t>(d, 4 * p->k_total + 65536);
     // selection kernels: `lpt` consecutive summary lines per thread, at most
-    // select_max_groups() workgroups of select_block() threads; enough
-    // workgroups that a candidate run per thread stays short
-    // Aim for about 256 workgroups (one per compute unit, so all are resident
-    // at once) with at least two lines per thread.
+    // select_max_groups() workgroups of select_block() threads. Aim for about
+    // 256 workgroups (one per compute unit) with at least two lines per thread.
     const int64_t sb = select_block(), sg = select_max_groups();
     int64_t lpt = std::max<int64_t>(2, (p->nlines + sb * 256 - 1) / (sb * 256));
     lpt = std::min<int64_t>(lpt, select_max_lpt());
     if ((p->nlines + sb * lpt - 1) / (sb * lpt) > sg) throw std::bad_alloc();  // d < 2^31
     p->sel_lpt = (int32_t)lpt;
     const int64_t g_lines = (p->nlines + sb * lpt - 1) / (sb * lpt);
-    const int64_t g_cands = std::min<int64_t>(sg, ((int64_t)p->cand_cap + sb * 4 - 1) / (sb * 4));
-    p->sel_grid = (int32_t)std::max<int64_t>(1, std::max(g_lines, g_cands));
+    const bool one = p->ngroups == 1;
+    // Candidates are the positions at or above the level-1 threshold bin:
+    // about k plus one bin's worth. One group: each region (the lines of one
+    // workgroup) stores up to rcap of them, several times the even share of
+    // 8k + 65536; per tensor: one compacted list of 4k + 65536. Heavier inputs
+    // fall back to re-reading lines.
+    if (one) {
+      p->sel_grid = (int32_t)std::max<int64_t>(1, g_lines);
+      const int64_t region = lpt * sb * kLine;
+      const int64_t share = (8 * p->k_total + 65536 + p->sel_grid - 1) / p->sel_grid;
+      p->rcap = (uint32_t)std::min<int64_t>(region, std::max<int64_t>(4096, (share + 63) / 64 * 64));
+    } else {
+      p->cand_cap = (uint32_t)std::min<int64_t>(d, 4 * p->k_total + 65536);
+      const int64_t g_cands = std::min<int64_t>(sg, ((int64_t)p->cand_cap + sb * 4 - 1) / (sb * 4));
+      p->sel_grid = (int32_t)std::max<int64_t>(1, std::max(g_lines, g_cands));
+    }
     // level-1 histogram copies per group: many for one global selection (all
     // workgroups add into it), a few per tensor in per-tensor mode
-    p->nslots = (p->ngroups == 1) ? 16 : 4;
+    p->nslots = one ? 16 : 4;
 
     // workspace layout (every region 256-B aligned)
     size_t o = 0;
@@ -213,16 +223,29 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     size_t z = 0;
     p->off_hist1 = z;   z = align_up(z + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
     p->off_hist2 = z;   z = align_up(z + (size_t)p->ngroups * kH2Bins * 4);
-    p->off_hist3 = z;   z = align_up(z + (size_t)p->ngroups * kH3Bins * 4);
-    p->off_flags1 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
-    p->off_flags2 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
-    p->off_meta = z;    z = align_up(z + 8);
+    if (one) {
+      p->off_gcnt = z;    z = align_up(z + (size_t)kH2Bins * 4);
+    } else {
+      p->off_hist3 = z;   z = align_up(z + (size_t)p->ngroups * kH3Bins * 4);
+      p->off_flags1 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
+      p->off_flags2 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
+      p->off_meta = z;    z = align_up(z + 8);
+    }
     p->zero_bytes = z;
     p->off_zero[0] = o; o = align_up(o + z);
     p->off_zero[1] = o; o = align_up(o + z);
     p->off_summ = o;    o = align_up(o + (size_t)p->nlines * sizeof(uint16_t));
-    p->off_base = o;    o = align_up(o + (size_t)p->ngroups * 8);
-    p->off_cand = o;    o = align_up(o + (size_t)p->cand_cap * 4);
+    if (one) {
+      const size_t slots = (size_t)p->sel_grid * p->rcap;
+      p->off_rcand = o;  o = align_up(o + slots * 16);
+      p->off_rband = o;  o = align_up(o + slots * 4);
+      p->off_rsuf = o;   o = align_up(o + (size_t)p->sel_grid * kH2Bins * 4);
+      p->off_rcnt = o;   o = align_up(o + (size_t)p->sel_grid * 8);
+      p->off_gband = o;  o = align_up(o + (size_t)kH2Bins * kBinCap * 8);
+    } else {
+      p->off_base = o;   o = align_up(o + (size_t)p->ngroups * 8);
+      p->off_cand = o;   o = align_up(o + (size_t)p->cand_cap * 4);
+    }
     p->ws_bytes = o;
   } catch (const std::bad_alloc&) {
     delete p;
@@ -333,19 +356,14 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   char* zn = base + plan->off_zero[par ^ 1];       // cleared for the next execution
   uint32_t* hist1 = reinterpret_cast<uint32_t*>(zb + plan->off_hist1);
   uint32_t* hist2 = reinterpret_cast<uint32_t*>(zb + plan->off_hist2);
-  uint32_t* hist3 = reinterpret_cast<uint32_t*>(zb + plan->off_hist3);
   uint16_t* summ = reinterpret_cast<uint16_t*>(base + plan->off_summ);
-  uint64_t* flags1 = reinterpret_cast<uint64_t*>(zb + plan->off_flags1);
-  uint64_t* flags2 = reinterpret_cast<uint64_t*>(zb + plan->off_flags2);
-  uint32_t* meta = reinterpret_cast<uint32_t*>(zb + plan->off_meta);
-  uint32_t* gbase = reinterpret_cast<uint32_t*>(base + plan->off_base);
-  int32_t* cand = reinterpret_cast<int32_t*>(base + plan->off_cand);
   const int32_t nt = plan->ntiles, ng = plan->ngroups;
-  const int single = (ng == 1) ? 1 : 0;
   const int64_t nl = plan->nlines;
   const int lpt = plan->sel_lpt, sg = plan->sel_grid;
   const Tracer tr{plan->events, plan->n_events, s};
   int li = 0;  // launch index, for the timing hook
+  uint32_t* clear_next = reinterpret_cast<uint32_t*>(zn);
+  const int64_t clear_words = (int64_t)(plan->zero_bytes / 4);
 
   hipError_t e = hipSuccess;
   if (plan->needs_clear) {  // after a failed run
@@ -358,34 +376,60 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   if (tr.ev && tr.n > 0) (void)hipEventRecord(tr.ev[0], s);
   e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s);
   tr.mark(li++);
-  if (e == hipSuccess && !single) {
-    e = launch_pick(1, groups, st, hist1, plan->nslots, ng, s);
-    tr.mark(li++);
-  }
-  if (e == hipSuccess) {
-    e = launch_gather(tiles, groups, st, hist1, plan->nslots, single, summ, nl, lpt, sg, hist2,
-                      flags1, cand, plan->cand_cap, meta, status, s);
-    tr.mark(li++);
-  }
-  if (e == hipSuccess && !single) {
-    e = launch_pick(2, groups, st, hist2, 1, ng, s);
-    tr.mark(li++);
-  }
-  if (e == hipSuccess) {
-    e = launch_hist3(tiles, nt, st, single, summ, nl, lpt, sg, hist2, cand, meta, hist3, s);
-    tr.mark(li++);
-  }
-  if (e == hipSuccess && !single) {
-    e = launch_pick(3, groups, st, hist3, 1, ng, s);
-    tr.mark(li++);
-    if (e == hipSuccess) e = launch_groupscan(groups, st, ng, gbase, s);
-    tr.mark(li++);
-  }
-  if (e == hipSuccess) {
-    e = launch_emit(tiles, nt, groups, st, single, summ, nl, lpt, sg, hist2, hist3, cand, meta,
-                    gbase, flags2, idx_out, val_out, status,
-                    reinterpret_cast<uint32_t*>(zn), (int64_t)(plan->zero_bytes / 4), s);
-    tr.mark(li++);
+  if (ng == 1) {
+    uint32_t* rcand = reinterpret_cast<uint32_t*>(base + plan->off_rcand);
+    uint32_t* rband = reinterpret_cast<uint32_t*>(base + plan->off_rband);
+    uint32_t* rsuf = reinterpret_cast<uint32_t*>(base + plan->off_rsuf);
+    uint32_t* rcnt = reinterpret_cast<uint32_t*>(base + plan->off_rcnt);
+    uint32_t* gcnt = reinterpret_cast<uint32_t*>(zb + plan->off_gcnt);
+    uint32_t* gband = reinterpret_cast<uint32_t*>(base + plan->off_gband);
+    if (e == hipSuccess) {
+      e = launch_collect(tiles, groups, st, hist1, plan->nslots, summ, nl, lpt, sg, plan->rcap,
+                         hist2, gcnt, gband, rcand, rband, rsuf, rcnt, s);
+      tr.mark(li++);
+    }
+    if (e == hipSuccess) {
+      e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, plan->rcap, hist2, gcnt, gband,
+                        rcand, rband, rsuf, rcnt, idx_out, val_out, clear_next, clear_words, s);
+      tr.mark(li++);
+    }
+  } else {
+    uint32_t* hist3 = reinterpret_cast<uint32_t*>(zb + plan->off_hist3);
+    uint64_t* flags1 = reinterpret_cast<uint64_t*>(zb + plan->off_flags1);
+    uint64_t* flags2 = reinterpret_cast<uint64_t*>(zb + plan->off_flags2);
+    uint32_t* meta = reinterpret_cast<uint32_t*>(zb + plan->off_meta);
+    uint32_t* gbase = reinterpret_cast<uint32_t*>(base + plan->off_base);
+    int32_t* cand = reinterpret_cast<int32_t*>(base + plan->off_cand);
+    if (e == hipSuccess) {
+      e = launch_pick(1, groups, st, hist1, plan->nslots, ng, s);
+      tr.mark(li++);
+    }
+    if (e == hipSuccess) {
+      e = launch_gather(tiles, st, summ, nl, lpt, sg, hist2, flags1, cand, plan->cand_cap, meta,
+                        status, s);
+      tr.mark(li++);
+    }
+    if (e == hipSuccess) {
+      e = launch_pick(2, groups, st, hist2, 1, ng, s);
+      tr.mark(li++);
+    }
+    if (e == hipSuccess) {
+      e = launch_hist3(tiles, nt, st, summ, nl, lpt, sg, cand, meta, hist3, s);
+      tr.mark(li++);
+    }
+    if (e == hipSuccess) {
+      e = launch_pick(3, groups, st, hist3, 1, ng, s);
+      tr.mark(li++);
+    }
+    if (e == hipSuccess) {
+      e = launch_groupscan(groups, st, ng, gbase, s);
+      tr.mark(li++);
+    }
+    if (e == hipSuccess) {
+      e = launch_emit(tiles, nt, groups, st, summ, nl, lpt, sg, cand, meta, gbase, flags2,
+                      idx_out, val_out, status, clear_next, clear_words, s);
+      tr.mark(li++);
+    }
   }
   if (e != hipSuccess) {
     plan->needs_clear = true;

@@ -72,23 +72,37 @@ hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, ui
                          int32_t nslots, uint16_t* summ, uint32_t* status, hipStream_t s);
 hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
                        const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s);
-hipError_t launch_gather(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
-                         const uint32_t* hist1, int nslots, int single, const uint16_t* summ,
-                         int64_t nlines, int lpt, int32_t grid, uint32_t* hist2,
-                         uint64_t* flags, int32_t* cand, uint32_t cap, uint32_t* meta,
-                         uint32_t* status, hipStream_t s);
+// one selection group
+constexpr int kBinCap = 256;  // band members listed per level-2 bin (global lists)
+hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
+                          const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
+                          int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* gcnt,
+                          uint32_t* gband, uint32_t* rcand, uint32_t* rband, uint32_t* rsuf,
+                          uint32_t* rcnt, hipStream_t s);
+hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
+                         const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
+                         int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* gcnt,
+                         const uint32_t* gband, const uint32_t* rcand, const uint32_t* rband,
+                         const uint32_t* rsuf, const uint32_t* rcnt, int32_t* idx_out,
+                         float* val_out, uint32_t* clear_next, int64_t clear_words,
+                         hipStream_t s);
+// several selection groups
+hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
+                         int64_t nlines, int lpt, int32_t grid, uint32_t* hist2, uint64_t* flags,
+                         int32_t* cand, uint32_t cap, uint32_t* meta, uint32_t* status,
+                         hipStream_t s);
 hipError_t launch_hist3(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
-                        int single, const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
-                        const uint32_t* hist2, const int32_t* cand, const uint32_t* meta,
-                        uint32_t* hist3, hipStream_t s);
+                        const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
+                        const int32_t* cand, const uint32_t* meta, uint32_t* hist3,
+                        hipStream_t s);
 hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32_t ngroups,
                             uint32_t* base, hipStream_t s);
 hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
-                       const GroupState* st, int single, const uint16_t* summ, int64_t nlines,
-                       int lpt, int32_t grid, const uint32_t* hist2, const uint32_t* hist3,
-                       const int32_t* cand, const uint32_t* meta, const uint32_t* base,
-                       uint64_t* flags, int32_t* idx_out, float* val_out, uint32_t* status,
-                       uint32_t* clear_next, int64_t clear_words, hipStream_t s);
+                       const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
+                       int32_t grid, const int32_t* cand, const uint32_t* meta,
+                       const uint32_t* base, uint64_t* flags, int32_t* idx_out, float* val_out,
+                       uint32_t* status, uint32_t* clear_next, int64_t clear_words,
+                       hipStream_t s);
 // launch-shape limits of the selection kernels
 int32_t select_max_groups();
 int32_t select_block();

@@ -5,16 +5,15 @@
 // the lower position; Alg. 1 output: ascending indices and the values of x):
 //   stream   x = g + r stored into r; 11-bit histogram of the magnitude key;
 //            one 16-bit max-key summary per 32-element line
-//   pick 1   bin of the k-th largest key (one workgroup per group)
-//   refine 2 10-bit histogram of the next key bits, only over the lines whose
-//            summary can hold a key of the chosen bin
-//   pick 2, refine 3, pick 3   the same for the last 10 bits: exact threshold
-//            key T and the tie quota `need` (elements equal to T to keep)
-//   count    per tile: #{key > T}, #{key == T}
-//   scan     exclusive prefix of those counts within each group
-//   emit     ordered compaction of the selected (idx, val); r[idx] = +0
-// Every step after the stream touches only lines whose summary reaches the
-// current key class, so for rho << 1 the data is streamed from HBM once.
+//   then a three-level radix select of the k-th largest key (11, 10 and 10
+//   bits) that reads only the lines whose summary reaches the current key
+//   class, and an ordered compaction of the selected (idx, val) with r[idx]
+//   set to +0:
+//   one group (global top-k):  collect, finish
+//   per-tensor groups:         pick 1, gather, pick 2, hist3, pick 3,
+//                              groupscan, emit
+// For rho << 1 the data is streamed from HBM once; the later kernels touch a
+// small fraction of it.
 //
 // Update (Alg. 2 accumulation of the gathered lists; Eq. (1) with optional
 // weight decay and momentum):
@@ -40,24 +39,99 @@ __device__ __forceinline__ uint32_t mag_key(float x) {
 
 constexpr uint32_t kNanKeyMin = 0x7F800001u;  // keys above +inf's are NaNs
 
-// Exclusive scan of one uint32 per thread across a kBlock-thread workgroup.
-// `buf` holds kBlock words of LDS. Returns the exclusive prefix; *total gets
-// the sum of all values.
-__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* buf,
-                                                    uint32_t* total) {
-  const int tid = threadIdx.x;
-  buf[tid] = v;
-  __syncthreads();
-  for (int off = 1; off < kBlock; off <<= 1) {
-    uint32_t add = (tid >= off) ? buf[tid - off] : 0u;
-    __syncthreads();
-    buf[tid] += add;
-    __syncthreads();
+// Inclusive prefix sum over the 64 lanes of a wavefront: DPP row shifts
+// (1, 2, 4, 8) within each row of 16 lanes, then the totals of the lower rows
+// added from readlane.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  const uint32_t t0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 15);
+  const uint32_t t1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 31);
+  const uint32_t t2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 47);
+  const int row = (int)(threadIdx.x & 63) >> 4;
+  x += (row > 0 ? t0 : 0u) + (row > 1 ? t1 : 0u) + (row > 2 ? t2 : 0u);
+  return x;
+}
+
+// Exclusive prefix sums of two values per thread over an NT-thread
+// workgroup (wave scans, then the wave totals through LDS). wsum: 2 * NT / 64
+// words of LDS. Returns the two prefixes; *total gets the two sums. Two
+// barriers; the second lets the next call reuse wsum.
+template <int NT>
+__device__ __forceinline__ uint2 block_scan2(uint32_t a, uint32_t b, uint32_t* wsum,
+                                             uint2* total) {
+  constexpr int NW = NT / 64;
+  const int tid = threadIdx.x, wid = tid >> 6;
+  const uint32_t xa = wave_incl_scan(a), xb = wave_incl_scan(b);
+  if ((tid & 63) == 63) {
+    wsum[wid] = xa;
+    wsum[NW + wid] = xb;
   }
-  uint32_t incl = buf[tid];
-  *total = buf[kBlock - 1];
   __syncthreads();
-  return incl - v;
+  uint32_t ba = 0u, bb = 0u, ta = 0u, tb = 0u;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const uint32_t sa = wsum[i], sb = wsum[NW + i];
+    ba += (i < wid) ? sa : 0u;
+    bb += (i < wid) ? sb : 0u;
+    ta += sa;
+    tb += sb;
+  }
+  *total = make_uint2(ta, tb);
+  __syncthreads();
+  return make_uint2(ba + xa - a, bb + xb - b);
+}
+
+// Exclusive prefix sums of four values per thread (same scheme and barriers).
+// wsum: 4 * NT / 64 words. pre[] and tot[] get the prefixes and the sums.
+template <int NT>
+__device__ __forceinline__ void block_scan4(const uint32_t (&v)[4], uint32_t* wsum,
+                                            uint32_t (&pre)[4], uint32_t (&tot)[4]) {
+  constexpr int NW = NT / 64;
+  const int tid = threadIdx.x, wid = tid >> 6;
+  uint32_t x[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) x[c] = wave_incl_scan(v[c]);
+  if ((tid & 63) == 63) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) wsum[c * NW + wid] = x[c];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    uint32_t b = 0u, t = 0u;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const uint32_t sv = wsum[c * NW + i];
+      b += (i < wid) ? sv : 0u;
+      t += sv;
+    }
+    pre[c] = b + x[c] - v[c];
+    tot[c] = t;
+  }
+  __syncthreads();
+}
+
+// One exclusive prefix sum over an NT-thread workgroup. wsum: NT / 64 words.
+template <int NT>
+__device__ __forceinline__ uint32_t block_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
+  constexpr int NW = NT / 64;
+  const int tid = threadIdx.x, wid = tid >> 6;
+  const uint32_t x = wave_incl_scan(v);
+  if ((tid & 63) == 63) wsum[wid] = x;
+  __syncthreads();
+  uint32_t before = 0u, all = 0u;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const uint32_t sv = wsum[i];
+    before += (i < wid) ? sv : 0u;
+    all += sv;
+  }
+  *total = all;
+  __syncthreads();
+  return before + x - v;
 }
 
 // Loads the elements [e0, e0 + n) of one line (n <= kLine) of x into v[].
@@ -284,7 +358,7 @@ __global__ __launch_bounds__(kBlock) void k_pick(int level, const GroupDesc* __r
 #pragma unroll
   for (int j = 0; j < PER; ++j) sum += c[j];
   uint32_t total;
-  const uint32_t excl = block_excl_scan(sum, part, &total);
+  const uint32_t excl = block_scan<kBlock>(sum, part, &total);
   if (excl < need && need <= excl + sum) {
     uint32_t acc = excl;
 #pragma unroll
@@ -316,21 +390,20 @@ __global__ __launch_bounds__(kBlock) void k_pick(int level, const GroupDesc* __r
 }
 
 // ---------------------------------------------------------------------------
-// Selection kernels after the level-1 pick (gather, hist3, emit).
+// Selection kernels after the stream.
 //
-// They run as at most kSMaxGroups workgroups of kSBlock threads. gather splits
-// the summary lines into contiguous ranges, one per workgroup (`lpt` lines per
-// thread, in order); hist3 and emit split the compacted candidate list the
-// same way (or the lines again, after a candidate overflow). A candidate is
-// encoded as (tile << 13) | position-in-tile.
+// They run as at most kSMaxGroups workgroups of kSBlock threads, each thread
+// owning `lpt` consecutive summary lines (or, in the per-tensor emit and
+// hist3, a run of the compacted candidate list). A candidate is encoded as
+// (tile << 13) | position-in-tile.
 //
-// Ordered output needs each workgroup's exclusive prefix of per-workgroup
-// counts. Each workgroup publishes its count in a flag word (bit 63 = valid)
-// and then reads the words of all lower-numbered workgroups. It waits only on
-// workgroups dispatched before it, which publish without waiting on anything,
-// so the wait always ends; it is still bounded (kSpinLimit polls per word),
-// after which TKEF_STATUS_TIMEOUT is recorded and the workgroup goes on. Flag
-// words are cleared before every execution.
+// The per-tensor path places its ordered output with a prefix of
+// per-workgroup counts: each workgroup publishes its count in a flag word
+// (bit 63 = valid) and then reads the words of all lower-numbered
+// workgroups. It waits only on workgroups dispatched before it, which publish
+// without waiting on anything, so the wait always ends; it is still bounded
+// (kSpinLimit polls per word), after which TKEF_STATUS_TIMEOUT is recorded and
+// the workgroup goes on. Flag words are cleared before every execution.
 constexpr int kSBlock = 1024;
 constexpr int kSWaves = kSBlock / 64;
 constexpr int kSMaxGroups = 4096;
@@ -339,6 +412,7 @@ constexpr int kCandShift = 13;   // log2(kTile)
 static_assert((1 << kCandShift) == kTile, "candidate encoding");
 constexpr uint64_t kFlagValid = 1ull << 63, kFlagVal = (1ull << 63) - 1;
 constexpr uint32_t kSpinLimit = 1u << 22;
+constexpr int kStage = 8;       // candidates a thread stages in LDS
 
 __device__ __forceinline__ uint64_t flag_load(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -356,32 +430,8 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
   return v;
 }
 
-// Exclusive scan over a kSBlock-thread workgroup (wave scans + a scan of the
-// wave totals). wsum: kSWaves words of LDS. Ends with a barrier.
 __device__ __forceinline__ uint32_t sblock_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  uint32_t x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t y = (uint32_t)__shfl_up((int)x, off);
-    if (lane >= off) x += y;
-  }
-  if (lane == 63) wsum[wid] = x;
-  __syncthreads();
-  if (wid == 0) {
-    uint32_t ws = (lane < kSWaves) ? wsum[lane] : 0u;
-#pragma unroll
-    for (int off = 1; off < kSWaves; off <<= 1) {
-      const uint32_t y = (uint32_t)__shfl_up((int)ws, off);
-      if (lane >= off) ws += y;
-    }
-    if (lane < kSWaves) wsum[lane] = ws;
-  }
-  __syncthreads();
-  const uint32_t before = wid ? wsum[wid - 1] : 0u;
-  *total = wsum[kSWaves - 1];
-  __syncthreads();
-  return before + x - v;
+  return block_scan<kSBlock>(v, wsum, total);
 }
 
 // Sum of one u64 per thread over the workgroup. red: kSWaves words of LDS.
@@ -423,32 +473,30 @@ __device__ uint64_t group_prefix(uint64_t* __restrict__ flags, uint64_t mine, ui
 
 // Within one workgroup: the bin of a 1024-bin histogram (highest bin first)
 // where the running count reaches `need`. res[] (LDS): bin, count above it,
-// count in it.
+// count in it; all zero if no bin does (need == 0 or above the total). Exactly
+// one thread writes res[], after the scan's barriers (so every reader of an
+// earlier result is done); ends with a barrier.
 __device__ __forceinline__ void sblock_pick(const uint32_t* __restrict__ hist, uint32_t need,
                                             uint32_t* wsum, uint32_t* res) {
   static_assert(kH2Bins == kSBlock && kH3Bins == kSBlock, "one bin per thread");
   const int tid = threadIdx.x;
   const int bin = kSBlock - 1 - tid;
   const uint32_t c = hist[bin];
-  __syncthreads();  // earlier readers of res[] are done
-  if (tid == 0) {
-    res[0] = 0u;
-    res[1] = 0u;
-    res[2] = 0u;
-  }
   uint32_t total;
   const uint32_t ex = sblock_scan(c, wsum, &total);
-  if (ex < need && need <= ex + c) {
-    res[0] = (uint32_t)bin;
-    res[1] = ex;
-    res[2] = c;
+  const bool found = ex < need && need <= ex + c;
+  const bool none = (need == 0u || need > total) && tid == kSBlock - 1;
+  if (found || none) {
+    res[0] = found ? (uint32_t)bin : 0u;
+    res[1] = found ? ex : 0u;
+    res[2] = found ? c : 0u;
   }
   __syncthreads();
 }
 
 // Within one workgroup: level-1 pick over a 2048-bin histogram held in
-// `nslots` copies (two bins per thread). Returns via res[]: bin, count above
-// it, count in it. Ends with a barrier.
+// `nslots` copies (two bins per thread). Returns via res[] as sblock_pick
+// does. Ends with a barrier.
 __device__ __forceinline__ void sblock_pick1(const uint32_t* __restrict__ hist1, int nslots,
                                              uint32_t need, uint32_t* wsum, uint32_t* res) {
   static_assert(kH1Bins == 2 * kSBlock, "two bins per thread");
@@ -460,12 +508,6 @@ __device__ __forceinline__ void sblock_pick1(const uint32_t* __restrict__ hist1,
     const uint2 v = *reinterpret_cast<const uint2*>(hist1 + (size_t)sl * kH1Bins + lo);
     c0 += v.x;
     c1 += v.y;
-  }
-  __syncthreads();  // earlier readers of res[] are done
-  if (tid == 0) {
-    res[0] = 0u;
-    res[1] = 0u;
-    res[2] = 0u;
   }
   uint32_t total;
   const uint32_t ex = sblock_scan(c0 + c1, wsum, &total);
@@ -479,6 +521,10 @@ __device__ __forceinline__ void sblock_pick1(const uint32_t* __restrict__ hist1,
       res[1] = ex + c1;
       res[2] = c0;
     }
+  } else if ((need == 0u || need > total) && tid == kSBlock - 1) {
+    res[0] = 0u;
+    res[1] = 0u;
+    res[2] = 0u;
   }
   __syncthreads();
 }
@@ -576,81 +622,478 @@ __device__ __forceinline__ void walk_cands(const TileDesc* __restrict__ tiles, i
 }
 
 // ---------------------------------------------------------------------------
-// gather: after the level-1 pick. Over the lines whose summary can hold a key
-// of at least the chosen bin B1: (a) histogram of key bits 19..10 of the
-// elements in bin B1 (level 2); (b) ordered compaction of all elements with
-// key >= B1 << 20 into `cand`. meta[0] = overflow (the candidates did not fit
-// in `cap`; later steps then read lines), meta[1] = candidate count.
-constexpr int kStage = 8;  // candidates / items a thread stages in LDS
+// One selection group (top-k over all tensors together): collect, finish.
+//
+// Workgroup w of either kernel owns the region of summary lines
+// [w * kSBlock * lpt, (w + 1) * kSBlock * lpt), lpt consecutive lines per
+// thread. No workgroup waits on another: the ordered output is placed from
+// small per-region counts that collect leaves behind.
+//
+// collect makes the level-1 pick (bin B1 of the k-th largest key) itself from
+// the slotted histogram. The region's flagged lines (summary >= B1 << 20) are
+// listed in LDS in position order and read one line per thread, all in one
+// round. It writes
+//   rcand[w]    the candidates (key >= B1 << 20) in position order, as
+//               {global index, bits of x, address of the residual element};
+//   rband[w]    the keys of the band members (key >> 20 == B1), ordered by
+//               level-2 bin (key bits 19..10) from the top;
+//   rsuf[w][b]  band members of the region in level-2 bins above b (written
+//               when the region has band members);
+//   gband[b]    the band members in level-2 bin b of all regions, as
+//               {key, region}, at most kBinCap per bin, in no particular
+//               order; gcnt[b] counts them (including those beyond kBinCap);
+//   rcnt[w]     {candidates | (rcand incomplete) << 31,
+//                band members | (band not stored) << 31}, counts exact;
+//   hist2       += the region's level-2 histogram.
+// A region with more than rcap candidates leaves rcand incomplete; one with
+// more than kBandCap band members stores no band keys (rband, gband). finish
+// then reads that region's lines instead.
+//
+// finish makes the level-2 pick (bin B2) from hist2, builds the level-3
+// histogram in LDS from the band members in bin B2 of all regions (rsuf tells
+// where they lie in rband) and picks the exact threshold key T and the number
+// of elements equal to T to keep. The elements above T in the regions before
+// its own are the non-band candidates, the band members above bin B2 and the
+// bin-B2 members above T; the elements equal to T are bin-B2 members. From
+// these counts workgroup w places its region's selection.
+constexpr int kOvWords = kSMaxGroups / 32;
+constexpr int kFlCap = 4096;     // flagged lines listed in LDS at a time
+constexpr int kBandCap = 4096;   // band members of a region kept in LDS
+constexpr int kC2Cap = 4096;     // level-2 class members kept in LDS by finish
+static_assert(kSMaxGroups <= 65536, "region numbers fit 16 bits");
 
+__global__ __launch_bounds__(kSBlock) void k_collect(
+    const TileDesc* __restrict__ tiles, const GroupDesc* __restrict__ groups,
+    GroupState* __restrict__ st, const uint32_t* __restrict__ hist1, int nslots,
+    const uint16_t* __restrict__ summ, int64_t nlines, int lpt, uint32_t rcap,
+    uint32_t* __restrict__ hist2, uint32_t* __restrict__ gcnt, uint2* __restrict__ gband,
+    uint4* __restrict__ rcand, uint32_t* __restrict__ rband, uint32_t* __restrict__ rsuf,
+    uint2* __restrict__ rcnt) {
+  static_assert(kH2Bins == kSBlock, "one level-2 bin per thread");
+  __shared__ uint32_t h[kH2Bins];
+  __shared__ uint32_t hoff[kH2Bins];
+  __shared__ uint32_t wsum[2 * kSWaves];
+  __shared__ uint32_t res[3];
+  __shared__ float* lptr[kFlCap];        // flagged lines: first element
+  __shared__ uint32_t lgidx[kFlCap];     // global index of the first element
+  __shared__ uint8_t lnum[kFlCap];       // elements in the line
+  __shared__ uint32_t bandk[kBandCap];
+  __shared__ uint32_t nband;
+  const int tid = threadIdx.x, w = blockIdx.x;
+  h[tid] = 0u;
+  if (tid == 0) nband = 0u;
+
+  // summaries of this thread's lines (independent of the pick), then the
+  // level-1 pick, whose barriers also publish the cleared LDS
+  LineSpan ls;
+  ls.load(tiles, summ, nlines, ((int64_t)w * kSBlock + tid) * lpt, lpt);
+  const uint32_t k = groups[0].k;
+  sblock_pick1(hist1, nslots, k, wsum, res);
+  const uint32_t B1 = res[0];
+  const uint32_t lo = B1 << kH1Shift;
+  if (w == 0 && tid == 0) {
+    GroupState s;
+    s.need = (res[1] < k) ? k - res[1] : 0u;
+    s.prefix = B1;
+    s.T = 0xFFFFFFFFu;
+    s.n_eq = 0u;
+    st[0] = s;
+  }
+
+  // flagged lines in position order: thread order, then line order
+  const uint32_t mask = ls.flagged([&](int) -> uint32_t { return lo; });
+  uint32_t F;
+  const uint32_t fex = sblock_scan((uint32_t)__popc(mask), wsum, &F);
+  uint32_t cw = 0u;   // candidates so far (workgroup-uniform)
+  bool fits = true;   // workgroup-uniform
+  uint4* __restrict__ cdst = rcand + (size_t)w * rcap;
+#pragma unroll 1
+  for (uint32_t c0 = 0; c0 < F; c0 += kFlCap) {
+    uint32_t m = mask, rank = fex;
+#pragma unroll 1
+    while (m) {
+      const int q = __ffs(m) - 1;
+      m &= m - 1u;
+      if (rank >= c0 && rank < c0 + (uint32_t)kFlCap) {
+        const TileDesc& t = ls.desc(q);
+        const int e0 = ls.e0(q);
+        lptr[rank - c0] = t.r + e0;
+        lgidx[rank - c0] = (uint32_t)(t.gstart + e0);
+        lnum[rank - c0] = (uint8_t)min(kLine, t.len - e0);
+      }
+      ++rank;
+    }
+    __syncthreads();
+    const uint32_t nl = min((uint32_t)kFlCap, F - c0);
+#pragma unroll 1
+    for (uint32_t b0 = 0; b0 < nl; b0 += kSBlock) {
+      const uint32_t i = b0 + tid;
+      float v[kLine];
+      uint32_t hm = 0u, gidx0 = 0u;
+      float* rp = nullptr;
+      if (i < nl) {
+        gidx0 = lgidx[i];
+        rp = lptr[i];
+        const int n = lnum[i];
+        load_line(rp, 0, n, v);
+#pragma unroll
+        for (int j = 0; j < kLine; ++j) {
+          const uint32_t key = mag_key(v[j]);
+          if (j < n && key >= lo) {
+            hm |= 1u << j;
+            if ((key >> kH1Shift) == B1) {
+              atomicAdd(&h[(key >> kH2Shift) & (kH2Bins - 1)], 1u);
+              const uint32_t slot = atomicAdd(&nband, 1u);
+              if (slot < (uint32_t)kBandCap) bandk[slot] = key;
+            }
+          }
+        }
+      }
+      uint32_t tot;
+      const uint32_t ex = sblock_scan((uint32_t)__popc(hm), wsum, &tot);
+      if (cw + tot > rcap) fits = false;
+      if (fits && hm) {
+        uint4* __restrict__ dst = cdst + cw + ex;
+        uint32_t o = 0u;
+#pragma unroll
+        for (int j = 0; j < kLine; ++j) {
+          if ((hm >> j) & 1u) {
+            const uint64_t a = reinterpret_cast<uint64_t>(rp + j);
+            dst[o] = make_uint4(gidx0 + (uint32_t)j, __float_as_uint(v[j]), (uint32_t)a,
+                                (uint32_t)(a >> 32));
+            ++o;
+          }
+        }
+      }
+      cw += tot;
+    }
+    __syncthreads();  // the line list is refilled next
+  }
+
+  // band members by level-2 bin from the top (thread tid owns bin 1023 - tid):
+  // sorted into rband[w] and appended to their bin's global list, whose slots
+  // for this region start at the value the bin's counter had
+  const int bin = kH2Bins - 1 - tid;
+  const uint32_t cb = h[bin];
+  uint32_t bw;
+  const uint32_t above = sblock_scan(cb, wsum, &bw);
+  const bool band_ok = bw <= (uint32_t)kBandCap;  // every band key is in bandk
+  if (cb) atomicAdd(&hist2[bin], cb);
+  const uint32_t gbase = (cb && band_ok) ? atomicAdd(&gcnt[bin], cb) : 0u;
+  if (bw) rsuf[(size_t)w * kH2Bins + bin] = above;
+  h[bin] = above;          // from here on: the bin's next slot in rband[w]
+  hoff[bin] = gbase - above;  // + that slot = the member's slot in gband[bin]
+  __syncthreads();
+  if (band_ok) {
+    uint32_t* __restrict__ dst = rband + (size_t)w * rcap;
+    for (uint32_t j = tid; j < bw; j += kSBlock) {
+      const uint32_t key = bandk[j];
+      const uint32_t b2 = (key >> kH2Shift) & (kH2Bins - 1);
+      const uint32_t slot = atomicAdd(&h[b2], 1u);
+      dst[slot] = key;
+      const uint32_t gs = hoff[b2] + slot;
+      if (gs < (uint32_t)kBinCap) gband[(size_t)b2 * kBinCap + gs] = make_uint2(key, (uint32_t)w);
+    }
+  }
+  if (tid == 0)
+    rcnt[w] = make_uint2(cw | ((fits ? 0u : 1u) << 31), bw | ((band_ok ? 0u : 1u) << 31));
+}
+
+// Calls f(key) for the level-2 class members (band members in bin B2) of the
+// stored regions among [0, wlim), reading them again from rband. Regions are
+// taken kSBlock at a time and their members spread over the workgroup through
+// a scan of the per-region counts. off, abv: kSBlock words of LDS each.
+// Uniform in the workgroup.
+template <typename F>
+__device__ __forceinline__ void for_class2(int wlim, uint32_t B2, uint32_t rcap,
+                                           const uint2* __restrict__ rcnt,
+                                           const uint32_t* __restrict__ rsuf,
+                                           const uint32_t* __restrict__ rband, uint32_t* off,
+                                           uint32_t* abv, uint32_t* wsum, F f) {
+  const int tid = threadIdx.x;
+#pragma unroll 1
+  for (int r0 = 0; r0 < wlim; r0 += kSBlock) {
+    const int r = r0 + tid;
+    uint32_t above = 0u, at = 0u;
+    if (r < wlim) {
+      const uint2 cnt = rcnt[r];
+      const uint32_t bw = cnt.y & 0x7FFFFFFFu;
+      if (bw && !(cnt.y >> 31)) {
+        const uint32_t* sr = rsuf + (size_t)r * kH2Bins;
+        above = sr[B2];
+        at = (B2 ? sr[B2 - 1] : bw) - above;
+      }
+    }
+    uint32_t tot;
+    const uint32_t ex = sblock_scan(at, wsum, &tot);
+    off[tid] = ex;
+    abv[tid] = above;
+    __syncthreads();
+#pragma unroll 1
+    for (uint32_t j = tid; j < tot; j += kSBlock) {
+      int a = 0, b = kSBlock - 1;  // the last region slot with off <= j holds member j
+      while (a < b) {
+        const int m = (a + b + 1) >> 1;
+        if (off[m] <= j) a = m; else b = m - 1;
+      }
+      f(rband[(size_t)(r0 + a) * rcap + abv[a] + (j - off[a])]);
+    }
+    __syncthreads();
+  }
+}
+
+constexpr int kRegPerThread = kSMaxGroups / kSBlock;
+
+__global__ __launch_bounds__(kSBlock) void k_finish(
+    const TileDesc* __restrict__ tiles, const GroupDesc* __restrict__ groups,
+    const GroupState* __restrict__ st, const uint16_t* __restrict__ summ, int64_t nlines,
+    int lpt, uint32_t rcap, const uint32_t* __restrict__ hist2,
+    const uint32_t* __restrict__ gcnt, const uint2* __restrict__ gband,
+    const uint4* __restrict__ rcand, const uint32_t* __restrict__ rband,
+    const uint32_t* __restrict__ rsuf, const uint2* __restrict__ rcnt,
+    int32_t* __restrict__ idx_out, float* __restrict__ val_out,
+    uint32_t* __restrict__ clear_next, int64_t clear_words) {
+  __shared__ uint32_t h[kH3Bins];
+  __shared__ uint32_t wsum[4 * kSWaves];
+  __shared__ uint32_t res[3];
+  __shared__ uint32_t off[kSBlock], abv[kSBlock];
+  __shared__ uint32_t ovbits[kOvWords];  // regions whose band keys were not stored
+  __shared__ uint32_t c2key[kC2Cap];     // level-2 class members of the stored regions
+  __shared__ uint16_t c2reg[kC2Cap];     // ... and their regions
+  __shared__ uint32_t n2;
+  const int tid = threadIdx.x, w = blockIdx.x, G = gridDim.x;
+  // clear the other copy of the zero-initialised scratch for the next run
+#pragma unroll 1
+  for (int64_t i = (int64_t)w * kSBlock + tid; i < clear_words; i += (int64_t)G * kSBlock)
+    clear_next[i] = 0u;
+  h[tid] = 0u;
+  for (int i = tid; i < kOvWords; i += kSBlock) ovbits[i] = 0u;
+  if (tid == 0) n2 = 0u;
+
+  // fetched together: level-1 state, this region's counts and first
+  // candidate, every region's counts (and, in the pick, the level-2 histogram)
+  const GroupState s0 = st[0];
+  const uint32_t k = groups[0].k;
+  const uint2 mine = rcnt[w];
+  const bool own_ov = (mine.x >> 31) != 0u;
+  const uint4* __restrict__ mc = rcand + (size_t)w * rcap;
+  uint32_t cb = 0u, ce = 0u;
+  if (!own_ov) {
+    const uint32_t per = (mine.x + kSBlock - 1) / kSBlock;
+    cb = min(mine.x, tid * per);
+    ce = min(mine.x, cb + per);
+  }
+  const uint4 v0 = (cb < ce) ? mc[cb] : make_uint4(0u, 0u, 0u, 0u);
+  uint2 cr[kRegPerThread];
+#pragma unroll
+  for (int q = 0; q < kRegPerThread; ++q) {
+    const int r = q * kSBlock + tid;
+    cr[q] = (r < G) ? rcnt[r] : make_uint2(0u, 0u);
+  }
+
+  // level 2 (the pick's barriers also publish the cleared LDS above)
+  sblock_pick(hist2, s0.need, wsum, res);
+  const uint32_t B2 = res[0];
+  const uint32_t need2 = (res[1] < s0.need) ? s0.need - res[1] : 0u;
+  const uint32_t cls21 = (s0.prefix << 10) | B2;
+
+  // The level-2 class (band members in bin B2): the bin's global list, and
+  // per earlier region the band members above bin B2 (from rsuf). gtb: this
+  // thread's share of the elements above T before region w.
+  const uint32_t gc = gcnt[B2];
+  const uint2 ge = (tid < kBinCap) ? gband[(size_t)B2 * kBinCap + tid] : make_uint2(0u, 0u);
+  uint32_t gtb = 0u;
+#pragma unroll
+  for (int q = 0; q < kRegPerThread; ++q) {
+    const int r = q * kSBlock + tid;
+    const uint32_t bw = cr[q].y & 0x7FFFFFFFu;
+    if (r < G && (cr[q].y >> 31)) atomicOr(&ovbits[r >> 5], 1u << (r & 31));
+    if (r < w) gtb += (cr[q].x & 0x7FFFFFFFu) - bw + (bw ? rsuf[(size_t)r * kH2Bins + B2] : 0u);
+  }
+  if (gc <= (uint32_t)kBinCap) {
+    if ((uint32_t)tid < gc) {
+      atomicAdd(&h[ge.x & (kH3Bins - 1)], 1u);
+      c2key[tid] = ge.x;
+      c2reg[tid] = (uint16_t)ge.y;
+    }
+    if (tid == 0) n2 = gc;
+    __syncthreads();
+  } else {
+    // more than kBinCap members: every stored region's through rsuf / rband
+#pragma unroll 1
+    for (int r0 = 0; r0 < G; r0 += kSBlock) {
+      const int r = r0 + tid;
+      uint32_t above = 0u, at = 0u;
+      if (r < G) {
+        const uint2 cnt = rcnt[r];
+        const uint32_t bw = cnt.y & 0x7FFFFFFFu;
+        if (bw && !(cnt.y >> 31)) {
+          const uint32_t* sr = rsuf + (size_t)r * kH2Bins;
+          above = sr[B2];
+          at = (B2 ? sr[B2 - 1] : bw) - above;
+        }
+      }
+      uint32_t tot;
+      const uint32_t ex = sblock_scan(at, wsum, &tot);
+      off[tid] = ex;
+      abv[tid] = above;
+      __syncthreads();
+#pragma unroll 1
+      for (uint32_t j = tid; j < tot; j += kSBlock) {
+        int a = 0, b = kSBlock - 1;  // the last region slot with off <= j holds member j
+        while (a < b) {
+          const int m = (a + b + 1) >> 1;
+          if (off[m] <= j) a = m; else b = m - 1;
+        }
+        const uint32_t key = rband[(size_t)(r0 + a) * rcap + abv[a] + (j - off[a])];
+        atomicAdd(&h[key & (kH3Bins - 1)], 1u);
+        const uint32_t slot = atomicAdd(&n2, 1u);
+        if (slot < (uint32_t)kC2Cap) {
+          c2key[slot] = key;
+          c2reg[slot] = (uint16_t)(r0 + a);
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // class-2 members of the regions without stored band keys: from their lines
+  const uint32_t thr2 = cls21 << kH2Shift;
+  auto in_cls2 = [&](int, uint32_t key) -> bool { return (key >> kH2Shift) == cls21; };
+  auto lines_class2 = [&](int wlim, auto f) {
+#pragma unroll 1
+    for (int wi = 0; wi * 32 < wlim; ++wi) {
+      uint32_t m = ovbits[wi];
+#pragma unroll 1
+      while (m) {
+        const int r = wi * 32 + __ffs(m) - 1;
+        m &= m - 1u;
+        if (r >= wlim) break;
+        LineSpan lr;
+        lr.load(tiles, summ, nlines, ((int64_t)r * kSBlock + tid) * lpt, lpt);
+        walk_mask(lr, lr.flagged([&](int) -> uint32_t { return thr2; }), in_cls2,
+                  [&](int, const TileDesc&, int, float, uint32_t key) { f(key); });
+      }
+    }
+  };
+  lines_class2(G, [&](uint32_t key) { atomicAdd(&h[key & (kH3Bins - 1)], 1u); });
+  __syncthreads();
+  sblock_pick(h, need2, wsum, res);
+  const uint32_t T = (cls21 << 10) | res[0];
+  const uint32_t need3 = (res[1] < need2) ? need2 - res[1] : 0u;
+
+  // class-2 members above T and equal to T in the regions before this one
+  uint32_t eqb = 0u;
+  auto tally = [&](uint32_t key) {
+    gtb += (key > T) ? 1u : 0u;
+    eqb += (key == T) ? 1u : 0u;
+  };
+  if (n2 <= (uint32_t)kC2Cap) {
+    for (uint32_t j = tid; j < n2; j += kSBlock)
+      if ((int)c2reg[j] < w) tally(c2key[j]);
+  } else {
+    for_class2(w, B2, rcap, rcnt, rsuf, rband, off, abv, wsum, tally);
+  }
+  lines_class2(w, tally);
+
+  // this region: its stored candidates (a run per thread), or its lines.
+  // Counts of (key > T) and (key == T) in position order.
+  LineSpan ls;
+  uint32_t mask = 0u;
+  if (own_ov) {
+    ls.load(tiles, summ, nlines, ((int64_t)w * kSBlock + tid) * lpt, lpt);
+    mask = ls.flagged([&](int) -> uint32_t { return T; });
+  }
+  auto at_least_T = [&](int, uint32_t key) -> bool { return key >= T; };
+  uint32_t gt = 0u, eq = 0u;
+  auto count = [&](float x) {
+    const uint32_t key = mag_key(x);
+    gt += (key > T) ? 1u : 0u;
+    eq += (key == T) ? 1u : 0u;
+  };
+  if (own_ov) {
+    walk_mask(ls, mask, at_least_T,
+              [&](int, const TileDesc&, int, float x, uint32_t) { count(x); });
+  } else {
+#pragma unroll 1
+    for (uint32_t j = cb; j < ce; ++j) count(__uint_as_float(((j == cb) ? v0 : mc[j]).y));
+  }
+  const uint32_t sv[4] = {gt, eq, gtb, eqb};
+  uint32_t pre[4], tot[4];
+  block_scan4<kSBlock>(sv, wsum, pre, tot);
+  if (gt + eq == 0u) return;
+  uint32_t gtr = tot[2] + pre[0];
+  uint32_t eqr = tot[3] + pre[1];
+  // write
+  auto write = [&](uint32_t gidx, float* rp, float x) {
+    const uint32_t key = mag_key(x);
+    if (key < T) return;
+    uint32_t pos = 0xFFFFFFFFu;
+    if (key > T) {
+      pos = gtr + min(eqr, need3);
+      ++gtr;
+    } else {
+      if (eqr < need3) pos = gtr + eqr;
+      ++eqr;
+    }
+    if (pos < k) {
+      idx_out[pos] = (int32_t)gidx;
+      val_out[pos] = x;
+      *rp = 0.0f;
+    }
+  };
+  if (own_ov) {
+    walk_mask(ls, mask, at_least_T, [&](int, const TileDesc& t, int e, float x, uint32_t) {
+      write((uint32_t)(t.gstart + e), t.r + e, x);
+    });
+  } else {
+#pragma unroll 1
+    for (uint32_t j = cb; j < ce; ++j) {
+      const uint4 v = (j == cb) ? v0 : mc[j];
+      write(v.x, reinterpret_cast<float*>(((uint64_t)v.w << 32) | v.z), __uint_as_float(v.y));
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Several selection groups (per-tensor top-k): pick 1, gather, pick 2, hist3,
+// pick 3, groupscan, emit. The picks run as k_pick, one workgroup per group.
+//
+// gather: over the lines whose summary can hold a key of at least the
+// group's level-1 bin B1: (a) the level-2 histogram of the elements in bin
+// B1; (b) ordered compaction of all elements with key >= B1 << 20 into
+// `cand`. meta[0] = overflow (the candidates did not fit in `cap`; later
+// steps then read lines), meta[1] = candidate count.
 __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__ tiles,
-                                                    const GroupDesc* __restrict__ groups,
-                                                    GroupState* __restrict__ st,
-                                                    const uint32_t* __restrict__ hist1, int nslots,
-                                                    int single, const uint16_t* __restrict__ summ,
+                                                    const GroupState* __restrict__ st,
+                                                    const uint16_t* __restrict__ summ,
                                                     int64_t nlines, int lpt,
                                                     uint32_t* __restrict__ hist2,
                                                     uint64_t* __restrict__ flags,
                                                     int32_t* __restrict__ cand, uint32_t cap,
                                                     uint32_t* __restrict__ meta,
                                                     uint32_t* __restrict__ status) {
-  __shared__ uint32_t h[kH2Bins];
-  __shared__ uint32_t wsum[kSWaves];
+  __shared__ uint32_t wsum[2 * kSWaves];
   __shared__ uint64_t red[kSWaves];
-  __shared__ uint32_t res[3];
   __shared__ int32_t stage[kStage * kSBlock];  // [slot][thread]
-  __shared__ uint32_t any;
   const int tid = threadIdx.x;
-  h[tid] = 0u;
-  if (tid == 0) any = 0u;
-
-  // 1. summaries and tiles of this thread's lines (independent of the pick)
   LineSpan ls;
   ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
-
-  // 2. level-1 pick. One selection group: every workgroup makes it itself
-  //    from the slotted histogram and workgroup 0 records it for the later
-  //    kernels. Several groups: the pick kernel has done it.
-  GroupState s0;
-  if (single) {
-    const uint32_t k = groups[0].k;
-    sblock_pick1(hist1, nslots, k, wsum, res);
-    s0.prefix = (k == 0u) ? 0xFFFFFFFFu : res[0];
-    s0.need = (k == 0u || res[1] >= k) ? 0u : k - res[1];
-    s0.T = 0xFFFFFFFFu;
-    s0.n_eq = 0u;
-    if (blockIdx.x == 0 && tid == 0) st[0] = s0;
-  } else {
-    s0 = st[0];
-  }
   // B1 = 0xFFFFFFFF for a group with nothing to select: shifted, it lies
   // above every key, so such a group yields no candidates
-  auto b1_of = [&](int g) -> uint32_t { return single ? s0.prefix : st[g].prefix; };
-  const uint32_t b1A = b1_of(ls.tA.group), b1B = b1_of(ls.tB.group);
-  const uint32_t mask = ls.flagged([&](int g) -> uint32_t {
-    return (g == ls.tA.group ? b1A : b1B) << kH1Shift;
-  });
-
-  // 3. count the candidates of the flagged lines; stage the first kStage in LDS
-  auto is_cand = [&](int g, uint32_t k) -> bool {
-    return k >= ((g == ls.tA.group ? b1A : b1B) << kH1Shift);
-  };
-  uint32_t c = 0u, hit = 0u;
+  const uint32_t b1A = st[ls.tA.group].prefix, b1B = st[ls.tB.group].prefix;
+  auto b1_of = [&](int g) -> uint32_t { return g == ls.tA.group ? b1A : b1B; };
+  const uint32_t mask = ls.flagged([&](int g) -> uint32_t { return b1_of(g) << kH1Shift; });
+  auto is_cand = [&](int g, uint32_t k) -> bool { return k >= (b1_of(g) << kH1Shift); };
+  uint32_t c = 0u;
   walk_mask(ls, mask, is_cand, [&](int tile, const TileDesc& t, int e, float, uint32_t k) {
-    const uint32_t b1 = (t.group == ls.tA.group) ? b1A : b1B;
     if (c < (uint32_t)kStage)
       stage[c * kSBlock + tid] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
     ++c;
-    if ((k >> kH1Shift) == b1) {
-      const uint32_t bin = (k >> kH2Shift) & (kH2Bins - 1);
-      if (single) atomicAdd(&h[bin], 1u);
-      else atomicAdd(&hist2[(size_t)t.group * kH2Bins + bin], 1u);
-      hit = 1u;
-    }
+    if ((k >> kH1Shift) == b1_of(t.group))
+      atomicAdd(&hist2[(size_t)t.group * kH2Bins + ((k >> kH2Shift) & (kH2Bins - 1))], 1u);
   });
-  if (hit) any = 1u;
 
-  // 4. ordered positions: scan within the workgroup, prefix across workgroups
+  // ordered positions: scan within the workgroup, prefix across workgroups
   uint32_t total;
   const uint32_t ex = sblock_scan(c, wsum, &total);
   const uint64_t pre = group_prefix(flags, total, red, status);
@@ -673,63 +1116,28 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
       });
     }
   }
-  if (single && any) {  // `any` was written before the scans' barriers
-    const uint32_t v = h[tid];
-    if (v) atomicAdd(&hist2[tid], v);
-  }
 }
 
-// Level-2 state of a group: redundant per workgroup for a single group (from
-// the level-2 histogram), else written by the pick kernel.
-__device__ __forceinline__ void sel_level2(const GroupState& s1, const uint32_t* __restrict__ hist2,
-                                           uint32_t* wsum, uint32_t* res, uint32_t* cls21,
-                                           uint32_t* need2) {
-  sblock_pick(hist2, s1.need, wsum, res);
-  *cls21 = (s1.prefix << 10) | res[0];
-  *need2 = (res[1] < s1.need) ? s1.need - res[1] : 0u;
-}
-
-// ---------------------------------------------------------------------------
-// hist3: histogram of the low 10 key bits over the level-2 class
-// (key >> 10 == prefix of 21 bits), read from the candidates (or the lines).
+// hist3: per-group histogram of the low 10 key bits over the group's level-2
+// class (key >> 10 == its 21-bit prefix), read from the candidates (or the
+// lines after an overflow).
 __global__ __launch_bounds__(kSBlock) void k_hist3(const TileDesc* __restrict__ tiles,
                                                    int32_t ntiles,
                                                    const GroupState* __restrict__ st,
-                                                   int single, const uint16_t* __restrict__ summ,
+                                                   const uint16_t* __restrict__ summ,
                                                    int64_t nlines, int lpt,
-                                                   const uint32_t* __restrict__ hist2,
                                                    const int32_t* __restrict__ cand,
                                                    const uint32_t* __restrict__ meta,
                                                    uint32_t* __restrict__ hist3) {
-  __shared__ uint32_t h[kH3Bins];
-  __shared__ uint32_t wsum[kSWaves];
-  __shared__ uint32_t res[3];
-  __shared__ uint32_t any;
   const int tid = threadIdx.x;
   const uint32_t ov = meta[0], C = meta[1];
-  const GroupState s0 = st[0];
-  h[tid] = 0u;
-  if (tid == 0) any = 0u;
-  uint32_t cls_single = 0xFFFFFFFFu, need_single = 0u;
-  if (single) {
-    sel_level2(s0, hist2, wsum, res, &cls_single, &need_single);
-  } else {
-    __syncthreads();
-  }
   auto cls_of = [&](int g) -> uint32_t {
-    if (single) return need_single ? cls_single : 0xFFFFFFFFu;
     const GroupState sg = st[g];
     return sg.need ? sg.prefix : 0xFFFFFFFFu;
   };
-  uint32_t hit = 0u;
   auto in_cls = [&](int g, uint32_t k) -> bool { return (k >> kH2Shift) == cls_of(g); };
   auto body = [&](int, const TileDesc& t, int, float, uint32_t k) {
-    if (in_cls(t.group, k)) {
-      const uint32_t bin = k & (kH3Bins - 1);
-      if (single) atomicAdd(&h[bin], 1u);
-      else atomicAdd(&hist3[(size_t)t.group * kH3Bins + bin], 1u);
-      hit = 1u;
-    }
+    if (in_cls(t.group, k)) atomicAdd(&hist3[(size_t)t.group * kH3Bins + (k & (kH3Bins - 1))], 1u);
   };
   if (ov) {
     LineSpan ls;
@@ -742,22 +1150,15 @@ __global__ __launch_bounds__(kSBlock) void k_hist3(const TileDesc* __restrict__ 
 #pragma unroll 1
     for (uint32_t j = wb + tid; j < we; j += kSBlock) walk_cands(tiles, ntiles, cand, j, j + 1, body);
   }
-  if (hit) any = 1u;
-  __syncthreads();
-  if (single && any) {
-    const uint32_t v = h[tid];
-    if (v) atomicAdd(&hist3[tid], v);
-  }
 }
 
-// ---------------------------------------------------------------------------
-// groupscan (per-tensor selections only): base[2g] = sum over earlier groups
-// of #{key > T}, base[2g + 1] = the same for #{key == T}.
+// groupscan: base[2g] = sum over earlier groups of #{key > T}, base[2g + 1] =
+// the same for #{key == T} (counting only the equal keys that are kept).
 __global__ __launch_bounds__(kSBlock) void k_groupscan(const GroupDesc* __restrict__ groups,
                                                        const GroupState* __restrict__ st,
                                                        int32_t ngroups,
                                                        uint32_t* __restrict__ base) {
-  __shared__ uint32_t wsum[kSWaves];
+  __shared__ uint32_t wsum[2 * kSWaves];
   const int tid = threadIdx.x;
   uint32_t carry_gt = 0u, carry_eq = 0u;
   for (int g0 = 0; g0 < ngroups; g0 += kSBlock) {
@@ -769,32 +1170,28 @@ __global__ __launch_bounds__(kSBlock) void k_groupscan(const GroupDesc* __restri
       gt = (k > s.need) ? k - s.need : 0u;
       eq = s.need ? s.n_eq : 0u;
     }
-    uint32_t tg, te;
-    const uint32_t xg = sblock_scan(gt, wsum, &tg);
-    const uint32_t xe = sblock_scan(eq, wsum, &te);
+    uint2 t;
+    const uint2 x = block_scan2<kSBlock>(gt, eq, wsum, &t);
     if (g < ngroups) {
-      base[2 * g] = carry_gt + xg;
-      base[2 * g + 1] = carry_eq + xe;
+      base[2 * g] = carry_gt + x.x;
+      base[2 * g + 1] = carry_eq + x.y;
     }
-    carry_gt += tg;
-    carry_eq += te;
+    carry_gt += t.x;
+    carry_eq += t.y;
   }
 }
 
-// ---------------------------------------------------------------------------
 // emit: ordered compaction of the selection. An element of group g with
-// key > T_g goes to slot (#gt before it in g) + min(#eq before it in g, need_g);
-// an element with key == T_g is kept while fewer than need_g equal keys
-// precede it in g. Counts before an element are global prefixes (over the
-// candidate list, in position order) minus the group's base.
+// key > T_g goes to slot (#gt before it in g) + min(#eq before it in g,
+// need_g); an element with key == T_g is kept while fewer than need_g equal
+// keys precede it in g. Counts before an element are global prefixes (over
+// the candidate list, in position order) minus the group's base.
 __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ tiles,
                                                   int32_t ntiles,
                                                   const GroupDesc* __restrict__ groups,
-                                                  const GroupState* __restrict__ st, int single,
+                                                  const GroupState* __restrict__ st,
                                                   const uint16_t* __restrict__ summ,
                                                   int64_t nlines, int lpt,
-                                                  const uint32_t* __restrict__ hist2,
-                                                  const uint32_t* __restrict__ hist3,
                                                   const int32_t* __restrict__ cand,
                                                   const uint32_t* __restrict__ meta,
                                                   const uint32_t* __restrict__ base,
@@ -804,9 +1201,8 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
                                                   uint32_t* __restrict__ status,
                                                   uint32_t* __restrict__ clear_next,
                                                   int64_t clear_words) {
-  __shared__ uint32_t wsum[kSWaves];
+  __shared__ uint32_t wsum[2 * kSWaves];
   __shared__ uint64_t red[kSWaves];
-  __shared__ uint32_t res[3];
   __shared__ int32_t stage_code[kStage * kSBlock];  // [slot][thread]: (tile << 13) | e
   __shared__ float stage_x[kStage * kSBlock];
   const int tid = threadIdx.x;
@@ -816,19 +1212,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
        i += (int64_t)gridDim.x * kSBlock)
     clear_next[i] = 0u;
   const uint32_t ov = meta[0], C = meta[1];
-  const GroupState s0 = st[0];
-  const GroupDesc gd0 = groups[0];
-  uint32_t T_one = 0xFFFFFFFFu, need_one = 0u;
-  if (single) {
-    uint32_t cls21, need2;
-    sel_level2(s0, hist2, wsum, res, &cls21, &need2);
-    sblock_pick(hist3, need2, wsum, res);
-    if (s0.need != 0u && need2 != 0u) {
-      T_one = (cls21 << 10) | res[0];
-      need_one = (res[1] < need2) ? need2 - res[1] : 0u;
-    }
-  }
-  auto T_of = [&](int g) -> uint32_t { return single ? T_one : st[g].T; };
+  auto T_of = [&](int g) -> uint32_t { return st[g].T; };
   // this thread's elements: a run of candidates, or (after an overflow) lines
   LineSpan ls;
   uint32_t mask = 0u, cb = 0u, ce = 0u;
@@ -860,21 +1244,20 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
   auto at_least_T = [&](int g, uint32_t k) -> bool { return k >= T_of(g); };
   if (ov) walk_mask(ls, mask, at_least_T, count);
   else walk_cands(tiles, ntiles, cand, cb, ce, count);
-  uint32_t tot_gt, tot_eq;
-  const uint32_t xg = sblock_scan(gt, wsum, &tot_gt);
-  const uint32_t xe = sblock_scan(eq, wsum, &tot_eq);
-  const uint64_t pre = group_prefix(flags, (uint64_t)tot_gt | ((uint64_t)tot_eq << 31), red, status);
+  uint2 tot;
+  const uint2 x2 = block_scan2<kSBlock>(gt, eq, wsum, &tot);
+  const uint64_t pre = group_prefix(flags, (uint64_t)tot.x | ((uint64_t)tot.y << 31), red, status);
   if (nst == 0u) return;
-  uint32_t gtr = (uint32_t)(pre & 0x7FFFFFFFu) + xg;
-  uint32_t eqr = (uint32_t)((pre >> 31) & 0x7FFFFFFFu) + xe;
+  uint32_t gtr = (uint32_t)(pre & 0x7FFFFFFFu) + x2.x;
+  uint32_t eqr = (uint32_t)((pre >> 31) & 0x7FFFFFFFu) + x2.y;
   // pass 2: write
   auto write = [&](int, const TileDesc& t, int e, float x, uint32_t k) {
     const int g = t.group;
     const uint32_t T = T_of(g);
     if (k < T) return;
-    const GroupDesc gd = single ? gd0 : groups[g];
-    const uint32_t need = single ? need_one : st[g].need;
-    const uint32_t bg = single ? 0u : base[2 * g], be = single ? 0u : base[2 * g + 1];
+    const GroupDesc gd = groups[g];
+    const uint32_t need = st[g].need;
+    const uint32_t bg = base[2 * g], be = base[2 * g + 1];
     uint32_t pos = 0xFFFFFFFFu;
     if (k > T) {
       pos = (gtr - bg) + min(eqr - be, need);
@@ -1023,9 +1406,9 @@ __global__ __launch_bounds__(kUBlock) void k_update(
     }
     sbeg[tid] = b;
     // inclusive prefix of the segment lengths, for the entry -> worker search
-    // (block_excl_scan ends with a barrier, so scan[] can be rewritten here)
+    // (block_scan ends with a barrier, so scan[] can be rewritten here)
     uint32_t total;
-    const uint32_t ex = block_excl_scan((uint32_t)(e - b), scan, &total);
+    const uint32_t ex = block_scan<kUBlock>((uint32_t)(e - b), scan, &total);
     scan[tid] = ex + (uint32_t)(e - b);
     __syncthreads();
     // entries of this batch of workers, kPairUnroll per thread with all
@@ -1171,22 +1554,47 @@ hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
   return hipGetLastError();
 }
 
-hipError_t launch_gather(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
-                         const uint32_t* hist1, int nslots, int single, const uint16_t* summ,
-                         int64_t nlines, int lpt, int32_t grid, uint32_t* hist2,
-                         uint64_t* flags, int32_t* cand, uint32_t cap, uint32_t* meta,
-                         uint32_t* status, hipStream_t s) {
-  hipLaunchKernelGGL(k_gather, dim3(grid), dim3(kSBlock), 0, s, tiles, groups, st, hist1, nslots,
-                     single, summ, nlines, lpt, hist2, flags, cand, cap, meta, status);
+hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
+                          const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
+                          int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* gcnt,
+                          uint32_t* gband, uint32_t* rcand, uint32_t* rband, uint32_t* rsuf,
+                          uint32_t* rcnt, hipStream_t s) {
+  hipLaunchKernelGGL(k_collect, dim3(grid), dim3(kSBlock), 0, s, tiles, groups, st, hist1, nslots,
+                     summ, nlines, lpt, rcap, hist2, gcnt, reinterpret_cast<uint2*>(gband),
+                     reinterpret_cast<uint4*>(rcand), rband, rsuf, reinterpret_cast<uint2*>(rcnt));
+  return hipGetLastError();
+}
+
+hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
+                         const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
+                         int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* gcnt,
+                         const uint32_t* gband, const uint32_t* rcand, const uint32_t* rband,
+                         const uint32_t* rsuf, const uint32_t* rcnt, int32_t* idx_out,
+                         float* val_out, uint32_t* clear_next, int64_t clear_words,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(k_finish, dim3(grid), dim3(kSBlock), 0, s, tiles, groups, st, summ,
+                     nlines, lpt, rcap, hist2, gcnt, reinterpret_cast<const uint2*>(gband),
+                     reinterpret_cast<const uint4*>(rcand), rband, rsuf,
+                     reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, clear_next,
+                     clear_words);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
+                         int64_t nlines, int lpt, int32_t grid, uint32_t* hist2, uint64_t* flags,
+                         int32_t* cand, uint32_t cap, uint32_t* meta, uint32_t* status,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(k_gather, dim3(grid), dim3(kSBlock), 0, s, tiles, st, summ, nlines, lpt,
+                     hist2, flags, cand, cap, meta, status);
   return hipGetLastError();
 }
 
 hipError_t launch_hist3(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
-                        int single, const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
-                        const uint32_t* hist2, const int32_t* cand, const uint32_t* meta,
-                        uint32_t* hist3, hipStream_t s) {
-  hipLaunchKernelGGL(k_hist3, dim3(grid), dim3(kSBlock), 0, s, tiles, ntiles, st, single, summ,
-                     nlines, lpt, hist2, cand, meta, hist3);
+                        const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
+                        const int32_t* cand, const uint32_t* meta, uint32_t* hist3,
+                        hipStream_t s) {
+  hipLaunchKernelGGL(k_hist3, dim3(grid), dim3(kSBlock), 0, s, tiles, ntiles, st, summ, nlines,
+                     lpt, cand, meta, hist3);
   return hipGetLastError();
 }
 
@@ -1197,14 +1605,14 @@ hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32
 }
 
 hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
-                       const GroupState* st, int single, const uint16_t* summ, int64_t nlines,
-                       int lpt, int32_t grid, const uint32_t* hist2, const uint32_t* hist3,
-                       const int32_t* cand, const uint32_t* meta, const uint32_t* base,
-                       uint64_t* flags, int32_t* idx_out, float* val_out, uint32_t* status,
-                       uint32_t* clear_next, int64_t clear_words, hipStream_t s) {
-  hipLaunchKernelGGL(k_emit, dim3(grid), dim3(kSBlock), 0, s, tiles, ntiles, groups, st, single, summ,
-                     nlines, lpt, hist2, hist3, cand, meta, base, flags, idx_out, val_out,
-                     status, clear_next, clear_words);
+                       const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
+                       int32_t grid, const int32_t* cand, const uint32_t* meta,
+                       const uint32_t* base, uint64_t* flags, int32_t* idx_out, float* val_out,
+                       uint32_t* status, uint32_t* clear_next, int64_t clear_words,
+                       hipStream_t s) {
+  hipLaunchKernelGGL(k_emit, dim3(grid), dim3(kSBlock), 0, s, tiles, ntiles, groups, st, summ,
+                     nlines, lpt, cand, meta, base, flags, idx_out, val_out, status, clear_next,
+                     clear_words);
   return hipGetLastError();
 }
 
