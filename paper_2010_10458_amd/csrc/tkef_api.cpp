@@ -115,7 +115,7 @@ struct tkef_sparsify_plan_s {
   size_t off_tiles = 0, off_groups = 0, off_state = 0, off_zero[2] = {0, 0}, zero_bytes = 0,
          off_hist1 = 0, off_hist2 = 0, off_hist3 = 0, off_flags1 = 0, off_flags2 = 0,
          off_meta = 0, off_summ = 0, off_base = 0, off_cand = 0, off_rcand = 0, off_rband = 0,
-         off_rsuf = 0, off_rcnt = 0, off_gcnt = 0, off_gband = 0, ws_bytes = 0;
+         off_rsuf = 0, off_rcnt = 0, off_rbin = 0, ws_bytes = 0;
   uint64_t executions = 0;   // since the last bind
   bool needs_clear = true;   // both copies must be cleared before the next run
   int32_t nlaunch() const { return ngroups == 1 ? kSparsifyNLaunchOne : kSparsifyNLaunchMany; }
@@ -188,10 +188,13 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     p->nlines = (int64_t)p->ntiles * kLinesPerTile;
     // selection kernels: `lpt` consecutive summary lines per thread, at most
     // select_max_groups() workgroups of select_block() threads. Aim for about
-    // 256 workgroups (one per compute unit) with at least two lines per thread.
+    // 256 workgroups (one per compute unit); lpt is a power of two from 4 up
+    // (the kernels fetch four 16-bit summaries per load, and a thread's lines
+    // must lie in one tile).
     const int64_t sb = select_block(), sg = select_max_groups();
-    int64_t lpt = std::max<int64_t>(2, (p->nlines + sb * 256 - 1) / (sb * 256));
-    lpt = std::min<int64_t>(lpt, select_max_lpt());
+    const int64_t want = (p->nlines + sb * 256 - 1) / (sb * 256);
+    int64_t lpt = 4;  // a power of two from 4 to select_max_lpt()
+    while (lpt < want && lpt < select_max_lpt()) lpt *= 2;
     if ((p->nlines + sb * lpt - 1) / (sb * lpt) > sg) throw std::bad_alloc();  // d < 2^31
     p->sel_lpt = (int32_t)lpt;
     const int64_t g_lines = (p->nlines + sb * lpt - 1) / (sb * lpt);
@@ -213,7 +216,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     }
     // level-1 histogram copies per group: many for one global selection (all
     // workgroups add into it), a few per tensor in per-tensor mode
-    p->nslots = one ? 16 : 4;
+    p->nslots = one ? kSlotsOne : kSlotsMany;
 
     // workspace layout (every region 256-B aligned)
     size_t o = 0;
@@ -223,9 +226,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     size_t z = 0;
     p->off_hist1 = z;   z = align_up(z + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
     p->off_hist2 = z;   z = align_up(z + (size_t)p->ngroups * kH2Bins * 4);
-    if (one) {
-      p->off_gcnt = z;    z = align_up(z + (size_t)kH2Bins * 4);
-    } else {
+    if (!one) {
       p->off_hist3 = z;   z = align_up(z + (size_t)p->ngroups * kH3Bins * 4);
       p->off_flags1 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
       p->off_flags2 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
@@ -241,7 +242,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
       p->off_rband = o;  o = align_up(o + slots * 4);
       p->off_rsuf = o;   o = align_up(o + (size_t)p->sel_grid * kH2Bins * 4);
       p->off_rcnt = o;   o = align_up(o + (size_t)p->sel_grid * 8);
-      p->off_gband = o;  o = align_up(o + (size_t)kH2Bins * kBinCap * 8);
+      p->off_rbin = o;   o = align_up(o + (size_t)kH2Bins * p->sel_grid * kPerBin * 4);
     } else {
       p->off_base = o;   o = align_up(o + (size_t)p->ngroups * 8);
       p->off_cand = o;   o = align_up(o + (size_t)p->cand_cap * 4);
@@ -316,6 +317,11 @@ extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* con
     e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_zero[0]), 0u,
                         (int64_t)((plan->off_zero[1] + plan->zero_bytes - plan->off_zero[0]) / 4),
                         stream);
+  // line summaries start at 0: the stream rewrites those of lines holding
+  // elements on every run and never writes the others
+  if (e == hipSuccess)
+    e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_summ), 0u,
+                        (int64_t)(plan->nlines * sizeof(uint16_t) / 4), stream);
   if (e == hipSuccess) e = hipStreamSynchronize(stream);
   if (e != hipSuccess) {
     plan->bound_ws = nullptr;
@@ -381,16 +387,15 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     uint32_t* rband = reinterpret_cast<uint32_t*>(base + plan->off_rband);
     uint32_t* rsuf = reinterpret_cast<uint32_t*>(base + plan->off_rsuf);
     uint32_t* rcnt = reinterpret_cast<uint32_t*>(base + plan->off_rcnt);
-    uint32_t* gcnt = reinterpret_cast<uint32_t*>(zb + plan->off_gcnt);
-    uint32_t* gband = reinterpret_cast<uint32_t*>(base + plan->off_gband);
+    uint32_t* rbin = reinterpret_cast<uint32_t*>(base + plan->off_rbin);
     if (e == hipSuccess) {
       e = launch_collect(tiles, groups, st, hist1, plan->nslots, summ, nl, lpt, sg, plan->rcap,
-                         hist2, gcnt, gband, rcand, rband, rsuf, rcnt, s);
+                         hist2, rbin, rcand, rband, rsuf, rcnt, s);
       tr.mark(li++);
     }
     if (e == hipSuccess) {
-      e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, plan->rcap, hist2, gcnt, gband,
-                        rcand, rband, rsuf, rcnt, idx_out, val_out, clear_next, clear_words, s);
+      e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, plan->rcap, hist2, rbin, rcand,
+                        rband, rsuf, rcnt, idx_out, val_out, clear_next, clear_words, s);
       tr.mark(li++);
     }
   } else {

@@ -24,6 +24,9 @@ static_assert(kLinesPerTile == kBlock, "one summary line per thread");
 constexpr int kH1Bins = 2048, kH1Shift = 20;
 constexpr int kH2Bins = 1024, kH2Shift = 10;
 constexpr int kH3Bins = 1024;
+// copies of the level-1 histogram (the stream's workgroups add into copy
+// blockIdx % copies): one global selection, per-tensor selections
+constexpr int kSlotsOne = 16, kSlotsMany = 4;
 
 struct TileDesc {        // 32 B, one per tile, written at bind
   const float* g;        // gradient, first element of the tile
@@ -73,19 +76,18 @@ hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, ui
 hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
                        const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s);
 // one selection group
-constexpr int kBinCap = 256;  // band members listed per level-2 bin (global lists)
+constexpr int kPerBin = 4;  // band keys per (level-2 bin, region) kept in the rbin table
 hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
                           const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
-                          int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* gcnt,
-                          uint32_t* gband, uint32_t* rcand, uint32_t* rband, uint32_t* rsuf,
-                          uint32_t* rcnt, hipStream_t s);
+                          int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* rbin,
+                          uint32_t* rcand, uint32_t* rband, uint32_t* rsuf, uint32_t* rcnt,
+                          hipStream_t s);
 hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
-                         int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* gcnt,
-                         const uint32_t* gband, const uint32_t* rcand, const uint32_t* rband,
-                         const uint32_t* rsuf, const uint32_t* rcnt, int32_t* idx_out,
-                         float* val_out, uint32_t* clear_next, int64_t clear_words,
-                         hipStream_t s);
+                         int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
+                         const uint32_t* rcand, const uint32_t* rband, const uint32_t* rsuf,
+                         const uint32_t* rcnt, int32_t* idx_out, float* val_out,
+                         uint32_t* clear_next, int64_t clear_words, hipStream_t s);
 // several selection groups
 hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
                          int64_t nlines, int lpt, int32_t grid, uint32_t* hist2, uint64_t* flags,

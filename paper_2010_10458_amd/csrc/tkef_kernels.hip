@@ -134,24 +134,59 @@ __device__ __forceinline__ uint32_t block_scan(uint32_t v, uint32_t* wsum, uint3
   return before + x - v;
 }
 
-// Loads the elements [e0, e0 + n) of one line (n <= kLine) of x into v[].
+// Device-memory views of pointers that were read from memory (tile
+// descriptors, LDS lists): loads and stores through them then use the global
+// instructions, whose completion counter is not shared with LDS operations.
+typedef __attribute__((address_space(1))) float gfloat;
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) v4f gv4f;
+__device__ __forceinline__ const gfloat* gptr(const float* p) { return (const gfloat*)p; }
+__device__ __forceinline__ gfloat* gptr(float* p) { return (gfloat*)p; }
+
+// Loads the elements [e0, e0 + n) of one line (0 <= n <= kLine) of x into
+// v[]; v[q] for q >= n is unspecified (callers mask by n).
 __device__ __forceinline__ void load_line(const float* __restrict__ x, int e0, int n,
                                           float (&v)[kLine]) {
   const float* p = x + e0;
   if (n == kLine && (reinterpret_cast<uintptr_t>(p) & 15u) == 0) {
-    const float4* p4 = reinterpret_cast<const float4*>(p);
+    const gv4f* p4 = (const gv4f*)p;
 #pragma unroll
     for (int q = 0; q < kLine / 4; ++q) {
-      float4 f = p4[q];
+      const v4f f = p4[q];
       v[4 * q + 0] = f.x;
       v[4 * q + 1] = f.y;
       v[4 * q + 2] = f.z;
       v[4 * q + 3] = f.w;
     }
-  } else {
+  } else if (n > 0) {
+    const gfloat* g = gptr(p);  // clamped indices: every load stays inside the line
 #pragma unroll
-    for (int q = 0; q < kLine; ++q) v[q] = (q < n) ? p[q] : 0.0f;
+    for (int q = 0; q < kLine; ++q) v[q] = g[min(q, n - 1)];
   }
+}
+
+// v[j] for a j that differs between lanes: a tree of selects on the bits of
+// j, written as bit arithmetic (a select of two array elements would be
+// turned into an indexed access, which moves v out of registers).
+__device__ __forceinline__ uint32_t sel_bits(uint32_t m, uint32_t a, uint32_t b) {
+  return a ^ ((a ^ b) & m);  // m == 0: a, m == ~0: b
+}
+__device__ __forceinline__ float pick_elem(const float (&v)[kLine], int j) {
+  static_assert(kLine == 32, "five select levels");
+  uint32_t a[16], b[8], c[4], d[2];
+  const uint32_t m0 = 0u - (uint32_t)(j & 1), m1 = 0u - (uint32_t)((j >> 1) & 1),
+                 m2 = 0u - (uint32_t)((j >> 2) & 1), m3 = 0u - (uint32_t)((j >> 3) & 1),
+                 m4 = 0u - (uint32_t)((j >> 4) & 1);
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    a[i] = sel_bits(m0, __float_as_uint(v[2 * i]), __float_as_uint(v[2 * i + 1]));
+#pragma unroll
+  for (int i = 0; i < 8; ++i) b[i] = sel_bits(m1, a[2 * i], a[2 * i + 1]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) c[i] = sel_bits(m2, b[2 * i], b[2 * i + 1]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) d[i] = sel_bits(m3, c[2 * i], c[2 * i + 1]);
+  return __uint_as_float(sel_bits(m4, d[0], d[1]));
 }
 
 }  // namespace
@@ -177,16 +212,15 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v, int64_t n) {
 constexpr int kQuarter = 2048;
 constexpr int kQuarterLines = kQuarter / kLine;
 
-typedef float v4f __attribute__((ext_vector_type(4)));
-
+// Non-temporal 16-byte load / store through a global-memory view.
 __device__ __forceinline__ float4 load_nt4(const float4* p) {
-  const v4f t = __builtin_nontemporal_load(reinterpret_cast<const v4f*>(p));
+  const v4f t = __builtin_nontemporal_load((const gv4f*)p);
   return make_float4(t.x, t.y, t.z, t.w);
 }
 
 __device__ __forceinline__ void store_nt4(float4* p, float4 v) {
   const v4f t = {v.x, v.y, v.z, v.w};
-  __builtin_nontemporal_store(t, reinterpret_cast<v4f*>(p));
+  __builtin_nontemporal_store(t, (gv4f*)p);
 }
 
 __device__ __forceinline__ uint32_t add_quad(float4 a, float4 b, float4& x, uint32_t* h) {
@@ -278,15 +312,15 @@ __global__ __launch_bounds__(kBlock) void k_stream(const TileDesc* __restrict__ 
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int e = q * kBlock + tid;
-        gv[q] = (e < len) ? g[e] : 0.0f;
-        rv[q] = (e < len) ? r[e] : 0.0f;
+        gv[q] = (e < len) ? gptr(g)[e] : 0.0f;
+        rv[q] = (e < len) ? gptr(r)[e] : 0.0f;
       }
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int e = q * kBlock + tid;
         if (e < len) {
           const float x = gv[q] + rv[q];
-          r[e] = x;
+          gptr(r)[e] = x;
           const uint32_t k = mag_key(x);
           atomicAdd(&h[k >> kH1Shift], 1u);
           atomicMax(&lmax[e / kLine], k);
@@ -308,12 +342,12 @@ __global__ __launch_bounds__(kBlock) void k_stream(const TileDesc* __restrict__ 
 // ---------------------------------------------------------------------------
 // pick: one workgroup per group. Walking the histogram from its highest bin,
 // find the bin where the running count first reaches `need`. Each thread owns
-// PER consecutive bins, summed over the histogram's `nslots` copies with
-// 16-byte loads that are all in flight together.
-template <int PER>
+// PER consecutive bins, summed over the histogram's NSLOT copies with 16-byte
+// loads that are all in flight together.
+template <int PER, int NSLOT>
 __global__ __launch_bounds__(kBlock) void k_pick(int level, const GroupDesc* __restrict__ groups,
                                                  GroupState* __restrict__ st,
-                                                 const uint32_t* __restrict__ hist, int nslots) {
+                                                 const uint32_t* __restrict__ hist) {
   constexpr int nbins = PER * kBlock;
   __shared__ uint32_t part[kBlock];
   __shared__ uint32_t res[3];
@@ -338,20 +372,24 @@ __global__ __launch_bounds__(kBlock) void k_pick(int level, const GroupDesc* __r
   }
   // this thread's bins: lo .. lo + PER - 1, threads ordered from the top
   const int lo = nbins - PER * (tid + 1);
-  const uint32_t* __restrict__ hg = hist + (size_t)g * nslots * nbins + lo;
+  const uint32_t* __restrict__ hg = hist + (size_t)g * NSLOT * nbins + lo;
+  uint4 v[NSLOT][PER / 4];
+#pragma unroll
+  for (int sl = 0; sl < NSLOT; ++sl)
+#pragma unroll
+    for (int q = 0; q < PER / 4; ++q)
+      v[sl][q] = reinterpret_cast<const uint4*>(hg + (size_t)sl * nbins)[q];
   uint32_t c[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) c[j] = 0u;
-#pragma unroll 16
-  for (int sl = 0; sl < nslots; ++sl) {
-    const uint4* p4 = reinterpret_cast<const uint4*>(hg + (size_t)sl * nbins);
+#pragma unroll
+  for (int sl = 0; sl < NSLOT; ++sl) {
 #pragma unroll
     for (int q = 0; q < PER / 4; ++q) {
-      const uint4 v = p4[q];
-      c[4 * q + 0] += v.x;
-      c[4 * q + 1] += v.y;
-      c[4 * q + 2] += v.z;
-      c[4 * q + 3] += v.w;
+      c[4 * q + 0] += v[sl][q].x;
+      c[4 * q + 1] += v[sl][q].y;
+      c[4 * q + 2] += v[sl][q].z;
+      c[4 * q + 3] += v[sl][q].w;
     }
   }
   uint32_t sum = 0u;
@@ -408,6 +446,7 @@ constexpr int kSBlock = 1024;
 constexpr int kSWaves = kSBlock / 64;
 constexpr int kSMaxGroups = 4096;
 constexpr int kSMaxLpt = 16;     // lines per thread at most
+static_assert(kLinesPerTile % kSMaxLpt == 0, "a thread's lines lie in one tile");
 constexpr int kCandShift = 13;   // log2(kTile)
 static_assert((1 << kCandShift) == kTile, "candidate encoding");
 constexpr uint64_t kFlagValid = 1ull << 63, kFlagVal = (1ull << 63) - 1;
@@ -495,19 +534,23 @@ __device__ __forceinline__ void sblock_pick(const uint32_t* __restrict__ hist, u
 }
 
 // Within one workgroup: level-1 pick over a 2048-bin histogram held in
-// `nslots` copies (two bins per thread). Returns via res[] as sblock_pick
-// does. Ends with a barrier.
-__device__ __forceinline__ void sblock_pick1(const uint32_t* __restrict__ hist1, int nslots,
-                                             uint32_t need, uint32_t* wsum, uint32_t* res) {
+// NSLOT copies (two bins per thread; every copy's load is issued before the
+// first is used). Returns via res[] as sblock_pick does. Ends with a barrier.
+template <int NSLOT>
+__device__ __forceinline__ void sblock_pick1(const uint32_t* __restrict__ hist1, uint32_t need,
+                                             uint32_t* wsum, uint32_t* res) {
   static_assert(kH1Bins == 2 * kSBlock, "two bins per thread");
   const int tid = threadIdx.x;
   const int lo = kH1Bins - 2 * (tid + 1);  // this thread's bins: lo, lo + 1 (from the top)
+  uint2 v[NSLOT];
+#pragma unroll
+  for (int sl = 0; sl < NSLOT; ++sl)
+    v[sl] = *reinterpret_cast<const uint2*>(hist1 + (size_t)sl * kH1Bins + lo);
   uint32_t c0 = 0u, c1 = 0u;
-#pragma unroll 16
-  for (int sl = 0; sl < nslots; ++sl) {
-    const uint2 v = *reinterpret_cast<const uint2*>(hist1 + (size_t)sl * kH1Bins + lo);
-    c0 += v.x;
-    c1 += v.y;
+#pragma unroll
+  for (int sl = 0; sl < NSLOT; ++sl) {
+    c0 += v[sl].x;
+    c1 += v[sl].y;
   }
   uint32_t total;
   const uint32_t ex = sblock_scan(c0 + c1, wsum, &total);
@@ -529,47 +572,44 @@ __device__ __forceinline__ void sblock_pick1(const uint32_t* __restrict__ hist1,
   __syncthreads();
 }
 
-// The thread's `lpt` consecutive summary lines starting at line0, seen
-// through the (at most two) tiles they lie in. Summaries and descriptors are
-// fetched together up front; flagged() gives the lines whose summary reaches
-// thr(group).
+// The thread's `lpt` consecutive summary lines starting at line l0. lpt is a
+// power of two up to kSMaxLpt and divides kLinesPerTile, so all of them lie
+// in one tile. flagged() gives the lines whose summary reaches thr(group).
+// Lines past a tile's elements keep the summary 0 that bind writes (the
+// stream never writes them), so they are flagged only for thr < 2^16, and
+// hold no elements then. Summaries and the descriptor are fetched together
+// up front.
 struct LineSpan {
-  int64_t line0, last;
-  int tile0, tile1;
-  TileDesc tA, tB;
+  int tile, e0, lim;  // tile, position of the first line's first element, lines held
+  TileDesc t;
   uint16_t sv[kSMaxLpt];
 
   __device__ __forceinline__ void load(const TileDesc* __restrict__ tiles,
                                        const uint16_t* __restrict__ summ, int64_t nlines,
                                        int64_t l0, int lpt) {
-    line0 = l0;
-    const bool has = l0 < nlines;
-    last = has ? min(l0 + lpt, nlines) - 1 : l0 - 1;
-    tile0 = has ? (int)(l0 / kLinesPerTile) : 0;
-    tile1 = has ? (int)(last / kLinesPerTile) : 0;
+    const bool has = l0 < nlines;  // nlines is a multiple of kLinesPerTile
+    tile = has ? (int)(l0 / kLinesPerTile) : 0;
+    e0 = (int)(l0 % kLinesPerTile) * kLine;
+    // four summaries per 8-byte load (l0 and lpt are multiples of 4)
 #pragma unroll
-    for (int q = 0; q < kSMaxLpt; ++q) sv[q] = (l0 + q <= last) ? summ[l0 + q] : (uint16_t)0;
-    tA = tiles[tile0];
-    tB = tiles[tile1];
+    for (int c = 0; c < kSMaxLpt / 4; ++c) {
+      uint2 v = make_uint2(0u, 0u);
+      if (has && 4 * c < lpt) v = *reinterpret_cast<const uint2*>(summ + l0 + 4 * c);
+      sv[4 * c + 0] = (uint16_t)(v.x & 0xFFFFu);
+      sv[4 * c + 1] = (uint16_t)(v.x >> 16);
+      sv[4 * c + 2] = (uint16_t)(v.y & 0xFFFFu);
+      sv[4 * c + 3] = (uint16_t)(v.y >> 16);
+    }
+    t = tiles[tile];
+    lim = has ? lpt : 0;
   }
-  __device__ __forceinline__ bool in_a(int q) const {
-    return (int)((line0 + q) / kLinesPerTile) == tile0;
-  }
-  __device__ __forceinline__ const TileDesc& desc(int q) const { return in_a(q) ? tA : tB; }
-  __device__ __forceinline__ int tile(int q) const { return in_a(q) ? tile0 : tile1; }
-  __device__ __forceinline__ int e0(int q) const {
-    return (int)((line0 + q) % kLinesPerTile) * kLine;
-  }
+  __device__ __forceinline__ int e0_of(int q) const { return e0 + q * kLine; }
   template <typename Thr>
   __device__ __forceinline__ uint32_t flagged(Thr thr) const {
-    const uint32_t ta = thr(tA.group) >> 16, tb = thr(tB.group) >> 16;
+    const uint32_t th = thr(t.group) >> 16;
     uint32_t m = 0u;
 #pragma unroll
-    for (int q = 0; q < kSMaxLpt; ++q) {
-      const bool a = in_a(q);
-      if (line0 + q <= last && e0(q) < (a ? tA.len : tB.len) && (uint32_t)sv[q] >= (a ? ta : tb))
-        m |= 1u << q;
-    }
+    for (int q = 0; q < kSMaxLpt; ++q) m |= (q < lim && (uint32_t)sv[q] >= th) ? (1u << q) : 0u;
     return m;
   }
 };
@@ -584,20 +624,20 @@ __device__ __forceinline__ void walk_mask(const LineSpan& ls, uint32_t mask, Hit
   while (mask) {
     const int q = __ffs(mask) - 1;
     mask &= mask - 1u;
-    const TileDesc& t = ls.desc(q);
-    const int e0 = ls.e0(q), n = min(kLine, t.len - e0);
+    const TileDesc& t = ls.t;
+    const int e0 = ls.e0_of(q), n = max(0, min(kLine, t.len - e0));
     float v[kLine];
     load_line(t.r, e0, n, v);
     uint32_t hm = 0u;
 #pragma unroll
     for (int j = 0; j < kLine; ++j)
       hm |= (j < n && hit(t.group, mag_key(v[j]))) ? (1u << j) : 0u;
-    const int tile = ls.tile(q);
+    const int tile = ls.tile;
 #pragma unroll 1
     while (hm) {
       const int j = __ffs(hm) - 1;
       hm &= hm - 1u;
-      const float x = t.r[e0 + j];
+      const float x = gptr(t.r)[e0 + j];
       f(tile, t, e0 + j, x, mag_key(x));
     }
   }
@@ -616,7 +656,7 @@ __device__ __forceinline__ void walk_cands(const TileDesc* __restrict__ tiles, i
     if (tile >= ntiles) continue;  // never produced; keeps accesses in bounds
     const TileDesc t = tiles[tile];
     if (e >= t.len) continue;
-    const float x = t.r[e];
+    const float x = gptr(t.r)[e];
     f(tile, t, e, x, mag_key(x));
   }
 }
@@ -639,20 +679,20 @@ __device__ __forceinline__ void walk_cands(const TileDesc* __restrict__ tiles, i
 //               level-2 bin (key bits 19..10) from the top;
 //   rsuf[w][b]  band members of the region in level-2 bins above b (written
 //               when the region has band members);
-//   gband[b]    the band members in level-2 bin b of all regions, as
-//               {key, region}, at most kBinCap per bin, in no particular
-//               order; gcnt[b] counts them (including those beyond kBinCap);
+//   rbin[b][w]  the first kPerBin keys of rband[w] in level-2 bin b (slots
+//               beyond the bin's count are left as they were);
 //   rcnt[w]     {candidates | (rcand incomplete) << 31,
 //                band members | (band not stored) << 31}, counts exact;
 //   hist2       += the region's level-2 histogram.
 // A region with more than rcap candidates leaves rcand incomplete; one with
-// more than kBandCap band members stores no band keys (rband, gband). finish
+// more than kBandCap band members stores no band keys (rband, rbin). finish
 // then reads that region's lines instead.
 //
 // finish makes the level-2 pick (bin B2) from hist2, builds the level-3
-// histogram in LDS from the band members in bin B2 of all regions (rsuf tells
-// where they lie in rband) and picks the exact threshold key T and the number
-// of elements equal to T to keep. The elements above T in the regions before
+// histogram in LDS from the band members in bin B2 of all regions (from rbin
+// and the counts in rsuf; from rband when a region has more than kPerBin) and
+// picks the exact threshold key T and the number of elements equal to T to
+// keep. The elements above T in the regions before
 // its own are the non-band candidates, the band members above bin B2 and the
 // bin-B2 members above T; the elements equal to T are bin-B2 members. From
 // these counts workgroup w places its region's selection.
@@ -660,15 +700,19 @@ constexpr int kOvWords = kSMaxGroups / 32;
 constexpr int kFlCap = 4096;     // flagged lines listed in LDS at a time
 constexpr int kBandCap = 4096;   // band members of a region kept in LDS
 constexpr int kC2Cap = 4096;     // level-2 class members kept in LDS by finish
+static_assert(kPerBin == 4, "rbin entries are read as one uint4");
 static_assert(kSMaxGroups <= 65536, "region numbers fit 16 bits");
 
+// (The sizes come last among the arguments: they are used at the start, so
+// both cache lines of the argument block are fetched then, and later reloads
+// of the pointers hit.)
 __global__ __launch_bounds__(kSBlock) void k_collect(
     const TileDesc* __restrict__ tiles, const GroupDesc* __restrict__ groups,
-    GroupState* __restrict__ st, const uint32_t* __restrict__ hist1, int nslots,
-    const uint16_t* __restrict__ summ, int64_t nlines, int lpt, uint32_t rcap,
-    uint32_t* __restrict__ hist2, uint32_t* __restrict__ gcnt, uint2* __restrict__ gband,
-    uint4* __restrict__ rcand, uint32_t* __restrict__ rband, uint32_t* __restrict__ rsuf,
-    uint2* __restrict__ rcnt) {
+    GroupState* __restrict__ st, const uint32_t* __restrict__ hist1,
+    const uint16_t* __restrict__ summ, uint32_t* __restrict__ hist2,
+    uint32_t* __restrict__ rbin, uint4* __restrict__ rcand, uint32_t* __restrict__ rband,
+    uint32_t* __restrict__ rsuf, uint2* __restrict__ rcnt, uint32_t rcap, int lpt,
+    int64_t nlines) {
   static_assert(kH2Bins == kSBlock, "one level-2 bin per thread");
   __shared__ uint32_t h[kH2Bins];
   __shared__ uint32_t hoff[kH2Bins];
@@ -687,8 +731,9 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
   // level-1 pick, whose barriers also publish the cleared LDS
   LineSpan ls;
   ls.load(tiles, summ, nlines, ((int64_t)w * kSBlock + tid) * lpt, lpt);
+  __builtin_amdgcn_sched_barrier(0);  // keep those loads ahead of the histogram's
   const uint32_t k = groups[0].k;
-  sblock_pick1(hist1, nslots, k, wsum, res);
+  sblock_pick1<kSlotsOne>(hist1, k, wsum, res);
   const uint32_t B1 = res[0];
   const uint32_t lo = B1 << kH1Shift;
   if (w == 0 && tid == 0) {
@@ -715,11 +760,11 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
       const int q = __ffs(m) - 1;
       m &= m - 1u;
       if (rank >= c0 && rank < c0 + (uint32_t)kFlCap) {
-        const TileDesc& t = ls.desc(q);
-        const int e0 = ls.e0(q);
+        const TileDesc& t = ls.t;
+        const int e0 = ls.e0_of(q);
         lptr[rank - c0] = t.r + e0;
         lgidx[rank - c0] = (uint32_t)(t.gstart + e0);
-        lnum[rank - c0] = (uint8_t)min(kLine, t.len - e0);
+        lnum[rank - c0] = (uint8_t)max(0, min(kLine, t.len - e0));
       }
       ++rank;
     }
@@ -729,7 +774,7 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
     for (uint32_t b0 = 0; b0 < nl; b0 += kSBlock) {
       const uint32_t i = b0 + tid;
       float v[kLine];
-      uint32_t hm = 0u, gidx0 = 0u;
+      uint32_t hm = 0u, bm = 0u, gidx0 = 0u;  // candidates, band members of the line
       float* rp = nullptr;
       if (i < nl) {
         gidx0 = lgidx[i];
@@ -739,14 +784,15 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
 #pragma unroll
         for (int j = 0; j < kLine; ++j) {
           const uint32_t key = mag_key(v[j]);
-          if (j < n && key >= lo) {
-            hm |= 1u << j;
-            if ((key >> kH1Shift) == B1) {
-              atomicAdd(&h[(key >> kH2Shift) & (kH2Bins - 1)], 1u);
-              const uint32_t slot = atomicAdd(&nband, 1u);
-              if (slot < (uint32_t)kBandCap) bandk[slot] = key;
-            }
-          }
+          hm |= (j < n && key >= lo) ? (1u << j) : 0u;
+          bm |= (j < n && (key >> kH1Shift) == B1) ? (1u << j) : 0u;
+        }
+#pragma unroll 1
+        for (uint32_t m2 = bm; m2; m2 &= m2 - 1u) {
+          const uint32_t key = mag_key(pick_elem(v, __ffs(m2) - 1));
+          atomicAdd(&h[(key >> kH2Shift) & (kH2Bins - 1)], 1u);
+          const uint32_t slot = atomicAdd(&nband, 1u);
+          if (slot < (uint32_t)kBandCap) bandk[slot] = key;
         }
       }
       uint32_t tot;
@@ -754,15 +800,12 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
       if (cw + tot > rcap) fits = false;
       if (fits && hm) {
         uint4* __restrict__ dst = cdst + cw + ex;
-        uint32_t o = 0u;
-#pragma unroll
-        for (int j = 0; j < kLine; ++j) {
-          if ((hm >> j) & 1u) {
-            const uint64_t a = reinterpret_cast<uint64_t>(rp + j);
-            dst[o] = make_uint4(gidx0 + (uint32_t)j, __float_as_uint(v[j]), (uint32_t)a,
-                                (uint32_t)(a >> 32));
-            ++o;
-          }
+#pragma unroll 1
+        for (uint32_t m2 = hm; m2; m2 &= m2 - 1u, ++dst) {
+          const int j = __ffs(m2) - 1;
+          const uint64_t a = reinterpret_cast<uint64_t>(rp + j);
+          *dst = make_uint4(gidx0 + (uint32_t)j, __float_as_uint(pick_elem(v, j)), (uint32_t)a,
+                            (uint32_t)(a >> 32));
         }
       }
       cw += tot;
@@ -771,18 +814,16 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
   }
 
   // band members by level-2 bin from the top (thread tid owns bin 1023 - tid):
-  // sorted into rband[w] and appended to their bin's global list, whose slots
-  // for this region start at the value the bin's counter had
+  // sorted into rband[w], and the first kPerBin of each bin also into rbin
   const int bin = kH2Bins - 1 - tid;
   const uint32_t cb = h[bin];
   uint32_t bw;
   const uint32_t above = sblock_scan(cb, wsum, &bw);
   const bool band_ok = bw <= (uint32_t)kBandCap;  // every band key is in bandk
   if (cb) atomicAdd(&hist2[bin], cb);
-  const uint32_t gbase = (cb && band_ok) ? atomicAdd(&gcnt[bin], cb) : 0u;
   if (bw) rsuf[(size_t)w * kH2Bins + bin] = above;
-  h[bin] = above;          // from here on: the bin's next slot in rband[w]
-  hoff[bin] = gbase - above;  // + that slot = the member's slot in gband[bin]
+  h[bin] = above;     // from here on: the bin's next slot in rband[w]
+  hoff[bin] = above;  // the bin's first slot
   __syncthreads();
   if (band_ok) {
     uint32_t* __restrict__ dst = rband + (size_t)w * rcap;
@@ -791,8 +832,8 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
       const uint32_t b2 = (key >> kH2Shift) & (kH2Bins - 1);
       const uint32_t slot = atomicAdd(&h[b2], 1u);
       dst[slot] = key;
-      const uint32_t gs = hoff[b2] + slot;
-      if (gs < (uint32_t)kBinCap) gband[(size_t)b2 * kBinCap + gs] = make_uint2(key, (uint32_t)w);
+      const uint32_t rank = slot - hoff[b2];
+      if (rank < (uint32_t)kPerBin) rbin[((size_t)b2 * gridDim.x + w) * kPerBin + rank] = key;
     }
   }
   if (tid == 0)
@@ -848,8 +889,8 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
     const TileDesc* __restrict__ tiles, const GroupDesc* __restrict__ groups,
     const GroupState* __restrict__ st, const uint16_t* __restrict__ summ, int64_t nlines,
     int lpt, uint32_t rcap, const uint32_t* __restrict__ hist2,
-    const uint32_t* __restrict__ gcnt, const uint2* __restrict__ gband,
-    const uint4* __restrict__ rcand, const uint32_t* __restrict__ rband,
+    const uint32_t* __restrict__ rbin, const uint4* __restrict__ rcand,
+    const uint32_t* __restrict__ rband,
     const uint32_t* __restrict__ rsuf, const uint2* __restrict__ rcnt,
     int32_t* __restrict__ idx_out, float* __restrict__ val_out,
     uint32_t* __restrict__ clear_next, int64_t clear_words) {
@@ -888,7 +929,8 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
 #pragma unroll
   for (int q = 0; q < kRegPerThread; ++q) {
     const int r = q * kSBlock + tid;
-    cr[q] = (r < G) ? rcnt[r] : make_uint2(0u, 0u);
+    cr[q] = make_uint2(0u, 0u);
+    if (q * kSBlock < G && r < G) cr[q] = rcnt[r];
   }
 
   // level 2 (the pick's barriers also publish the cleared LDS above)
@@ -897,29 +939,53 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   const uint32_t need2 = (res[1] < s0.need) ? s0.need - res[1] : 0u;
   const uint32_t cls21 = (s0.prefix << 10) | B2;
 
-  // The level-2 class (band members in bin B2): the bin's global list, and
-  // per earlier region the band members above bin B2 (from rsuf). gtb: this
-  // thread's share of the elements above T before region w.
-  const uint32_t gc = gcnt[B2];
-  const uint2 ge = (tid < kBinCap) ? gband[(size_t)B2 * kBinCap + tid] : make_uint2(0u, 0u);
+  // The level-2 class (band members in bin B2) of every region, fetched with
+  // the counts that place it: per region, bw band members, `above` of them
+  // in bins above B2 and `at` in bin B2, whose first kPerBin keys are in
+  // rbin. gtb: this thread's share of the elements above T before region w.
   uint32_t gtb = 0u;
+  bool slow = false;  // some region has more than kPerBin class-2 members
 #pragma unroll
   for (int q = 0; q < kRegPerThread; ++q) {
+    if (q * kSBlock >= G) break;
     const int r = q * kSBlock + tid;
+    if (r >= G) continue;
     const uint32_t bw = cr[q].y & 0x7FFFFFFFu;
-    if (r < G && (cr[q].y >> 31)) atomicOr(&ovbits[r >> 5], 1u << (r & 31));
-    if (r < w) gtb += (cr[q].x & 0x7FFFFFFFu) - bw + (bw ? rsuf[(size_t)r * kH2Bins + B2] : 0u);
-  }
-  if (gc <= (uint32_t)kBinCap) {
-    if ((uint32_t)tid < gc) {
-      atomicAdd(&h[ge.x & (kH3Bins - 1)], 1u);
-      c2key[tid] = ge.x;
-      c2reg[tid] = (uint16_t)ge.y;
+    const bool ov = (cr[q].y >> 31) != 0u;
+    if (ov) atomicOr(&ovbits[r >> 5], 1u << (r & 31));
+    if (!bw) {
+      if (r < w) gtb += cr[q].x & 0x7FFFFFFFu;
+      continue;
     }
-    if (tid == 0) n2 = gc;
-    __syncthreads();
-  } else {
-    // more than kBinCap members: every stored region's through rsuf / rband
+    const uint32_t* sr = rsuf + (size_t)r * kH2Bins;
+    const uint32_t above = sr[B2];
+    const uint32_t at = (B2 ? sr[B2 - 1] : bw) - above;
+    const uint4 e = *reinterpret_cast<const uint4*>(rbin + ((size_t)B2 * G + r) * kPerBin);
+    if (r < w) gtb += (cr[q].x & 0x7FFFFFFFu) - bw + above;
+    if (ov) continue;
+    if (at > (uint32_t)kPerBin) {
+      slow = true;
+      continue;
+    }
+    const uint32_t ek[4] = {e.x, e.y, e.z, e.w};
+#pragma unroll
+    for (int c = 0; c < kPerBin; ++c) {
+      if ((uint32_t)c < at) {
+        atomicAdd(&h[ek[c] & (kH3Bins - 1)], 1u);
+        const uint32_t slot = atomicAdd(&n2, 1u);
+        if (slot < (uint32_t)kC2Cap) {
+          c2key[slot] = ek[c];
+          c2reg[slot] = (uint16_t)r;
+        }
+      }
+    }
+  }
+  if (slow) atomicOr(&n2, 0x80000000u);  // members beyond rbin: take all from rband
+  __syncthreads();
+  if (n2 & 0x80000000u) {
+    __syncthreads();  // every thread has read n2
+    if (tid == 0) n2 = 0u;
+    for (int i = tid; i < kH3Bins; i += kSBlock) h[i] = 0u;
 #pragma unroll 1
     for (int r0 = 0; r0 < G; r0 += kSBlock) {
       const int r = r0 + tid;
@@ -934,7 +1000,7 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
         }
       }
       uint32_t tot;
-      const uint32_t ex = sblock_scan(at, wsum, &tot);
+      const uint32_t ex = sblock_scan(at, wsum, &tot);  // (its barriers order the reset above)
       off[tid] = ex;
       abv[tid] = above;
       __syncthreads();
@@ -1038,7 +1104,7 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
     if (pos < k) {
       idx_out[pos] = (int32_t)gidx;
       val_out[pos] = x;
-      *rp = 0.0f;
+      *gptr(rp) = 0.0f;
     }
   };
   if (own_ov) {
@@ -1080,8 +1146,8 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
   ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
   // B1 = 0xFFFFFFFF for a group with nothing to select: shifted, it lies
   // above every key, so such a group yields no candidates
-  const uint32_t b1A = st[ls.tA.group].prefix, b1B = st[ls.tB.group].prefix;
-  auto b1_of = [&](int g) -> uint32_t { return g == ls.tA.group ? b1A : b1B; };
+  const uint32_t b1t = st[ls.t.group].prefix;
+  auto b1_of = [&](int) -> uint32_t { return b1t; };
   const uint32_t mask = ls.flagged([&](int g) -> uint32_t { return b1_of(g) << kH1Shift; });
   auto is_cand = [&](int g, uint32_t k) -> bool { return k >= (b1_of(g) << kH1Shift); };
   uint32_t c = 0u;
@@ -1269,7 +1335,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
     if (pos < gd.k) {
       idx_out[gd.out_base + pos] = t.gstart + e;
       val_out[gd.out_base + pos] = x;
-      t.r[e] = 0.0f;
+      gptr(t.r)[e] = 0.0f;
     }
   };
   if (nst <= (uint32_t)kStage) {
@@ -1478,7 +1544,7 @@ __global__ __launch_bounds__(kUBlock) void k_update(
           const int mid = (lo + hi + 1) >> 1;
           if (tens[mid].goff <= gi) lo = mid; else hi = mid - 1;
         }
-        float* wp = tens[lo].w + (gi - tens[lo].goff);
+        gfloat* wp = gptr(tens[lo].w + (gi - tens[lo].goff));
         const float stepv = lr * acc[li];
         *wp = *wp - stepv;
       }
@@ -1493,25 +1559,24 @@ __global__ __launch_bounds__(kUBlock) void k_update(
     if (z <= a) continue;
     const int cnt = (int)(z - a);
     const int la = (int)(a - base);
-    float* __restrict__ w = tt.w + (a - tt.goff);
-    float* __restrict__ bm = mom ? tt.b + (a - tt.goff) : nullptr;
+    gfloat* __restrict__ w = gptr(tt.w + (a - tt.goff));
+    gfloat* __restrict__ bm = mom ? gptr(tt.b + (a - tt.goff)) : nullptr;
     const bool vec = ((reinterpret_cast<uintptr_t>(w) |
                        (bm ? reinterpret_cast<uintptr_t>(bm) : 0u)) & 15u) == 0;
     int done = 0;
     if (vec) {
       const int nv = cnt >> 2;
-      float4* w4 = reinterpret_cast<float4*>(w);
-      float4* b4 = reinterpret_cast<float4*>(bm);
+      gv4f* w4 = (gv4f*)w;
+      gv4f* b4 = (gv4f*)bm;
       for (int q = tid; q < nv; q += kUBlock) {
-        float4 wq = w4[q];
-        float4 bq = bm ? b4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+        const v4f wv4 = w4[q];
+        const v4f bv4 = bm ? b4[q] : v4f{0.f, 0.f, 0.f, 0.f};
+        float wq[4] = {wv4.x, wv4.y, wv4.z, wv4.w}, bq[4] = {bv4.x, bv4.y, bv4.z, bv4.w};
         const int l = la + 4 * q;
-        wq.x = sgd_step(acc[l + 0], wq.x, bq.x, mom, lr, mu, wd);
-        wq.y = sgd_step(acc[l + 1], wq.y, bq.y, mom, lr, mu, wd);
-        wq.z = sgd_step(acc[l + 2], wq.z, bq.z, mom, lr, mu, wd);
-        wq.w = sgd_step(acc[l + 3], wq.w, bq.w, mom, lr, mu, wd);
-        w4[q] = wq;
-        if (mom) b4[q] = bq;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) wq[c] = sgd_step(acc[l + c], wq[c], bq[c], mom, lr, mu, wd);
+        w4[q] = v4f{wq[0], wq[1], wq[2], wq[3]};
+        if (mom) b4[q] = v4f{bq[0], bq[1], bq[2], bq[3]};
       }
       done = nv << 2;
     }
@@ -1545,36 +1610,39 @@ hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
                        const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s) {
   static_assert(kH1Bins == 8 * kBlock && kH2Bins == 4 * kBlock && kH3Bins == 4 * kBlock,
                 "pick: bins per thread");
-  if (level == 1)
-    hipLaunchKernelGGL(k_pick<8>, dim3(ngroups), dim3(kBlock), 0, s, level, groups, st, hist,
-                       nslots);
-  else
-    hipLaunchKernelGGL(k_pick<4>, dim3(ngroups), dim3(kBlock), 0, s, level, groups, st, hist,
-                       nslots);
+  if (level == 1) {
+    if (nslots != kSlotsMany) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_pick<8, kSlotsMany>), dim3(ngroups), dim3(kBlock), 0, s, level, groups,
+                       st, hist);
+  } else {
+    if (nslots != 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_pick<4, 1>), dim3(ngroups), dim3(kBlock), 0, s, level, groups, st,
+                       hist);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
                           const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
-                          int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* gcnt,
-                          uint32_t* gband, uint32_t* rcand, uint32_t* rband, uint32_t* rsuf,
-                          uint32_t* rcnt, hipStream_t s) {
-  hipLaunchKernelGGL(k_collect, dim3(grid), dim3(kSBlock), 0, s, tiles, groups, st, hist1, nslots,
-                     summ, nlines, lpt, rcap, hist2, gcnt, reinterpret_cast<uint2*>(gband),
-                     reinterpret_cast<uint4*>(rcand), rband, rsuf, reinterpret_cast<uint2*>(rcnt));
+                          int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* rbin,
+                          uint32_t* rcand, uint32_t* rband, uint32_t* rsuf, uint32_t* rcnt,
+                          hipStream_t s) {
+  if (nslots != kSlotsOne) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_collect, dim3(grid), dim3(kSBlock), 0, s, tiles, groups, st, hist1,
+                     summ, hist2, rbin, reinterpret_cast<uint4*>(rcand), rband, rsuf,
+                     reinterpret_cast<uint2*>(rcnt), rcap, lpt, nlines);
   return hipGetLastError();
 }
 
 hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
-                         int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* gcnt,
-                         const uint32_t* gband, const uint32_t* rcand, const uint32_t* rband,
-                         const uint32_t* rsuf, const uint32_t* rcnt, int32_t* idx_out,
-                         float* val_out, uint32_t* clear_next, int64_t clear_words,
-                         hipStream_t s) {
+                         int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
+                         const uint32_t* rcand, const uint32_t* rband, const uint32_t* rsuf,
+                         const uint32_t* rcnt, int32_t* idx_out, float* val_out,
+                         uint32_t* clear_next, int64_t clear_words, hipStream_t s) {
   hipLaunchKernelGGL(k_finish, dim3(grid), dim3(kSBlock), 0, s, tiles, groups, st, summ,
-                     nlines, lpt, rcap, hist2, gcnt, reinterpret_cast<const uint2*>(gband),
-                     reinterpret_cast<const uint4*>(rcand), rband, rsuf,
+                     nlines, lpt, rcap, hist2, rbin, reinterpret_cast<const uint4*>(rcand),
+                     rband, rsuf,
                      reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, clear_next,
                      clear_words);
   return hipGetLastError();
