@@ -119,9 +119,11 @@ int tkef_sparsify_execute(tkef_sparsify_plan plan, void *ws, size_t ws_bytes,
                           hipStream_t stream);
 
 /* Optional timing hook: with n_events >= nlaunch + 1, each execution records
- * events[0] before its first kernel and events[i + 1] after kernel i (HIP
- * events created by the caller). Pass NULL to switch it off. Names of the
- * kernels in launch order are available from tkef_sparsify_plan_launch_name. */
+ * events[0] at the start of its first kernel and events[i + 1] at the end of
+ * kernel i (HIP events created by the caller; the kernel dispatches record
+ * them, so no extra commands run between the kernels). Pass NULL to switch it
+ * off. Names of the kernels in launch order are available from
+ * tkef_sparsify_plan_launch_name. */
 int tkef_sparsify_plan_set_events(tkef_sparsify_plan plan, hipEvent_t *events,
                                   int32_t n_events);
 const char *tkef_sparsify_plan_launch_name(tkef_sparsify_plan plan, int32_t i);
@@ -182,6 +184,7 @@ int tkef_update_execute(tkef_update_plan plan, const int32_t *idx, const float *
                         const int32_t *nnz, float lr, float mu, float wd, void *ws,
                         size_t ws_bytes, uint32_t *status, hipStream_t stream);
 
+/* Optional timing hook, as tkef_sparsify_plan_set_events. */
 int tkef_update_plan_set_events(tkef_update_plan plan, hipEvent_t *events,
                                 int32_t n_events);
 const char *tkef_update_plan_launch_name(tkef_update_plan plan, int32_t i);

@@ -48,14 +48,18 @@ int check_numels(const int64_t* numels, int32_t ntensors, int64_t* total) {
   return TKEF_OK;
 }
 
-// Records the optional timing event that follows launch `i` (or precedes
-// launch 0 when i == -1).
+// Optional timing events of an execution: ev[0] is recorded at the start of
+// launch 0 and ev[i + 1] at the end of launch i, by the dispatches themselves
+// (no separate event commands between the kernels).
 struct Tracer {
   hipEvent_t* ev;
   int32_t n;
-  hipStream_t s;
-  void mark(int i) const {
-    if (ev && i + 1 < n) (void)hipEventRecord(ev[i + 1], s);
+  Ev at(int i) const {
+    Ev e;
+    if (!ev) return e;
+    if (i == 0 && n > 0) e.start = ev[0];
+    if (i + 1 < n) e.stop = ev[i + 1];
+    return e;
   }
 };
 
@@ -366,7 +370,7 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   const int32_t nt = plan->ntiles, ng = plan->ngroups;
   const int64_t nl = plan->nlines;
   const int lpt = plan->sel_lpt, sg = plan->sel_grid;
-  const Tracer tr{plan->events, plan->n_events, s};
+  const Tracer tr{plan->events, plan->n_events};
   int li = 0;  // launch index, for the timing hook
   uint32_t* clear_next = reinterpret_cast<uint32_t*>(zn);
   const int64_t clear_words = (int64_t)(plan->zero_bytes / 4);
@@ -379,25 +383,21 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     if (e != hipSuccess) return TKEF_EHIP;
     plan->needs_clear = false;
   }
-  if (tr.ev && tr.n > 0) (void)hipEventRecord(tr.ev[0], s);
-  e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s);
-  tr.mark(li++);
+  e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s,
+                    tr.at(li++));
   if (ng == 1) {
     uint32_t* rcand = reinterpret_cast<uint32_t*>(base + plan->off_rcand);
     uint32_t* rband = reinterpret_cast<uint32_t*>(base + plan->off_rband);
     uint32_t* rsuf = reinterpret_cast<uint32_t*>(base + plan->off_rsuf);
     uint32_t* rcnt = reinterpret_cast<uint32_t*>(base + plan->off_rcnt);
     uint32_t* rbin = reinterpret_cast<uint32_t*>(base + plan->off_rbin);
-    if (e == hipSuccess) {
+    if (e == hipSuccess)
       e = launch_collect(tiles, groups, st, hist1, plan->nslots, summ, nl, lpt, sg, plan->rcap,
-                         hist2, rbin, rcand, rband, rsuf, rcnt, s);
-      tr.mark(li++);
-    }
-    if (e == hipSuccess) {
+                         hist2, rbin, rcand, rband, rsuf, rcnt, s, tr.at(li++));
+    if (e == hipSuccess)
       e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, plan->rcap, hist2, rbin, rcand,
-                        rband, rsuf, rcnt, idx_out, val_out, clear_next, clear_words, s);
-      tr.mark(li++);
-    }
+                        rband, rsuf, rcnt, idx_out, val_out, clear_next, clear_words, s,
+                        tr.at(li++));
   } else {
     uint32_t* hist3 = reinterpret_cast<uint32_t*>(zb + plan->off_hist3);
     uint64_t* flags1 = reinterpret_cast<uint64_t*>(zb + plan->off_flags1);
@@ -405,36 +405,19 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     uint32_t* meta = reinterpret_cast<uint32_t*>(zb + plan->off_meta);
     uint32_t* gbase = reinterpret_cast<uint32_t*>(base + plan->off_base);
     int32_t* cand = reinterpret_cast<int32_t*>(base + plan->off_cand);
-    if (e == hipSuccess) {
-      e = launch_pick(1, groups, st, hist1, plan->nslots, ng, s);
-      tr.mark(li++);
-    }
-    if (e == hipSuccess) {
+    if (e == hipSuccess)
+      e = launch_pick(1, groups, st, hist1, plan->nslots, ng, s, tr.at(li++));
+    if (e == hipSuccess)
       e = launch_gather(tiles, st, summ, nl, lpt, sg, hist2, flags1, cand, plan->cand_cap, meta,
-                        status, s);
-      tr.mark(li++);
-    }
-    if (e == hipSuccess) {
-      e = launch_pick(2, groups, st, hist2, 1, ng, s);
-      tr.mark(li++);
-    }
-    if (e == hipSuccess) {
-      e = launch_hist3(tiles, nt, st, summ, nl, lpt, sg, cand, meta, hist3, s);
-      tr.mark(li++);
-    }
-    if (e == hipSuccess) {
-      e = launch_pick(3, groups, st, hist3, 1, ng, s);
-      tr.mark(li++);
-    }
-    if (e == hipSuccess) {
-      e = launch_groupscan(groups, st, ng, gbase, s);
-      tr.mark(li++);
-    }
-    if (e == hipSuccess) {
+                        status, s, tr.at(li++));
+    if (e == hipSuccess) e = launch_pick(2, groups, st, hist2, 1, ng, s, tr.at(li++));
+    if (e == hipSuccess)
+      e = launch_hist3(tiles, nt, st, summ, nl, lpt, sg, cand, meta, hist3, s, tr.at(li++));
+    if (e == hipSuccess) e = launch_pick(3, groups, st, hist3, 1, ng, s, tr.at(li++));
+    if (e == hipSuccess) e = launch_groupscan(groups, st, ng, gbase, s, tr.at(li++));
+    if (e == hipSuccess)
       e = launch_emit(tiles, nt, groups, st, summ, nl, lpt, sg, cand, meta, gbase, flags2,
-                      idx_out, val_out, status, clear_next, clear_words, s);
-      tr.mark(li++);
-    }
+                      idx_out, val_out, status, clear_next, clear_words, s, tr.at(li++));
   }
   if (e != hipSuccess) {
     plan->needs_clear = true;
@@ -614,16 +597,13 @@ extern "C" int tkef_update_execute(tkef_update_plan plan, const int32_t* idx, co
   int32_t* seg = reinterpret_cast<int32_t*>(base + plan->off_seg);
   const int sparse_mode = (mu == 0.0f && wd == 0.0f) ? 1 : 0;
   const int has_mom = (mu != 0.0f) ? 1 : 0;
-  const Tracer tr{plan->events, plan->n_events, s};
-  if (tr.ev && tr.n > 0) (void)hipEventRecord(tr.ev[0], s);
+  const Tracer tr{plan->events, plan->n_events};
   hipError_t e = launch_seg(idx, plan->stride, nnz, plan->P, (int32_t)plan->d, plan->ntiles_u,
-                            seg, status, s);
-  tr.mark(0);
-  if (e == hipSuccess) {
+                            seg, status, s, tr.at(0));
+  if (e == hipSuccess)
     e = launch_update(tens, first, plan->ntensors, (int32_t)plan->d, plan->ntiles_u, idx, val,
-                      plan->stride, nnz, plan->P, seg, lr, mu, wd, sparse_mode, has_mom, s);
-    tr.mark(1);
-  }
+                      plan->stride, nnz, plan->P, seg, lr, mu, wd, sparse_mode, has_mom, s,
+                      tr.at(1));
   return hip_rc(e);
 }
 

@@ -69,42 +69,47 @@ struct UpdTensor {       // 32 B, one per parameter tensor, written at bind
 static_assert(sizeof(UpdTensor) == 32, "UpdTensor layout");
 
 // ---- kernel launchers (tkef_kernels.hip) --------------------------------------
+// Optional timing events attached to one launch (recorded by the dispatch
+// itself at the kernel's start and end).
+struct Ev {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
 // Each returns the hipError_t of its launch.
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
 hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, uint32_t* hist1,
-                         int32_t nslots, uint16_t* summ, uint32_t* status, hipStream_t s);
+                         int32_t nslots, uint16_t* summ, uint32_t* status, hipStream_t s, const Ev& ev);
 hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
-                       const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s);
+                       const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s, const Ev& ev);
 // one selection group
 constexpr int kPerBin = 4;  // band keys per (level-2 bin, region) kept in the rbin table
 hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
                           const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
                           int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* rbin,
                           uint32_t* rcand, uint32_t* rband, uint32_t* rsuf, uint32_t* rcnt,
-                          hipStream_t s);
+                          hipStream_t s, const Ev& ev);
 hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
                          int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
                          const uint32_t* rcand, const uint32_t* rband, const uint32_t* rsuf,
                          const uint32_t* rcnt, int32_t* idx_out, float* val_out,
-                         uint32_t* clear_next, int64_t clear_words, hipStream_t s);
+                         uint32_t* clear_next, int64_t clear_words, hipStream_t s, const Ev& ev);
 // several selection groups
 hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
                          int64_t nlines, int lpt, int32_t grid, uint32_t* hist2, uint64_t* flags,
                          int32_t* cand, uint32_t cap, uint32_t* meta, uint32_t* status,
-                         hipStream_t s);
+                         hipStream_t s, const Ev& ev);
 hipError_t launch_hist3(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
                         const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
                         const int32_t* cand, const uint32_t* meta, uint32_t* hist3,
-                        hipStream_t s);
+                        hipStream_t s, const Ev& ev);
 hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32_t ngroups,
-                            uint32_t* base, hipStream_t s);
+                            uint32_t* base, hipStream_t s, const Ev& ev);
 hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
                        const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
                        int32_t grid, const int32_t* cand, const uint32_t* meta,
                        const uint32_t* base, uint64_t* flags, int32_t* idx_out, float* val_out,
                        uint32_t* status, uint32_t* clear_next, int64_t clear_words,
-                       hipStream_t s);
+                       hipStream_t s, const Ev& ev);
 // launch-shape limits of the selection kernels
 int32_t select_max_groups();
 int32_t select_block();
@@ -112,11 +117,11 @@ int32_t select_max_lpt();
 
 hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, int32_t P,
                       int32_t d, int32_t ntiles_u, int32_t* seg, uint32_t* status,
-                      hipStream_t s);
+                      hipStream_t s, const Ev& ev);
 hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32_t ntens,
                          int32_t d, int32_t ntiles_u, const int32_t* idx, const float* val,
                          int64_t stride, const int32_t* nnz, int32_t P, const int32_t* seg,
                          float lr, float mu, float wd, int sparse_mode, int has_mom,
-                         hipStream_t s);
+                         hipStream_t s, const Ev& ev);
 
 }  // namespace tkef

@@ -21,6 +21,7 @@
 //            are ascending, so tile boundaries are where idx >> shift grows)
 //   update   per tile: LDS accumulation of all workers' entries of the tile,
 //            then one pass applying the SGD step to that parameter range
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "tkef.h"
@@ -1589,49 +1590,51 @@ __global__ __launch_bounds__(kUBlock) void k_update(
 }
 
 // ---------------------------------------------------------------------------
-// launchers
+// launchers (the timing events, when given, are recorded by the dispatch)
+
+template <typename K, typename... Args>
+hipError_t launch(K kernel, dim3 grid, dim3 block, hipStream_t s, const Ev& ev, Args... args) {
+  hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev.start, ev.stop, 0, args...);
+  return hipGetLastError();
+}
 
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   int64_t blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)blocks), dim3(256), 0, s, p, v, n);
-  return hipGetLastError();
+  return launch(k_fill_u32, dim3((unsigned)blocks), dim3(256), s, Ev{}, p, v, n);
 }
 
 hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, uint32_t* hist1,
-                         int32_t nslots, uint16_t* summ, uint32_t* status, hipStream_t s) {
-  hipLaunchKernelGGL(k_stream, dim3(grid), dim3(kBlock), 0, s, tiles, ntiles, hist1, nslots,
-                     summ, status);
-  return hipGetLastError();
+                         int32_t nslots, uint16_t* summ, uint32_t* status, hipStream_t s,
+                         const Ev& ev) {
+  return launch(k_stream, dim3(grid), dim3(kBlock), s, ev, tiles, ntiles, hist1, nslots, summ,
+                status);
 }
 
 hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
-                       const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s) {
+                       const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s,
+                       const Ev& ev) {
   static_assert(kH1Bins == 8 * kBlock && kH2Bins == 4 * kBlock && kH3Bins == 4 * kBlock,
                 "pick: bins per thread");
   if (level == 1) {
     if (nslots != kSlotsMany) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_pick<8, kSlotsMany>), dim3(ngroups), dim3(kBlock), 0, s, level, groups,
-                       st, hist);
-  } else {
-    if (nslots != 1) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_pick<4, 1>), dim3(ngroups), dim3(kBlock), 0, s, level, groups, st,
-                       hist);
+    return launch(k_pick<8, kSlotsMany>, dim3(ngroups), dim3(kBlock), s, ev, level, groups, st,
+                  hist);
   }
-  return hipGetLastError();
+  if (nslots != 1) return hipErrorInvalidValue;
+  return launch(k_pick<4, 1>, dim3(ngroups), dim3(kBlock), s, ev, level, groups, st, hist);
 }
 
 hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
                           const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
                           int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* rbin,
                           uint32_t* rcand, uint32_t* rband, uint32_t* rsuf, uint32_t* rcnt,
-                          hipStream_t s) {
+                          hipStream_t s, const Ev& ev) {
   if (nslots != kSlotsOne) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_collect, dim3(grid), dim3(kSBlock), 0, s, tiles, groups, st, hist1,
-                     summ, hist2, rbin, reinterpret_cast<uint4*>(rcand), rband, rsuf,
-                     reinterpret_cast<uint2*>(rcnt), rcap, lpt, nlines);
-  return hipGetLastError();
+  return launch(k_collect, dim3(grid), dim3(kSBlock), s, ev, tiles, groups, st, hist1, summ,
+                hist2, rbin, reinterpret_cast<uint4*>(rcand), rband, rsuf,
+                reinterpret_cast<uint2*>(rcnt), rcap, lpt, nlines);
 }
 
 hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
@@ -1639,37 +1642,33 @@ hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
                          const uint32_t* rcand, const uint32_t* rband, const uint32_t* rsuf,
                          const uint32_t* rcnt, int32_t* idx_out, float* val_out,
-                         uint32_t* clear_next, int64_t clear_words, hipStream_t s) {
-  hipLaunchKernelGGL(k_finish, dim3(grid), dim3(kSBlock), 0, s, tiles, groups, st, summ,
-                     nlines, lpt, rcap, hist2, rbin, reinterpret_cast<const uint4*>(rcand),
-                     rband, rsuf,
-                     reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, clear_next,
-                     clear_words);
-  return hipGetLastError();
+                         uint32_t* clear_next, int64_t clear_words, hipStream_t s,
+                         const Ev& ev) {
+  return launch(k_finish, dim3(grid), dim3(kSBlock), s, ev, tiles, groups, st, summ, nlines, lpt,
+                rcap, hist2, rbin, reinterpret_cast<const uint4*>(rcand), rband, rsuf,
+                reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, clear_next,
+                clear_words);
 }
 
 hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
                          int64_t nlines, int lpt, int32_t grid, uint32_t* hist2, uint64_t* flags,
                          int32_t* cand, uint32_t cap, uint32_t* meta, uint32_t* status,
-                         hipStream_t s) {
-  hipLaunchKernelGGL(k_gather, dim3(grid), dim3(kSBlock), 0, s, tiles, st, summ, nlines, lpt,
-                     hist2, flags, cand, cap, meta, status);
-  return hipGetLastError();
+                         hipStream_t s, const Ev& ev) {
+  return launch(k_gather, dim3(grid), dim3(kSBlock), s, ev, tiles, st, summ, nlines, lpt, hist2,
+                flags, cand, cap, meta, status);
 }
 
 hipError_t launch_hist3(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
                         const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
                         const int32_t* cand, const uint32_t* meta, uint32_t* hist3,
-                        hipStream_t s) {
-  hipLaunchKernelGGL(k_hist3, dim3(grid), dim3(kSBlock), 0, s, tiles, ntiles, st, summ, nlines,
-                     lpt, cand, meta, hist3);
-  return hipGetLastError();
+                        hipStream_t s, const Ev& ev) {
+  return launch(k_hist3, dim3(grid), dim3(kSBlock), s, ev, tiles, ntiles, st, summ, nlines, lpt,
+                cand, meta, hist3);
 }
 
 hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32_t ngroups,
-                            uint32_t* base, hipStream_t s) {
-  hipLaunchKernelGGL(k_groupscan, dim3(1), dim3(kSBlock), 0, s, groups, st, ngroups, base);
-  return hipGetLastError();
+                            uint32_t* base, hipStream_t s, const Ev& ev) {
+  return launch(k_groupscan, dim3(1), dim3(kSBlock), s, ev, groups, st, ngroups, base);
 }
 
 hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
@@ -1677,11 +1676,9 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
                        int32_t grid, const int32_t* cand, const uint32_t* meta,
                        const uint32_t* base, uint64_t* flags, int32_t* idx_out, float* val_out,
                        uint32_t* status, uint32_t* clear_next, int64_t clear_words,
-                       hipStream_t s) {
-  hipLaunchKernelGGL(k_emit, dim3(grid), dim3(kSBlock), 0, s, tiles, ntiles, groups, st, summ,
-                     nlines, lpt, cand, meta, base, flags, idx_out, val_out, status, clear_next,
-                     clear_words);
-  return hipGetLastError();
+                       hipStream_t s, const Ev& ev) {
+  return launch(k_emit, dim3(grid), dim3(kSBlock), s, ev, tiles, ntiles, groups, st, summ, nlines,
+                lpt, cand, meta, base, flags, idx_out, val_out, status, clear_next, clear_words);
 }
 
 int32_t select_max_groups() { return kSMaxGroups; }
@@ -1690,24 +1687,22 @@ int32_t select_max_lpt() { return kSMaxLpt; }
 
 hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, int32_t P,
                       int32_t d, int32_t ntiles_u, int32_t* seg, uint32_t* status,
-                      hipStream_t s) {
+                      hipStream_t s, const Ev& ev) {
   int64_t bx = (stride + 255) / 256;
   if (bx < 1) bx = 1;
-  hipLaunchKernelGGL(k_seg, dim3((unsigned)bx, (unsigned)P), dim3(256), 0, s, idx, stride, nnz,
-                     P, d, ntiles_u, seg, status);
-  return hipGetLastError();
+  return launch(k_seg, dim3((unsigned)bx, (unsigned)P), dim3(256), s, ev, idx, stride, nnz, P, d,
+                ntiles_u, seg, status);
 }
 
 hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32_t ntens,
                          int32_t d, int32_t ntiles_u, const int32_t* idx, const float* val,
                          int64_t stride, const int32_t* nnz, int32_t P, const int32_t* seg,
                          float lr, float mu, float wd, int sparse_mode, int has_mom,
-                         hipStream_t s) {
+                         hipStream_t s, const Ev& ev) {
   const int32_t per_xcd = (ntiles_u + kXcds - 1) / kXcds;
-  hipLaunchKernelGGL(k_update, dim3(per_xcd * kXcds), dim3(kUBlock), 0, s, tens, tile_first,
-                     ntens, d, ntiles_u, per_xcd, idx, val, stride, nnz, P, seg, lr, mu, wd,
-                     sparse_mode, has_mom);
-  return hipGetLastError();
+  return launch(k_update, dim3(per_xcd * kXcds), dim3(kUBlock), s, ev, tens, tile_first, ntens, d,
+                ntiles_u, per_xcd, idx, val, stride, nnz, P, seg, lr, mu, wd, sparse_mode,
+                has_mom);
 }
 
 }  // namespace tkef
