@@ -307,7 +307,7 @@ extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* con
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       cus <= 0)
     return TKEF_EHIP;
-  const int64_t units = (int64_t)plan->ntiles * (kTile / 2048);
+  const int64_t units = (int64_t)plan->ntiles * (kTile / kStreamUnit);
   plan->stream_grid = (int32_t)std::min<int64_t>((int64_t)4 * cus, units);
   char* base = static_cast<char*>(ws);
   hipError_t e = hipMemcpyAsync(base + plan->off_tiles, plan->tiles.data(),

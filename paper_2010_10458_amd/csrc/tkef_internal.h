@@ -18,6 +18,9 @@ constexpr int kTile = 8192;
 constexpr int kLine = 32;
 constexpr int kLinesPerTile = kTile / kLine;  // == kBlock: one line per thread
 static_assert(kLinesPerTile == kBlock, "one summary line per thread");
+// The stream walks the tiles in units of kStreamUnit elements (a persistent
+// grid takes units round-robin).
+constexpr int kStreamUnit = 2048;
 
 // Magnitude key = float bits with the sign cleared. The threshold search is a
 // three-level radix select on it: 11 bits, then 10, then 10.

@@ -204,14 +204,17 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v, int64_t n) {
 //
 // Persistent grid (a few workgroups per CU) walking the tiles in quarters of
 // kQuarter elements, so that at any moment the whole GPU streams through one
-// compact window of memory. g and r are read with non-temporal loads (each is
-// read exactly once); x is stored normally so that the few lines re-read by
-// the later steps are likely still cached. Each workgroup keeps an LDS
+// compact window of memory. g and r are read and x is written with
+// non-temporal accesses: each element is touched once, and normal stores,
+// although a little faster for the stream alone, leave dirty lines whose
+// write-back slows the kernels that follow. Each workgroup keeps an LDS
 // histogram and adds it to one of `nslots` copies of its group's global
 // histogram when the group changes and at the end; the copies spread the
 // atomics of many workgroups over many addresses.
-constexpr int kQuarter = 2048;
+constexpr int kQuarter = kStreamUnit;
 constexpr int kQuarterLines = kQuarter / kLine;
+constexpr int kQV = kQuarter / (4 * kBlock);  // float4 of each array per thread per unit
+static_assert(kQV * 4 * kBlock == kQuarter && kTile % kQuarter == 0, "stream unit shape");
 
 // Non-temporal 16-byte load / store through a global-memory view.
 __device__ __forceinline__ float4 load_nt4(const float4* p) {
@@ -282,26 +285,25 @@ __global__ __launch_bounds__(kBlock) void k_stream(const TileDesc* __restrict__ 
     const bool full = len == kQuarter &&
         ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(r)) & 15u) == 0;
     if (full) {
-      // 512 float4 per quarter: two per thread; a line is 8 consecutive lanes
+      // kQV float4 of g and of r per thread, all loads in flight together; a
+      // line is 8 consecutive lanes
       const float4* __restrict__ g4 = reinterpret_cast<const float4*>(g);
       float4* __restrict__ r4 = reinterpret_cast<float4*>(r);
-      const float4 a0 = load_nt4(g4 + tid), a1 = load_nt4(g4 + kBlock + tid);
-      const float4 b0 = load_nt4(r4 + tid), b1 = load_nt4(r4 + kBlock + tid);
-      float4 x0, x1;
-      uint32_t m0 = add_quad(a0, b0, x0, h);
-      uint32_t m1 = add_quad(a1, b1, x1, h);
-      store_nt4(r4 + tid, x0);
-      store_nt4(r4 + kBlock + tid, x1);
-      tmax = max(tmax, max(m0, m1));
-      m0 = max(m0, (uint32_t)__shfl_xor((int)m0, 1));
-      m1 = max(m1, (uint32_t)__shfl_xor((int)m1, 1));
-      m0 = max(m0, (uint32_t)__shfl_xor((int)m0, 2));
-      m1 = max(m1, (uint32_t)__shfl_xor((int)m1, 2));
-      m0 = max(m0, (uint32_t)__shfl_xor((int)m0, 4));
-      m1 = max(m1, (uint32_t)__shfl_xor((int)m1, 4));
-      if ((tid & 7) == 0) {
-        sq[tid >> 3] = (uint16_t)(m0 >> 16);
-        sq[(kBlock + tid) >> 3] = (uint16_t)(m1 >> 16);
+      float4 a[kQV], b[kQV];
+#pragma unroll
+      for (int v = 0; v < kQV; ++v) a[v] = load_nt4(g4 + v * kBlock + tid);
+#pragma unroll
+      for (int v = 0; v < kQV; ++v) b[v] = load_nt4(r4 + v * kBlock + tid);
+#pragma unroll
+      for (int v = 0; v < kQV; ++v) {
+        float4 x;
+        uint32_t m = add_quad(a[v], b[v], x, h);
+        store_nt4(r4 + v * kBlock + tid, x);
+        tmax = max(tmax, m);
+        m = max(m, (uint32_t)__shfl_xor((int)m, 1));
+        m = max(m, (uint32_t)__shfl_xor((int)m, 2));
+        m = max(m, (uint32_t)__shfl_xor((int)m, 4));
+        if ((tid & 7) == 0) sq[(v * kBlock + tid) >> 3] = (uint16_t)(m >> 16);
       }
     } else {
       // partial or misaligned quarter: element by element, every load issued
@@ -736,15 +738,8 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
   const uint32_t k = groups[0].k;
   sblock_pick1<kSlotsOne>(hist1, k, wsum, res);
   const uint32_t B1 = res[0];
+  const uint32_t above1 = res[1];
   const uint32_t lo = B1 << kH1Shift;
-  if (w == 0 && tid == 0) {
-    GroupState s;
-    s.need = (res[1] < k) ? k - res[1] : 0u;
-    s.prefix = B1;
-    s.T = 0xFFFFFFFFu;
-    s.n_eq = 0u;
-    st[0] = s;
-  }
 
   // flagged lines in position order: thread order, then line order
   const uint32_t mask = ls.flagged([&](int) -> uint32_t { return lo; });
@@ -811,7 +806,9 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
       }
       cw += tot;
     }
-    __syncthreads();  // the line list is refilled next
+    // the line list is refilled for the next chunk (a barrier also waits for
+    // this thread's global stores, so it is skipped when none follows)
+    if (c0 + (uint32_t)kFlCap < F) __syncthreads();
   }
 
   // band members by level-2 bin from the top (thread tid owns bin 1023 - tid):
@@ -821,11 +818,12 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
   uint32_t bw;
   const uint32_t above = sblock_scan(cb, wsum, &bw);
   const bool band_ok = bw <= (uint32_t)kBandCap;  // every band key is in bandk
-  if (cb) atomicAdd(&hist2[bin], cb);
-  if (bw) rsuf[(size_t)w * kH2Bins + bin] = above;
   h[bin] = above;     // from here on: the bin's next slot in rband[w]
   hoff[bin] = above;  // the bin's first slot
   __syncthreads();
+  // (global stores after the last barrier: a barrier waits for them)
+  if (cb) atomicAdd(&hist2[bin], cb);
+  if (bw) rsuf[(size_t)w * kH2Bins + bin] = above;
   if (band_ok) {
     uint32_t* __restrict__ dst = rband + (size_t)w * rcap;
     for (uint32_t j = tid; j < bw; j += kSBlock) {
@@ -839,6 +837,14 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
   }
   if (tid == 0)
     rcnt[w] = make_uint2(cw | ((fits ? 0u : 1u) << 31), bw | ((band_ok ? 0u : 1u) << 31));
+  if (w == 0 && tid == 0) {  // the level-1 result
+    GroupState s;
+    s.need = (above1 < k) ? k - above1 : 0u;
+    s.prefix = B1;
+    s.T = 0xFFFFFFFFu;
+    s.n_eq = 0u;
+    st[0] = s;
+  }
 }
 
 // Calls f(key) for the level-2 class members (band members in bin B2) of the
@@ -904,10 +910,6 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   __shared__ uint16_t c2reg[kC2Cap];     // ... and their regions
   __shared__ uint32_t n2;
   const int tid = threadIdx.x, w = blockIdx.x, G = gridDim.x;
-  // clear the other copy of the zero-initialised scratch for the next run
-#pragma unroll 1
-  for (int64_t i = (int64_t)w * kSBlock + tid; i < clear_words; i += (int64_t)G * kSBlock)
-    clear_next[i] = 0u;
   h[tid] = 0u;
   for (int i = tid; i < kOvWords; i += kSBlock) ovbits[i] = 0u;
   if (tid == 0) n2 = 0u;
@@ -1087,6 +1089,11 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   const uint32_t sv[4] = {gt, eq, gtb, eqb};
   uint32_t pre[4], tot[4];
   block_scan4<kSBlock>(sv, wsum, pre, tot);
+  // clear the other copy of the zero-initialised scratch for the next run
+  // (after the last barrier, which would wait for these stores)
+#pragma unroll 1
+  for (int64_t i = (int64_t)w * kSBlock + tid; i < clear_words; i += (int64_t)G * kSBlock)
+    clear_next[i] = 0u;
   if (gt + eq == 0u) return;
   uint32_t gtr = tot[2] + pre[0];
   uint32_t eqr = tot[3] + pre[1];
