@@ -1371,10 +1371,19 @@ __global__ void k_seg(const int32_t* __restrict__ idx, int64_t stride,
                       const int32_t* __restrict__ nnz, int32_t P, int32_t d, int32_t ntiles_u,
                       int32_t* __restrict__ seg, uint32_t* __restrict__ status) {
   const int p = blockIdx.y;
-  int64_t n = nnz ? (int64_t)nnz[p] : stride;
-  n = n < 0 ? 0 : (n > stride ? stride : n);
   const int32_t* __restrict__ L = idx + (int64_t)p * stride;
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  // this entry and the one before it, read before the count is known (every
+  // j < stride is inside the list's storage), so all three loads overlap; no
+  // storage at all for stride == 0 (a kernel-wide value)
+  const int64_t jc = j < stride ? j : stride - 1;
+  int32_t i_here = 0, i_prev = 0;
+  if (stride > 0) {
+    i_here = L[jc];
+    i_prev = L[jc > 0 ? jc - 1 : 0];
+  }
+  int64_t n = nnz ? (int64_t)nnz[p] : stride;
+  n = n < 0 ? 0 : (n > stride ? stride : n);
   if (n == 0) {
     for (int64_t u = j; u <= ntiles_u; u += (int64_t)gridDim.x * blockDim.x)
       seg[u * P + p] = 0;
@@ -1384,12 +1393,12 @@ __global__ void k_seg(const int32_t* __restrict__ idx, int64_t stride,
   auto tile_of = [&](int32_t i) -> int32_t {
     return i < 0 ? 0 : (i >= d ? ntiles_u - 1 : (i >> kUShift));
   };
-  const int32_t i = L[j];
+  const int32_t i = i_here;
   uint32_t bad = (i < 0 || i >= d) ? TKEF_STATUS_INDEX_RANGE : 0u;
   const int32_t t = tile_of(i);
   int32_t tp = -1;
   if (j > 0) {
-    const int32_t ip = L[j - 1];
+    const int32_t ip = i_prev;
     if (ip > i) bad |= TKEF_STATUS_UNSORTED;
     tp = tile_of(ip);
   }
