@@ -44,6 +44,12 @@ extern "C" {
 #define TKEF_ESTATE (-5)     /* plan not bound, or bound to another workspace */
 #define TKEF_ENOMEM (-6)     /* host allocation failed */
 
+/* value formats of the (idx, val) lists */
+#define TKEF_VAL_F32 0 /* binary32 (default) */
+#define TKEF_VAL_F16 1 /* binary16, converted from binary32 with round-to-nearest-even
+                          (overflow to infinity, subnormals kept); Sec. 5.3 sends FP16
+                          elements */
+
 /* selection modes */
 #define TKEF_GLOBAL 0     /* one selection over the concatenated tensor list */
 #define TKEF_PER_TENSOR 1 /* one selection per tensor, k_t from rho per tensor */
@@ -112,11 +118,18 @@ int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float *const *grads,
                             hipStream_t stream);
 
 /* Runs one sparsify on the bound tensors: reads g, updates r in place, writes
- * k_total pairs to idx_out (device int32) and val_out (device float32). ws
+ * k_total pairs to idx_out (device int32) and val_out (device float32, or
+ * binary16 after tkef_sparsify_plan_set_value_format(plan, TKEF_VAL_F16)). ws
  * must be the bound workspace. status: optional device word. Asynchronous. */
 int tkef_sparsify_execute(tkef_sparsify_plan plan, void *ws, size_t ws_bytes,
-                          int32_t *idx_out, float *val_out, uint32_t *status,
+                          int32_t *idx_out, void *val_out, uint32_t *status,
                           hipStream_t stream);
+
+/* Value format of val_out: TKEF_VAL_F32 (default) or TKEF_VAL_F16 (the wire
+ * format of Sec. 5.3). With binary16 values the residual still keeps the
+ * binary32 x where not selected and +0 where selected: the rounding of the
+ * sent value is not fed back. Host only; TKEF_EINVAL for another format. */
+int tkef_sparsify_plan_set_value_format(tkef_sparsify_plan plan, int32_t format);
 
 /* Optional timing hook: with n_events >= nlaunch + 1, each execution records
  * events[0] at the start of its first kernel and events[i + 1] at the end of
@@ -135,7 +148,7 @@ int tkef_sparsify_workspace(const int64_t *numels, int32_t ntensors, int32_t mod
                             int64_t *k_total);
 int tkef_sparsify(const float *const *grads, float *const *residuals,
                   const int64_t *numels, int32_t ntensors, int32_t mode, double rho,
-                  int64_t k, int32_t *idx_out, float *val_out, void *ws,
+                  int64_t k, int32_t *idx_out, void *val_out, void *ws,
                   size_t ws_bytes, uint32_t *status, hipStream_t stream);
 
 /* ========================================================================
@@ -176,13 +189,29 @@ int tkef_update_plan_bind(tkef_update_plan plan, float *const *params,
                           float *const *momentum, void *ws, size_t ws_bytes,
                           hipStream_t stream);
 
-/* Applies one aggregate + update. idx (device int32) and val (device float32)
- * hold P * stride entries; nnz: optional device int32 array of P counts
- * (each clamped to [0, stride]). mu != 0 needs momentum buffers at bind.
- * lr, mu, wd must be finite. Asynchronous. */
-int tkef_update_execute(tkef_update_plan plan, const int32_t *idx, const float *val,
+/* Applies one aggregate + update. idx (device int32) and val (device float32,
+ * or binary16 after tkef_update_plan_set_value_format(plan, TKEF_VAL_F16);
+ * binary16 values are widened exactly and summed in binary32) hold P * stride
+ * entries; nnz: optional device int32 array of P counts (each clamped to
+ * [0, stride]). mu != 0 needs momentum buffers at bind. lr, mu, wd must be
+ * finite. Asynchronous. */
+int tkef_update_execute(tkef_update_plan plan, const int32_t *idx, const void *val,
                         const int32_t *nnz, float lr, float mu, float wd, void *ws,
                         size_t ws_bytes, uint32_t *status, hipStream_t stream);
+
+/* Aggregation only (Alg. 2, which returns the accumulated g~ = sum over the
+ * m gathered lists, each added at its indices into a zeroed vector): writes
+ * G_i into the bound tensors at every position (0 where no list names it);
+ * their previous contents are not read. Same lists, value formats and
+ * summation as tkef_update_execute; momentum buffers are not used.
+ * Asynchronous. */
+int tkef_aggregate_execute(tkef_update_plan plan, const int32_t *idx, const void *val,
+                           const int32_t *nnz, void *ws, size_t ws_bytes, uint32_t *status,
+                           hipStream_t stream);
+
+/* Value format of the val arrays execute / aggregate read: TKEF_VAL_F32
+ * (default) or TKEF_VAL_F16. Host only. */
+int tkef_update_plan_set_value_format(tkef_update_plan plan, int32_t format);
 
 /* Optional timing hook, as tkef_sparsify_plan_set_events. */
 int tkef_update_plan_set_events(tkef_update_plan plan, hipEvent_t *events,
@@ -195,10 +224,16 @@ int tkef_update_workspace(const int64_t *numels, int32_t ntensors, int32_t P,
                           int64_t stride, size_t *workspace_bytes);
 int tkef_sparse_aggregate_update(float *const *params, float *const *momentum,
                                  const int64_t *numels, int32_t ntensors,
-                                 const int32_t *idx, const float *val, int32_t P,
+                                 const int32_t *idx, const void *val, int32_t P,
                                  int64_t stride, const int32_t *nnz, float lr,
                                  float mu, float wd, void *ws, size_t ws_bytes,
                                  uint32_t *status, hipStream_t stream);
+/* One-shot aggregation into the T tensors outs (create + bind + aggregate +
+ * destroy; synchronizes `stream` once, during bind). val_format as above. */
+int tkef_sparse_aggregate(float *const *outs, const int64_t *numels, int32_t ntensors,
+                          const int32_t *idx, const void *val, int32_t val_format, int32_t P,
+                          int64_t stride, const int32_t *nnz, void *ws, size_t ws_bytes,
+                          uint32_t *status, hipStream_t stream);
 
 #ifdef __cplusplus
 }

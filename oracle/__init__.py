@@ -60,6 +60,8 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_rank.restype = i64
     lib.oracle_update.argtypes = [vp, vp, i64, i32, vp, vp, i64, vp, f32, f32, f32]
     lib.oracle_update.restype = ctypes.c_int
+    lib.oracle_aggregate.argtypes = [vp, i64, i32, vp, vp, i64, vp]
+    lib.oracle_aggregate.restype = ctypes.c_int
     return lib
 
 
@@ -87,6 +89,14 @@ def _ptr(a: np.ndarray) -> int:
 
 def _f32(a) -> np.ndarray:
     return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def f16_rne(x) -> np.ndarray:
+    """Values on the wire in 16-bit floating point (Sec. 5.3 sends FP16
+    elements): binary32 -> binary16, round to nearest, ties to even, overflow
+    to infinity, subnormals kept (numpy's IEEE conversion)."""
+    with np.errstate(over="ignore"):
+        return np.ascontiguousarray(x, dtype=np.float32).astype(np.float16)
 
 
 class Oracle:
@@ -167,6 +177,22 @@ class Oracle:
                 np.concatenate(vals) if vals else np.empty(0, np.float32), outs, ks)
 
     # -- aggregate + update ------------------------------------------------
+    def aggregate(self, d: int, idx, val, nnz=None) -> np.ndarray:
+        """Dense sum of the lists (Alg. 2 accumulation), worker order. idx,
+        val: (P, stride) gathered layout (float16 values are widened exactly)."""
+        idx = np.ascontiguousarray(idx, dtype=np.int32)
+        val = np.ascontiguousarray(np.asarray(val).astype(np.float32))
+        if idx.ndim == 1:
+            idx, val = idx[None, :], val[None, :]
+        P, stride = idx.shape
+        nnz = np.full(P, stride, np.int64) if nnz is None else np.ascontiguousarray(nnz, np.int64)
+        # NaN-filled, so that a position the C code never writes shows up
+        out = np.full(max(d, 1), np.nan, dtype=np.float32)
+        rc = self.lib.oracle_aggregate(_ptr(out), d, P, _ptr(idx), _ptr(val), stride, _ptr(nnz))
+        if rc != ORC_OK:
+            raise OracleError(f"oracle_aggregate rc={rc}")
+        return out[:d]
+
     def update(self, w, b, idx, val, nnz=None, lr=0.1, mu=0.0, wd=0.0
                ) -> Tuple[np.ndarray, Optional[np.ndarray]]:
         """w, b: flat float32 (copies are updated and returned). idx, val:

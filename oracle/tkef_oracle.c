@@ -193,3 +193,26 @@ int oracle_update(float *w, float *b, int64_t d, int32_t P,
     free(touched);
     return ORC_OK;
 }
+
+/* Aggregation alone (Alg. 2, which returns the accumulated vector: g~ = 0,
+ * then for p = 1..m in order: g~[iota_p] += kappa_p), written densely:
+ * out[i] = the binary32 sum, in worker order, of the values that the lists
+ * give position i; 0 where no list names i. */
+int oracle_aggregate(float *out, int64_t d, int32_t P, const int32_t *idx,
+                     const float *val, int64_t stride, const int64_t *nnz) {
+    if (d < 0 || P < 0 || stride < 0) return ORC_EINVAL;
+    for (int32_t q = 0; q < P; ++q) {
+        if (nnz[q] < 0 || nnz[q] > stride) return ORC_EINVAL;
+        for (int64_t j = 0; j < nnz[q]; ++j) {
+            int32_t i = idx[(int64_t)q * stride + j];
+            if (i < 0 || (int64_t)i >= d) return ORC_ERANGE;
+        }
+    }
+    for (int64_t i = 0; i < d; ++i) out[i] = 0.0f;
+    for (int32_t q = 0; q < P; ++q) {
+        const int32_t *iq = idx + (int64_t)q * stride;
+        const float *vq = val + (int64_t)q * stride;
+        for (int64_t j = 0; j < nnz[q]; ++j) out[iq[j]] += vq[j];
+    }
+    return ORC_OK;
+}

@@ -30,6 +30,8 @@ PER_TENSOR = 1
 STATUS_NAN = 1
 STATUS_UNSORTED = 2
 STATUS_INDEX_RANGE = 4
+VAL_F32 = 0
+VAL_F16 = 1
 
 OK, EINVAL, ERANGE, EWORKSPACE, EHIP, ESTATE, ENOMEM = 0, -1, -2, -3, -4, -5, -6
 
@@ -59,6 +61,7 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
         "tkef_sparsify_execute": ([vp, vp, sz, vp, vp, vp, vp], ctypes.c_int),
         "tkef_sparsify_plan_set_events": ([vp, P(vp), i32], ctypes.c_int),
         "tkef_sparsify_plan_launch_name": ([vp, i32], ctypes.c_char_p),
+        "tkef_sparsify_plan_set_value_format": ([vp, i32], ctypes.c_int),
         "tkef_sparsify_workspace": ([P(i64), i32, i32, f64, i64, P(sz), P(i64)], ctypes.c_int),
         "tkef_sparsify": ([P(vp), P(vp), P(i64), i32, i32, f64, i64, vp, vp, vp, sz, vp, vp],
                           ctypes.c_int),
@@ -69,6 +72,10 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
         "tkef_update_execute": ([vp, vp, vp, vp, f32, f32, f32, vp, sz, vp, vp], ctypes.c_int),
         "tkef_update_plan_set_events": ([vp, P(vp), i32], ctypes.c_int),
         "tkef_update_plan_launch_name": ([vp, i32], ctypes.c_char_p),
+        "tkef_update_plan_set_value_format": ([vp, i32], ctypes.c_int),
+        "tkef_aggregate_execute": ([vp, vp, vp, vp, vp, sz, vp, vp], ctypes.c_int),
+        "tkef_sparse_aggregate": ([P(vp), P(i64), i32, vp, vp, i32, i32, i64, vp, vp, sz, vp,
+                                   vp], ctypes.c_int),
         "tkef_update_workspace": ([P(i64), i32, i32, i64, P(sz)], ctypes.c_int),
         "tkef_sparse_aggregate_update": ([P(vp), P(vp), P(i64), i32, vp, vp, i32, i64, vp, f32,
                                           f32, f32, vp, sz, vp, vp], ctypes.c_int),
@@ -124,6 +131,14 @@ def _check_f32_tensors(ts: Sequence[torch.Tensor], what: str) -> None:
             raise ValueError(f"{what}: expected contiguous float32 CUDA tensors")
 
 
+def _val_format(dtype) -> int:
+    if dtype == torch.float32:
+        return VAL_F32
+    if dtype == torch.float16:
+        return VAL_F16
+    raise ValueError("values are float32 or float16")
+
+
 def _events(events: Optional[Sequence[torch.cuda.Event]]):
     """Raw event handles of torch events (each recorded once so it exists)."""
     if not events:
@@ -140,13 +155,16 @@ class SparsifyPlan:
     """Plan for sparsifying a fixed list of tensor sizes (see tkef.h)."""
 
     def __init__(self, numels: Sequence[int], mode: int = GLOBAL, rho: Optional[float] = None,
-                 k: Optional[int] = None):
+                 k: Optional[int] = None, val_dtype=torch.float32):
         self._numels = [int(n) for n in numels]
         self._h = ctypes.c_void_p()
         L = lib()
         _check("tkef_sparsify_plan_create", L.tkef_sparsify_plan_create(
             _i64_array(self._numels), len(self._numels), int(mode),
             float(rho) if rho is not None else 0.0, int(k) if k else 0, ctypes.byref(self._h)))
+        self.val_dtype = val_dtype
+        _check("tkef_sparsify_plan_set_value_format",
+               L.tkef_sparsify_plan_set_value_format(self._h, _val_format(val_dtype)))
         ws, kt, d, ng, nl = (ctypes.c_size_t(), ctypes.c_int64(), ctypes.c_int64(),
                              ctypes.c_int32(), ctypes.c_int32())
         _check("tkef_sparsify_plan_info", L.tkef_sparsify_plan_info(
@@ -207,11 +225,11 @@ class SparsifyPlan:
         if idx_out is None:
             idx_out = torch.empty(max(self.k_total, 1), dtype=torch.int32, device=dev)
         if val_out is None:
-            val_out = torch.empty(max(self.k_total, 1), dtype=torch.float32, device=dev)
+            val_out = torch.empty(max(self.k_total, 1), dtype=self.val_dtype, device=dev)
         if idx_out.numel() < self.k_total or val_out.numel() < self.k_total:
             raise ValueError("output buffers too small")
-        if idx_out.dtype != torch.int32 or val_out.dtype != torch.float32:
-            raise ValueError("idx_out must be int32 and val_out float32")
+        if idx_out.dtype != torch.int32 or val_out.dtype != self.val_dtype:
+            raise ValueError("idx_out must be int32 and val_out of the plan's value dtype")
         _check("tkef_sparsify_execute", lib().tkef_sparsify_execute(
             self._h, self.ws.data_ptr(), self.ws.numel(), idx_out.data_ptr(),
             val_out.data_ptr(), status.data_ptr() if status is not None else None,
@@ -222,7 +240,7 @@ class SparsifyPlan:
 class UpdatePlan:
     """Plan for the sparse aggregate + SGD update of a fixed parameter list."""
 
-    def __init__(self, numels: Sequence[int], P: int, stride: int):
+    def __init__(self, numels: Sequence[int], P: int, stride: int, val_dtype=torch.float32):
         self._numels = [int(n) for n in numels]
         self.P, self.stride = int(P), int(stride)
         self._h = ctypes.c_void_p()
@@ -230,6 +248,9 @@ class UpdatePlan:
         _check("tkef_update_plan_create", L.tkef_update_plan_create(
             _i64_array(self._numels), len(self._numels), self.P, self.stride,
             ctypes.byref(self._h)))
+        self.val_dtype = val_dtype
+        _check("tkef_update_plan_set_value_format",
+               L.tkef_update_plan_set_value_format(self._h, _val_format(val_dtype)))
         ws, d, nl = ctypes.c_size_t(), ctypes.c_int64(), ctypes.c_int32()
         _check("tkef_update_plan_info", L.tkef_update_plan_info(
             self._h, ctypes.byref(ws), ctypes.byref(d), ctypes.byref(nl)))
@@ -271,23 +292,36 @@ class UpdatePlan:
         self._events = (arr, list(events) if events else None)
         _check("tkef_update_plan_set_events", lib().tkef_update_plan_set_events(self._h, arr, n))
 
-    def execute(self, idx: torch.Tensor, val: torch.Tensor, lr: float, mu: float = 0.0,
-                wd: float = 0.0, nnz: Optional[torch.Tensor] = None,
-                status: Optional[torch.Tensor] = None, stream=None) -> None:
+    def _check_lists(self, idx, val, nnz):
         if self._bound is None or self.ws is None:
             raise RuntimeError("plan is not bound")
-        if idx.dtype != torch.int32 or val.dtype != torch.float32:
-            raise ValueError("idx must be int32 and val float32")
+        if idx.dtype != torch.int32 or val.dtype != self.val_dtype:
+            raise ValueError("idx must be int32 and val of the plan's value dtype")
         if not (idx.is_cuda and val.is_cuda and idx.is_contiguous() and val.is_contiguous()):
             raise ValueError("idx and val must be contiguous CUDA tensors")
         if idx.numel() < self.P * self.stride or val.numel() < self.P * self.stride:
             raise ValueError("idx / val hold fewer than P * stride entries")
         if nnz is not None and (nnz.dtype != torch.int32 or nnz.numel() < self.P or not nnz.is_cuda):
             raise ValueError("nnz must be a CUDA int32 tensor of P counts")
+
+    def execute(self, idx: torch.Tensor, val: torch.Tensor, lr: float, mu: float = 0.0,
+                wd: float = 0.0, nnz: Optional[torch.Tensor] = None,
+                status: Optional[torch.Tensor] = None, stream=None) -> None:
+        self._check_lists(idx, val, nnz)
         _check("tkef_update_execute", lib().tkef_update_execute(
             self._h, idx.data_ptr(), val.data_ptr(),
             nnz.data_ptr() if nnz is not None else None, float(lr), float(mu), float(wd),
             self.ws.data_ptr(), self.ws.numel(),
+            status.data_ptr() if status is not None else None, _stream_handle(stream)))
+
+    def aggregate(self, idx: torch.Tensor, val: torch.Tensor, nnz: Optional[torch.Tensor] = None,
+                  status: Optional[torch.Tensor] = None, stream=None) -> None:
+        """Writes the sum of the P lists into the bound tensors (every
+        position; zero where no list names it)."""
+        self._check_lists(idx, val, nnz)
+        _check("tkef_aggregate_execute", lib().tkef_aggregate_execute(
+            self._h, idx.data_ptr(), val.data_ptr(),
+            nnz.data_ptr() if nnz is not None else None, self.ws.data_ptr(), self.ws.numel(),
             status.data_ptr() if status is not None else None, _stream_handle(stream)))
 
 
@@ -296,10 +330,12 @@ class UpdatePlan:
 
 def sparsify(grads: Sequence[torch.Tensor], residuals: Sequence[torch.Tensor],
              rho: Optional[float] = None, mode: int = GLOBAL, k: Optional[int] = None,
-             status: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+             status: Optional[torch.Tensor] = None, val_dtype=torch.float32
+             ) -> Tuple[torch.Tensor, torch.Tensor]:
     """x = g + r; top-k of |x| (ties to the lower position); r <- x with the
-    selected entries zeroed. Returns (idx int32, val float32)."""
-    plan = SparsifyPlan([t.numel() for t in grads], mode=mode, rho=rho, k=k)
+    selected entries zeroed. Returns (idx int32, val of val_dtype: float32,
+    or float16 rounded to nearest even)."""
+    plan = SparsifyPlan([t.numel() for t in grads], mode=mode, rho=rho, k=k, val_dtype=val_dtype)
     plan.bind(grads, residuals)
     return plan.execute(status=status)
 
@@ -315,6 +351,19 @@ def sparse_aggregate_update(params: Sequence[torch.Tensor], idx: torch.Tensor,
     if idx.dim() == 1:
         idx, val = idx.view(1, -1), val.view(1, -1)
     P, stride = idx.shape
-    plan = UpdatePlan([t.numel() for t in params], P=P, stride=stride)
+    plan = UpdatePlan([t.numel() for t in params], P=P, stride=stride, val_dtype=val.dtype)
     plan.bind(params, momentum)
     plan.execute(idx.contiguous(), val.contiguous(), lr=lr, mu=mu, wd=wd, nnz=nnz, status=status)
+
+
+def sparse_aggregate(outs: Sequence[torch.Tensor], idx: torch.Tensor, val: torch.Tensor,
+                     nnz: Optional[torch.Tensor] = None,
+                     status: Optional[torch.Tensor] = None) -> None:
+    """outs <- sum of P workers' sparse lists (idx, val: (P, stride) gathered
+    layout), densely: every position written, zero where no list names it."""
+    if idx.dim() == 1:
+        idx, val = idx.view(1, -1), val.view(1, -1)
+    P, stride = idx.shape
+    plan = UpdatePlan([t.numel() for t in outs], P=P, stride=stride, val_dtype=val.dtype)
+    plan.bind(outs)
+    plan.aggregate(idx.contiguous(), val.contiguous(), nnz=nnz, status=status)

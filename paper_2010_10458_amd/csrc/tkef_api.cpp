@@ -120,6 +120,7 @@ struct tkef_sparsify_plan_s {
          off_hist1 = 0, off_hist2 = 0, off_hist3 = 0, off_flags1 = 0, off_flags2 = 0,
          off_meta = 0, off_summ = 0, off_base = 0, off_cand = 0, off_rcand = 0, off_rband = 0,
          off_rsuf = 0, off_rcnt = 0, off_rbin = 0, ws_bytes = 0;
+  int32_t val_format = TKEF_VAL_F32;  // value array written by execute
   uint64_t executions = 0;   // since the last bind
   bool needs_clear = true;   // both copies must be cleared before the next run
   int32_t nlaunch() const { return ngroups == 1 ? kSparsifyNLaunchOne : kSparsifyNLaunchMany; }
@@ -350,8 +351,14 @@ extern "C" const char* tkef_sparsify_plan_launch_name(tkef_sparsify_plan plan, i
   return plan->ngroups == 1 ? kSparsifyLaunchesOne[i] : kSparsifyLaunchesMany[i];
 }
 
+extern "C" int tkef_sparsify_plan_set_value_format(tkef_sparsify_plan plan, int32_t format) {
+  if (!plan || (format != TKEF_VAL_F32 && format != TKEF_VAL_F16)) return TKEF_EINVAL;
+  plan->val_format = format;
+  return TKEF_OK;
+}
+
 extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t ws_bytes,
-                                     int32_t* idx_out, float* val_out, uint32_t* status,
+                                     int32_t* idx_out, void* val_out, uint32_t* status,
                                      hipStream_t s) {
   if (!plan) return TKEF_EINVAL;
   if (!ws || ws_bytes < plan->ws_bytes || !aligned_ws(ws)) return TKEF_EWORKSPACE;
@@ -371,6 +378,7 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   const int64_t nl = plan->nlines;
   const int lpt = plan->sel_lpt, sg = plan->sel_grid;
   const Tracer tr{plan->events, plan->n_events};
+  const int val16 = plan->val_format == TKEF_VAL_F16 ? 1 : 0;
   int li = 0;  // launch index, for the timing hook
   uint32_t* clear_next = reinterpret_cast<uint32_t*>(zn);
   const int64_t clear_words = (int64_t)(plan->zero_bytes / 4);
@@ -396,7 +404,7 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
                          hist2, rbin, rcand, rband, rsuf, rcnt, s, tr.at(li++));
     if (e == hipSuccess)
       e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, plan->rcap, hist2, rbin, rcand,
-                        rband, rsuf, rcnt, idx_out, val_out, clear_next, clear_words, s,
+                        rband, rsuf, rcnt, idx_out, val_out, val16, clear_next, clear_words, s,
                         tr.at(li++));
   } else {
     uint32_t* hist3 = reinterpret_cast<uint32_t*>(zb + plan->off_hist3);
@@ -417,7 +425,7 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     if (e == hipSuccess) e = launch_groupscan(groups, st, ng, gbase, s, tr.at(li++));
     if (e == hipSuccess)
       e = launch_emit(tiles, nt, groups, st, summ, nl, lpt, sg, cand, meta, gbase, flags2,
-                      idx_out, val_out, status, clear_next, clear_words, s, tr.at(li++));
+                      idx_out, val_out, val16, status, clear_next, clear_words, s, tr.at(li++));
   }
   if (e != hipSuccess) {
     plan->needs_clear = true;
@@ -440,7 +448,7 @@ extern "C" int tkef_sparsify_workspace(const int64_t* numels, int32_t ntensors, 
 
 extern "C" int tkef_sparsify(const float* const* grads, float* const* residuals,
                              const int64_t* numels, int32_t ntensors, int32_t mode, double rho,
-                             int64_t k, int32_t* idx_out, float* val_out, void* ws,
+                             int64_t k, int32_t* idx_out, void* val_out, void* ws,
                              size_t ws_bytes, uint32_t* status, hipStream_t stream) {
   tkef_sparsify_plan p = nullptr;
   int rc = tkef_sparsify_plan_create(numels, ntensors, mode, rho, k, &p);
@@ -466,6 +474,7 @@ struct tkef_update_plan_s {
   size_t off_tens = 0, off_first = 0, off_seg = 0, ws_bytes = 0;
   void* bound_ws = nullptr;
   bool has_mom = false;
+  int32_t val_format = TKEF_VAL_F32;  // value arrays read by execute / aggregate
   hipEvent_t* events = nullptr;
   int32_t n_events = 0;
 };
@@ -582,29 +591,54 @@ extern "C" const char* tkef_update_plan_launch_name(tkef_update_plan plan, int32
   return kUpdateLaunches[i];
 }
 
-extern "C" int tkef_update_execute(tkef_update_plan plan, const int32_t* idx, const float* val,
-                                   const int32_t* nnz, float lr, float mu, float wd, void* ws,
-                                   size_t ws_bytes, uint32_t* status, hipStream_t s) {
+extern "C" int tkef_update_plan_set_value_format(tkef_update_plan plan, int32_t format) {
+  if (!plan || (format != TKEF_VAL_F32 && format != TKEF_VAL_F16)) return TKEF_EINVAL;
+  plan->val_format = format;
+  return TKEF_OK;
+}
+
+namespace {
+
+// seg + update with the given operation on the tile sums.
+int update_run(tkef_update_plan plan, const int32_t* idx, const void* val, const int32_t* nnz,
+               float lr, float mu, float wd, int op, void* ws, size_t ws_bytes,
+               uint32_t* status, hipStream_t s) {
   if (!plan) return TKEF_EINVAL;
   if (!ws || ws_bytes < plan->ws_bytes || !aligned_ws(ws)) return TKEF_EWORKSPACE;
   if (plan->bound_ws != ws) return TKEF_ESTATE;
   if (plan->stride > 0 && (!idx || !val)) return TKEF_EINVAL;
-  if (!std::isfinite(lr) || !std::isfinite(mu) || !std::isfinite(wd)) return TKEF_ERANGE;
-  if (mu != 0.0f && !plan->has_mom) return TKEF_EINVAL;
   char* base = static_cast<char*>(ws);
   const UpdTensor* tens = reinterpret_cast<const UpdTensor*>(base + plan->off_tens);
   const int32_t* first = reinterpret_cast<const int32_t*>(base + plan->off_first);
   int32_t* seg = reinterpret_cast<int32_t*>(base + plan->off_seg);
-  const int sparse_mode = (mu == 0.0f && wd == 0.0f) ? 1 : 0;
-  const int has_mom = (mu != 0.0f) ? 1 : 0;
+  const int has_mom = (op == kOpSgd && mu != 0.0f) ? 1 : 0;
+  const int val16 = plan->val_format == TKEF_VAL_F16 ? 1 : 0;
   const Tracer tr{plan->events, plan->n_events};
   hipError_t e = launch_seg(idx, plan->stride, nnz, plan->P, (int32_t)plan->d, plan->ntiles_u,
                             seg, status, s, tr.at(0));
   if (e == hipSuccess)
     e = launch_update(tens, first, plan->ntensors, (int32_t)plan->d, plan->ntiles_u, idx, val,
-                      plan->stride, nnz, plan->P, seg, lr, mu, wd, sparse_mode, has_mom, s,
+                      val16, plan->stride, nnz, plan->P, seg, lr, mu, wd, op, has_mom, s,
                       tr.at(1));
   return hip_rc(e);
+}
+
+}  // namespace
+
+extern "C" int tkef_update_execute(tkef_update_plan plan, const int32_t* idx, const void* val,
+                                   const int32_t* nnz, float lr, float mu, float wd, void* ws,
+                                   size_t ws_bytes, uint32_t* status, hipStream_t s) {
+  if (!plan) return TKEF_EINVAL;
+  if (!std::isfinite(lr) || !std::isfinite(mu) || !std::isfinite(wd)) return TKEF_ERANGE;
+  if (mu != 0.0f && !plan->has_mom) return TKEF_EINVAL;
+  const int op = (mu == 0.0f && wd == 0.0f) ? kOpSparseSgd : kOpSgd;
+  return update_run(plan, idx, val, nnz, lr, mu, wd, op, ws, ws_bytes, status, s);
+}
+
+extern "C" int tkef_aggregate_execute(tkef_update_plan plan, const int32_t* idx, const void* val,
+                                      const int32_t* nnz, void* ws, size_t ws_bytes,
+                                      uint32_t* status, hipStream_t s) {
+  return update_run(plan, idx, val, nnz, 0.0f, 0.0f, 0.0f, kOpAggregate, ws, ws_bytes, status, s);
 }
 
 extern "C" int tkef_update_workspace(const int64_t* numels, int32_t ntensors, int32_t P,
@@ -619,7 +653,7 @@ extern "C" int tkef_update_workspace(const int64_t* numels, int32_t ntensors, in
 
 extern "C" int tkef_sparse_aggregate_update(float* const* params, float* const* momentum,
                                             const int64_t* numels, int32_t ntensors,
-                                            const int32_t* idx, const float* val, int32_t P,
+                                            const int32_t* idx, const void* val, int32_t P,
                                             int64_t stride, const int32_t* nnz, float lr,
                                             float mu, float wd, void* ws, size_t ws_bytes,
                                             uint32_t* status, hipStream_t stream) {
@@ -628,6 +662,20 @@ extern "C" int tkef_sparse_aggregate_update(float* const* params, float* const* 
   if (rc) return rc;
   rc = tkef_update_plan_bind(p, params, momentum, ws, ws_bytes, stream);
   if (!rc) rc = tkef_update_execute(p, idx, val, nnz, lr, mu, wd, ws, ws_bytes, status, stream);
+  tkef_update_plan_destroy(p);
+  return rc;
+}
+
+extern "C" int tkef_sparse_aggregate(float* const* outs, const int64_t* numels, int32_t ntensors,
+                                     const int32_t* idx, const void* val, int32_t val_format,
+                                     int32_t P, int64_t stride, const int32_t* nnz, void* ws,
+                                     size_t ws_bytes, uint32_t* status, hipStream_t stream) {
+  tkef_update_plan p = nullptr;
+  int rc = tkef_update_plan_create(numels, ntensors, P, stride, &p);
+  if (rc) return rc;
+  rc = tkef_update_plan_set_value_format(p, val_format);
+  if (!rc) rc = tkef_update_plan_bind(p, outs, nullptr, ws, ws_bytes, stream);
+  if (!rc) rc = tkef_aggregate_execute(p, idx, val, nnz, ws, ws_bytes, status, stream);
   tkef_update_plan_destroy(p);
   return rc;
 }

@@ -63,6 +63,9 @@ constexpr int kUBlock = 256;
 constexpr int kUShift = 12;
 constexpr int kUTile = 1 << kUShift;  // 4096 positions, 16 KB of LDS
 
+// what the update kernel does with the tile sums G
+enum { kOpSgd = 0, kOpSparseSgd = 1, kOpAggregate = 2 };
+
 struct UpdTensor {       // 32 B, one per parameter tensor, written at bind
   float* w;
   float* b;              // momentum buffer or null
@@ -94,7 +97,7 @@ hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
                          int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
                          const uint32_t* rcand, const uint32_t* rband, const uint32_t* rsuf,
-                         const uint32_t* rcnt, int32_t* idx_out, float* val_out,
+                         const uint32_t* rcnt, int32_t* idx_out, void* val_out, int val16,
                          uint32_t* clear_next, int64_t clear_words, hipStream_t s, const Ev& ev);
 // several selection groups
 hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
@@ -110,8 +113,8 @@ hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32
 hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
                        const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
                        int32_t grid, const int32_t* cand, const uint32_t* meta,
-                       const uint32_t* base, uint64_t* flags, int32_t* idx_out, float* val_out,
-                       uint32_t* status, uint32_t* clear_next, int64_t clear_words,
+                       const uint32_t* base, uint64_t* flags, int32_t* idx_out, void* val_out,
+                       int val16, uint32_t* status, uint32_t* clear_next, int64_t clear_words,
                        hipStream_t s, const Ev& ev);
 // launch-shape limits of the selection kernels
 int32_t select_max_groups();
@@ -122,9 +125,9 @@ hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, in
                       int32_t d, int32_t ntiles_u, int32_t* seg, uint32_t* status,
                       hipStream_t s, const Ev& ev);
 hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32_t ntens,
-                         int32_t d, int32_t ntiles_u, const int32_t* idx, const float* val,
-                         int64_t stride, const int32_t* nnz, int32_t P, const int32_t* seg,
-                         float lr, float mu, float wd, int sparse_mode, int has_mom,
+                         int32_t d, int32_t ntiles_u, const int32_t* idx, const void* val,
+                         int val16, int64_t stride, const int32_t* nnz, int32_t P,
+                         const int32_t* seg, float lr, float mu, float wd, int op, int has_mom,
                          hipStream_t s, const Ev& ev);
 
 }  // namespace tkef

@@ -22,6 +22,7 @@
 //   update   per tile: LDS accumulation of all workers' entries of the tile,
 //            then one pass applying the SGD step to that parameter range
 #include <hip/hip_ext.h>
+#include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
 #include "tkef.h"
@@ -188,6 +189,17 @@ __device__ __forceinline__ float pick_elem(const float (&v)[kLine], int j) {
 #pragma unroll
   for (int i = 0; i < 2; ++i) d[i] = sel_bits(m3, c[2 * i], c[2 * i + 1]);
   return __uint_as_float(sel_bits(m4, d[0], d[1]));
+}
+
+// Values on the wire: binary32, or binary16 rounded to nearest even (Sec. 5.3
+// sends FP16 elements). val16 selects the format of the value array.
+__device__ __forceinline__ void put_val(void* out, size_t pos, float x, int val16) {
+  if (val16) reinterpret_cast<uint16_t*>(out)[pos] = __half_as_ushort(__float2half_rn(x));
+  else reinterpret_cast<float*>(out)[pos] = x;
+}
+__device__ __forceinline__ float get_val(const void* in, size_t pos, int val16) {
+  return val16 ? __half2float(__ushort_as_half(reinterpret_cast<const uint16_t*>(in)[pos]))
+               : reinterpret_cast<const float*>(in)[pos];
 }
 
 }  // namespace
@@ -899,7 +911,7 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
     const uint32_t* __restrict__ rbin, const uint4* __restrict__ rcand,
     const uint32_t* __restrict__ rband,
     const uint32_t* __restrict__ rsuf, const uint2* __restrict__ rcnt,
-    int32_t* __restrict__ idx_out, float* __restrict__ val_out,
+    int32_t* __restrict__ idx_out, void* __restrict__ val_out, int val16,
     uint32_t* __restrict__ clear_next, int64_t clear_words) {
   __shared__ uint32_t h[kH3Bins];
   __shared__ uint32_t wsum[4 * kSWaves];
@@ -1111,7 +1123,7 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
     }
     if (pos < k) {
       idx_out[pos] = (int32_t)gidx;
-      val_out[pos] = x;
+      put_val(val_out, pos, x, val16);
       *gptr(rp) = 0.0f;
     }
   };
@@ -1271,7 +1283,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
                                                   const uint32_t* __restrict__ base,
                                                   uint64_t* __restrict__ flags,
                                                   int32_t* __restrict__ idx_out,
-                                                  float* __restrict__ val_out,
+                                                  void* __restrict__ val_out, int val16,
                                                   uint32_t* __restrict__ status,
                                                   uint32_t* __restrict__ clear_next,
                                                   int64_t clear_words) {
@@ -1342,7 +1354,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
     }
     if (pos < gd.k) {
       idx_out[gd.out_base + pos] = t.gstart + e;
-      val_out[gd.out_base + pos] = x;
+      put_val(val_out, (size_t)gd.out_base + pos, x, val16);
       gptr(t.r)[e] = 0.0f;
     }
   };
@@ -1409,7 +1421,10 @@ __global__ void k_seg(const int32_t* __restrict__ idx, int64_t stride,
 }
 
 // ---------------------------------------------------------------------------
-// update: one workgroup per update tile.
+// update: one workgroup per update tile. op: kOpSgd (every position: weight
+// decay and optional momentum), kOpSparseSgd (mu = wd = 0: only the positions
+// some list names), kOpAggregate (no step: the tile's sums G are written into
+// the bound tensors, every position, zero where no list names it).
 __device__ __forceinline__ float sgd_step(float G, float w, float& b, bool mom, float lr,
                                           float mu, float wd) {
   const float decay = wd * w;
@@ -1430,9 +1445,11 @@ constexpr int kUVecPerThread = kUTile / 4 / kUBlock;  // float4 per thread per t
 __global__ __launch_bounds__(kUBlock) void k_update(
     const UpdTensor* __restrict__ tens, const int32_t* __restrict__ tile_first, int32_t ntens,
     int32_t d, int32_t ntiles_u, int32_t per_xcd, const int32_t* __restrict__ idx,
-    const float* __restrict__ val, int64_t stride, const int32_t* __restrict__ nnz, int32_t P,
-    const int32_t* __restrict__ seg, float lr, float mu, float wd, int sparse_mode,
+    const void* __restrict__ val, int val16, int64_t stride, const int32_t* __restrict__ nnz,
+    int32_t P, const int32_t* __restrict__ seg, float lr, float mu, float wd, int op,
     int has_mom) {
+  const bool sparse_mode = op == kOpSparseSgd;
+  const bool densify = op == kOpAggregate;
   __shared__ __align__(16) float acc[kUTile];
   __shared__ uint32_t mask[kUTile / 32];
   __shared__ int32_t sbeg[kUBlock];
@@ -1459,7 +1476,7 @@ __global__ __launch_bounds__(kUBlock) void k_update(
                     ((reinterpret_cast<uintptr_t>(w_tile) |
                       (mom ? reinterpret_cast<uintptr_t>(b_tile) : 0u)) & 15u) == 0;
   float4 wv[kUVecPerThread], bv[kUVecPerThread];
-  if (fast) {
+  if (fast && !densify) {  // (aggregation only writes the tile)
     const float4* w4 = reinterpret_cast<const float4*>(w_tile);
     const float4* b4 = reinterpret_cast<const float4*>(b_tile);
 #pragma unroll
@@ -1514,7 +1531,7 @@ __global__ __launch_bounds__(kUBlock) void k_update(
           const uint32_t before = lo ? scan[lo - 1] : 0u;
           const int64_t gi = (int64_t)(p0 + lo) * stride + sbeg[lo] + (q - before);
           li[j] = idx[gi] - base;
-          vv[j] = val[gi];
+          vv[j] = get_val(val, (size_t)gi, val16);
         }
       }
 #pragma unroll
@@ -1537,6 +1554,10 @@ __global__ __launch_bounds__(kUBlock) void k_update(
     for (int q = 0; q < kUVecPerThread; ++q) {
       const int v = q * kUBlock + tid;
       const float4 G = a4[v];
+      if (densify) {
+        store_nt4(w4 + v, G);
+        continue;
+      }
       float4 w = wv[q], bb = mom ? bv[q] : make_float4(0.f, 0.f, 0.f, 0.f);
       w.x = sgd_step(G.x, w.x, bb.x, mom, lr, mu, wd);
       w.y = sgd_step(G.y, w.y, bb.y, mom, lr, mu, wd);
@@ -1586,6 +1607,11 @@ __global__ __launch_bounds__(kUBlock) void k_update(
       gv4f* w4 = (gv4f*)w;
       gv4f* b4 = (gv4f*)bm;
       for (int q = tid; q < nv; q += kUBlock) {
+        if (densify) {
+          const int l = la + 4 * q;
+          w4[q] = v4f{acc[l], acc[l + 1], acc[l + 2], acc[l + 3]};
+          continue;
+        }
         const v4f wv4 = w4[q];
         const v4f bv4 = bm ? b4[q] : v4f{0.f, 0.f, 0.f, 0.f};
         float wq[4] = {wv4.x, wv4.y, wv4.z, wv4.w}, bq[4] = {bv4.x, bv4.y, bv4.z, bv4.w};
@@ -1598,6 +1624,10 @@ __global__ __launch_bounds__(kUBlock) void k_update(
       done = nv << 2;
     }
     for (int q = done + tid; q < cnt; q += kUBlock) {
+      if (densify) {
+        w[q] = acc[la + q];
+        continue;
+      }
       float bq = mom ? bm[q] : 0.0f;
       w[q] = sgd_step(acc[la + q], w[q], bq, mom, lr, mu, wd);
       if (mom) bm[q] = bq;
@@ -1657,12 +1687,12 @@ hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
                          int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
                          const uint32_t* rcand, const uint32_t* rband, const uint32_t* rsuf,
-                         const uint32_t* rcnt, int32_t* idx_out, float* val_out,
+                         const uint32_t* rcnt, int32_t* idx_out, void* val_out, int val16,
                          uint32_t* clear_next, int64_t clear_words, hipStream_t s,
                          const Ev& ev) {
   return launch(k_finish, dim3(grid), dim3(kSBlock), s, ev, tiles, groups, st, summ, nlines, lpt,
                 rcap, hist2, rbin, reinterpret_cast<const uint4*>(rcand), rband, rsuf,
-                reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, clear_next,
+                reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, val16, clear_next,
                 clear_words);
 }
 
@@ -1690,11 +1720,12 @@ hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32
 hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
                        const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
                        int32_t grid, const int32_t* cand, const uint32_t* meta,
-                       const uint32_t* base, uint64_t* flags, int32_t* idx_out, float* val_out,
-                       uint32_t* status, uint32_t* clear_next, int64_t clear_words,
+                       const uint32_t* base, uint64_t* flags, int32_t* idx_out, void* val_out,
+                       int val16, uint32_t* status, uint32_t* clear_next, int64_t clear_words,
                        hipStream_t s, const Ev& ev) {
   return launch(k_emit, dim3(grid), dim3(kSBlock), s, ev, tiles, ntiles, groups, st, summ, nlines,
-                lpt, cand, meta, base, flags, idx_out, val_out, status, clear_next, clear_words);
+                lpt, cand, meta, base, flags, idx_out, val_out, val16, status, clear_next,
+                clear_words);
 }
 
 int32_t select_max_groups() { return kSMaxGroups; }
@@ -1711,13 +1742,13 @@ hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, in
 }
 
 hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32_t ntens,
-                         int32_t d, int32_t ntiles_u, const int32_t* idx, const float* val,
-                         int64_t stride, const int32_t* nnz, int32_t P, const int32_t* seg,
-                         float lr, float mu, float wd, int sparse_mode, int has_mom,
+                         int32_t d, int32_t ntiles_u, const int32_t* idx, const void* val,
+                         int val16, int64_t stride, const int32_t* nnz, int32_t P,
+                         const int32_t* seg, float lr, float mu, float wd, int op, int has_mom,
                          hipStream_t s, const Ev& ev) {
   const int32_t per_xcd = (ntiles_u + kXcds - 1) / kXcds;
   return launch(k_update, dim3(per_xcd * kXcds), dim3(kUBlock), s, ev, tens, tile_first, ntens, d,
-                ntiles_u, per_xcd, idx, val, stride, nnz, P, seg, lr, mu, wd, sparse_mode,
+                ntiles_u, per_xcd, idx, val, val16, stride, nnz, P, seg, lr, mu, wd, op,
                 has_mom);
 }
 

@@ -413,4 +413,79 @@ def pin_update_worker_permutation(orc):
     assert np.all(np.abs(b1.astype(np.float64) - b2) <= 1e-6 * (np.abs(b1) + S / 0.1))
 
 
+def pin_aggregate_dyadic_exact(orc):
+    # dyadic values with a small exponent range: every binary32 partial sum is
+    # exact, so the dense sum equals the rational sum of each position
+    rng = _rng(25)
+    d, P, k = 3000, 11, 400
+    idx, val = _dyadic_lists(rng, d, P, k)
+    nnz = rng.integers(0, k + 1, P)
+    nnz[0] = k
+    out = orc.aggregate(d, idx, val, nnz)
+    G = [Fraction(0)] * d
+    for p in range(P):
+        for j in range(int(nnz[p])):
+            G[idx[p, j]] += Fraction(float(val[p, j]))
+    exp = np.array([float(v) for v in G], np.float32)
+    assert np.array_equal(bits(out), bits(np.where(exp == 0, np.float32(0), exp)))
+
+
+def pin_aggregate_worker_order_and_zero(orc):
+    # g~ starts at +0 and the lists are added one worker after the other:
+    # 1 + 2^-24 rounds to 1 (tie to even), so two such terms after a 1 vanish,
+    # while the same terms first would give 1 + 2^-23
+    t = np.float32(2.0 ** -24)
+    idx = np.array([[0, 3], [0, 3], [0, 3]], np.int32)
+    val = np.array([[1.0, t], [t, t], [t, 1.0]], np.float32)
+    out = orc.aggregate(6, idx, val)
+    assert out[0] == np.float32(1.0)
+    assert out[3] == np.float32(1.0 + 2.0 ** -23)
+    # untouched positions are +0; a lone -0 added to +0 gives +0; P = 0 gives zeros
+    assert np.array_equal(bits(out[[1, 2, 4, 5]]), np.zeros(4, np.uint32))
+    out = orc.aggregate(4, np.array([[2]], np.int32), np.array([[-0.0]], np.float32))
+    assert np.array_equal(bits(out), np.zeros(4, np.uint32))
+    out = orc.aggregate(5, np.zeros((0, 3), np.int32), np.zeros((0, 3), np.float32),
+                        np.zeros(0, np.int64))
+    assert np.array_equal(bits(out), np.zeros(5, np.uint32))
+
+
+def pin_aggregate_float64_bound(orc):
+    # worker-ordered binary32 sum of c terms: within (c - 1) u sum|v| of the
+    # exact sum (standard recursive-summation bound), duplicates included
+    rng = _rng(26)
+    d, P, k = 20_000, 16, 2500
+    idx = np.stack([np.sort(rng.choice(d, k, replace=False)) for _ in range(P)]).astype(np.int32)
+    idx[3, :40] = 17  # one list naming the same position many times
+    val = (rng.standard_normal((P, k)) * 1e-2).astype(np.float32)
+    out = orc.aggregate(d, idx, val)
+    G, A = np.zeros(d), np.zeros(d)
+    np.add.at(G, idx.ravel(), val.ravel().astype(np.float64))
+    np.add.at(A, idx.ravel(), np.abs(val.ravel().astype(np.float64)))
+    cnt = np.bincount(idx.ravel(), minlength=d)
+    u = 2.0 ** -24
+    assert np.all(np.abs(out.astype(np.float64) - G) <= np.maximum(cnt - 1, 0) * u * A * 1.0001 + 1e-45)
+    assert np.array_equal(bits(out[cnt == 0]), np.zeros(int((cnt == 0).sum()), np.uint32))
+    # a position named once carries its value bit for bit
+    one = cnt == 1
+    assert np.array_equal(bits(out[one]), bits(G[one].astype(np.float32)))
+
+
+def pin_f16_known_conversions(orc):
+    # IEEE binary16 facts: largest finite 65504; 65520 is the midpoint to the
+    # next (absent) step and rounds to infinity; 2^-24 is the least subnormal,
+    # 2^-25 ties to 0 (even), 3*2^-25 ties up to 2^-23; 1/3 -> 0x3555;
+    # 1 + 2^-11 ties to 1, 1 + 3*2^-11 ties up to 1 + 2^-9
+    from oracle import f16_rne
+    cases = [(65504.0, 0x7BFF), (65519.0, 0x7BFF), (65520.0, 0x7C00), (-1e9, 0xFC00),
+             (2.0 ** -24, 0x0001), (2.0 ** -25, 0x0000), (3 * 2.0 ** -25, 0x0002),
+             (-(2.0 ** -14), 0x8400), (np.float32(1 / 3), 0x3555), (1.0 + 2.0 ** -11, 0x3C00),
+             (1.0 + 3 * 2.0 ** -11, 0x3C02), (-0.0, 0x8000), (np.inf, 0x7C00)]
+    got = f16_rne(np.array([c[0] for c in cases], np.float32)).view(np.uint16)
+    assert [int(v) for v in got] == [c[1] for c in cases], [hex(v) for v in got]
+    assert np.isnan(f16_rne(np.array([np.nan], np.float32))[0])
+    # round-trip: every finite binary16 value is a binary32 value and maps to itself
+    h = np.arange(0, 0x7C00, dtype=np.uint16).view(np.float16)
+    assert np.array_equal(f16_rne(h.astype(np.float32)).view(np.uint16), h.view(np.uint16))
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

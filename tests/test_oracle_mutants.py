@@ -42,6 +42,14 @@ MUTANTS = {
     "dense_lr_twice": ("float step = lr * U;", "float step = lr * lr * U;"),
     "plain_lr_dropped": ("float step = lr * G[i];", "float step = G[i];"),
     "nesterov": ("U = b[i];", "U = D + mu * b[i];"),
+    "aggregate_overwrites": ("out[iq[j]] += vq[j];", "out[iq[j]] = vq[j];"),
+    "aggregate_mean": ("out[iq[j]] += vq[j];", "out[iq[j]] += vq[j] / (float)P;"),
+    "aggregate_not_zeroed": ("for (int64_t i = 0; i < d; ++i) out[i] = 0.0f;", "(void)0;"),
+    "aggregate_first_worker_dropped": ("for (int32_t q = 0; q < P; ++q) {\n        const int32_t *iq",
+                                       "for (int32_t q = 1; q < P; ++q) {\n        const int32_t *iq"),
+    "aggregate_reverse_workers": ("for (int32_t q = 0; q < P; ++q) {\n        const int32_t *iq",
+                                  "for (int32_t q = P - 1; q >= 0; --q) {\n        const int32_t *iq"),
+    "aggregate_nnz_ignored": ("for (int64_t j = 0; j < nnz[q]; ++j) out", "for (int64_t j = 0; j < stride; ++j) out"),
 }
 
 
