@@ -46,6 +46,9 @@ def parse_args():
     ap.add_argument("--replicas", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip timing the CPU oracle")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the variant paths timed after the step (fp16 values, dense "
+                         "aggregation, shard-shaped sparsify)")
     ap.add_argument("--kernel-events", type=int, default=1,
                     help="record HIP events around every kernel (1) or only per phase (0)")
     ap.add_argument("--probe-copy", type=int, default=0, metavar="MIB",
@@ -127,6 +130,89 @@ def cpu_baseline(sizes, d):
             "sparsify_s": round(t_sp, 3), "update_s": round(t_up, 3),
             "update_GBps": round(upd_bytes / t_up / 1e9, 3),
             "host_cpus": os.cpu_count()}
+
+
+def time_calls(plan_of, call, n_calls, warmup, make_events):
+    """Mean whole-call and per-kernel times (ms) of call(plan_of(i)) over
+    n_calls, from events recorded by the plans' own dispatches. plan_of
+    rotates over plans with separate buffers, as the step does."""
+    import numpy as np
+    import torch
+    names = plan_of(0).launch_names()
+    for i in range(warmup):
+        call(plan_of(i))
+    evs = [make_events(len(names) + 1) for _ in range(n_calls)]
+    torch.cuda.synchronize()
+    for t in range(n_calls):
+        pl = plan_of(warmup + t)
+        pl.set_events(evs[t])
+        call(pl)
+        pl.set_events(None)
+    torch.cuda.synchronize()
+    total = float(np.mean([e[0].elapsed_time(e[-1]) for e in evs]))
+    kern = {n: round(float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs])) * 1e3, 2)
+            for i, n in enumerate(names)}
+    return total, kern
+
+
+def extras(args, tk, gen, sizes, d, bank, resid, idx_all, val_all, nnz, k_total, make_events):
+    """Variant paths on the same resident inputs, each timed like the step
+    (rotating buffers): binary16 values out of the sparsify, the dense
+    aggregation of the P = 128 lists, and the per-GPU shard of the
+    hierarchical scheme (8 contiguous shards of a flat 25.6 M gradient,
+    k~ = ceil(rho d / 8))."""
+    import torch
+    dev = bank[0][0].device
+    K, W, R = args.steps, args.warmup, len(resid)
+    ex = {}
+
+    log("extras: sparsify with binary16 values")
+    p16 = [[tk.SparsifyPlan(sizes, rho=RHO, val_dtype=torch.float16).bind(bank[s], resid[j])
+            for j in range(R)] for s in range(len(bank))]
+    i16 = torch.empty(k_total, dtype=torch.int32, device=dev)
+    v16 = torch.empty(k_total, dtype=torch.float16, device=dev)
+    ms, kern = time_calls(lambda i: p16[i % len(bank)][i % R], lambda pl: pl.execute(i16, v16),
+                          K, W, make_events)
+    ex["sparsify_fp16_us"] = round(ms * 1e3, 2)
+    ex["sparsify_fp16_kernels_us"] = kern
+    del p16
+
+    log("extras: dense aggregation of the P = 128 lists")
+    outs = [[torch.empty(n, device=dev) for n in sizes] for _ in range(R)]
+    aplans = [tk.UpdatePlan(sizes, P=P_WORKERS, stride=K_LIST).bind(outs[j]) for j in range(R)]
+    ms, kern = time_calls(lambda i: aplans[i % R],
+                          lambda pl: pl.aggregate(idx_all[aplans.index(pl)],
+                                                  val_all[aplans.index(pl)], nnz=nnz),
+                          K, W, make_events)
+    pairs = k_total + (P_WORKERS - 1) * K_LIST
+    ex["aggregate_us"] = round(ms * 1e3, 2)
+    ex["aggregate_GBps"] = round((4 * d + 8 * pairs) / (ms / 1e3) / 1e9, 1)
+    ex["aggregate_kernels_us"] = kern
+    del outs, aplans
+
+    log("extras: shard-shaped sparsify (1 of 8 shards)")
+    n_sh = 8
+    shard = -(-d // n_sh)
+    k_sh = -(-d // (n_sh * 1000))          # ceil(rho d / 8) with rho = 1/1000
+    flats = [torch.from_numpy(gen.flat_normal(d, config=2, step=s, std=1e-2)).to(dev)
+             for s in range(2)]
+    rflat = [torch.zeros(d, device=dev) for _ in range(2)]
+    # the 7 full shards of two gradients: 14 plans, 360 MB of g and r, rotated
+    # so that no call finds its inputs in the last-level cache
+    splans = [tk.SparsifyPlan([shard], k=k_sh).bind([flats[s][q * shard:(q + 1) * shard]],
+                                                     [rflat[s][q * shard:(q + 1) * shard]])
+              for s in range(2) for q in range(n_sh - 1)]
+    si = torch.empty(k_sh, dtype=torch.int32, device=dev)
+    sv = torch.empty(k_sh, dtype=torch.float32, device=dev)
+    ms, kern = time_calls(lambda i: splans[i % len(splans)], lambda pl: pl.execute(si, sv),
+                          max(K, 2 * len(splans)), len(splans), make_events)
+    ex["shard"] = {"d": shard, "k": k_sh, "shards_rotated": len(splans),
+                   "sparsify_us": round(ms * 1e3, 2),
+                   "Gelem_per_s": round(shard / (ms / 1e3) / 1e9, 2),
+                   "frac_hbm_peak": round((12 * shard + 8 * k_sh) / (ms / 1e3) / 1e9
+                                          / HBM_PEAK_GBPS, 4),
+                   "kernels_us": kern}
+    return ex
 
 
 def main() -> int:
@@ -277,6 +363,9 @@ def main() -> int:
         "roofline": roofline,
         "cpu_baseline": None,
     }
+    if not args.no_extras:
+        out["extras"] = extras(args, tk, gen, sizes, d, bank, resid, idx_all, val_all, nnz,
+                               k_total, make_events)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on one step (bounded sample)")
         out["cpu_baseline"] = cpu_baseline(sizes, d)
