@@ -7,7 +7,8 @@ package. It shares no code with the GPU library and never imports it.
 
 The C part is built with gcc into ``oracle/liboracle.so`` (``build()``); the
 list handling around it (concatenating a tensor list, per-tensor groups) is
-plain numpy.
+plain numpy. The approximate selector of Alg. 1 (MSTopK) is plain numpy in
+float64, in ``oracle/mstopk.py``.
 """
 from __future__ import annotations
 
