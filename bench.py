@@ -177,6 +177,34 @@ def extras(args, tk, gen, sizes, d, bank, resid, idx_all, val_all, nnz, k_total,
     ex["sparsify_fp16_kernels_us"] = kern
     del p16
 
+    log("extras: MSTopK (Alg. 1, N = 30) on the same workload")
+    pms = [[tk.SparsifyPlan(sizes, mode=tk.APPROX, rho=RHO, n_search=30).bind(bank[s], resid[j])
+            for j in range(R)] for s in range(len(bank))]
+    ims = torch.empty(k_total, dtype=torch.int32, device=dev)
+    vms = torch.empty(k_total, dtype=torch.float32, device=dev)
+    ms, kern = time_calls(lambda i: pms[i % len(bank)][i % R],
+                          lambda pl: pl.execute(ims, vms, window_word=0x9E3779B97F4A7C15),
+                          K, W, make_events)
+    # selection quality against the exact top-k of the same x (fresh residual)
+    x_ref = [t.clone() for t in bank[0]]
+    r0 = [torch.zeros_like(t) for t in bank[0]]
+    pe = tk.SparsifyPlan(sizes, rho=RHO).bind(x_ref, r0)
+    ie, _ = pe.execute()
+    r1 = [torch.zeros_like(t) for t in bank[0]]
+    pa = tk.SparsifyPlan(sizes, mode=tk.APPROX, rho=RHO, n_search=30).bind(x_ref, r1)
+    ia, _ = pa.execute(window_word=0x9E3779B97F4A7C15)
+    info = pa.approx_result()
+    xf = torch.cat(x_ref).abs().double()
+    overlap = torch.isin(ia.long(), ie.long()).sum().item() / k_total
+    mass = (xf[ia.long()].sum() / xf[ie.long()].sum()).item()
+    ex["mstopk"] = {"n_search": 30, "sparsify_us": round(ms * 1e3, 2),
+                    "Gelem_per_s": round(d / (ms / 1e3) / 1e9, 2),
+                    "kernels_us": kern,
+                    "overlap_with_exact": round(overlap, 5),
+                    "abs_mass_vs_exact": round(mass, 6),
+                    "k1": info["k1"], "band_taken": info["take"], "band": info["k2"] - info["k1"]}
+    del pms, pe, pa, x_ref, r0, r1
+
     log("extras: dense aggregation of the P = 128 lists")
     outs = [[torch.empty(n, device=dev) for n in sizes] for _ in range(R)]
     aplans = [tk.UpdatePlan(sizes, P=P_WORKERS, stride=K_LIST).bind(outs[j]) for j in range(R)]

@@ -53,12 +53,15 @@ extern "C" {
 /* selection modes */
 #define TKEF_GLOBAL 0     /* one selection over the concatenated tensor list */
 #define TKEF_PER_TENSOR 1 /* one selection per tensor, k_t from rho per tensor */
+#define TKEF_APPROX 2     /* one selection over the concatenated list with MSTopK (Alg. 1) */
 
 /* device status bits */
 #define TKEF_STATUS_NAN 1u         /* sparsify saw a NaN in g + r */
 #define TKEF_STATUS_UNSORTED 2u    /* an update index list is not ascending */
 #define TKEF_STATUS_INDEX_RANGE 4u /* an update index lies outside [0, d) */
 #define TKEF_STATUS_TIMEOUT 8u     /* a bounded wait between workgroups gave up (results invalid) */
+#define TKEF_STATUS_NONFINITE 16u  /* MSTopK saw an infinity or NaN in g + r (it then takes
+                                       the first k positions) */
 
 int tkef_version(void);
 const char *tkef_strerror(int code);
@@ -130,6 +133,39 @@ int tkef_sparsify_execute(tkef_sparsify_plan plan, void *ws, size_t ws_bytes,
  * binary32 x where not selected and +0 where selected: the rounding of the
  * sent value is not fed back. Host only; TKEF_EINVAL for another format. */
 int tkef_sparsify_plan_set_value_format(tkef_sparsify_plan plan, int32_t format);
+
+/* MSTopK parameters of a TKEF_APPROX plan (Alg. 1). n_search: rounds of the
+ * threshold bisection, 1..48 (the paper runs 30, which is the default; the
+ * kernel count, 2 + ceil(n_search / 6), is reported by *_info after this
+ * call). window_word: the 64-bit value the band offset is drawn from for the
+ * next executions: offset = window_word mod (band - (k - k1) + 1), so a
+ * caller wanting the paper's random offset passes a fresh random word per
+ * execution. Host only; TKEF_EINVAL for another mode or n_search outside
+ * 1..48.
+ *
+ * What a TKEF_APPROX execution computes (readings of Alg. 1): x = g + r as
+ * above; a = |x|; mean = (the exact sum of a, rounded once to double) / d in
+ * double; u = max a; round i of N takes ratio = l + (r - l) / 2 and
+ * thres = mean + ratio * (u - mean) in double and counts n = #{a >= thres}
+ * (a widened exactly); n <= k sets r = ratio and, if n > k1, (k1, thres1) =
+ * (n, thres); otherwise l = ratio and, if n < k2, (k2, thres2) = (n, thres);
+ * start l = 0, r = 1, k1 = 0, thres1 = +inf, k2 = d, thres2 = 0. The result
+ * is {a >= thres1} plus the band members {thres2 <= a < thres1} of rank
+ * offset .. offset + k - k1 - 1 in position order; idx ascending, val = x at
+ * idx, r = x with the selected positions set to +0. Exactly k pairs. */
+int tkef_sparsify_plan_set_approx(tkef_sparsify_plan plan, int32_t n_search,
+                                  uint64_t window_word);
+
+/* Host; synchronizes `stream`. Reads back the search result of the last
+ * TKEF_APPROX execution on the bound ws: out[0] = the mean, out[1] = u (as
+ * doubles); cnt[0] = k1, cnt[1] = k2 (the recorded counts), cnt[2] = the
+ * window offset, cnt[3] = k - k1 (taken from the band), cnt[4] = the key
+ * (binary32 bits with the sign cleared) of the smallest binary32 >= thres1
+ * (2^31 when thres1 was never set), cnt[5] = the same for thres2. Either
+ * array may be NULL. TKEF_EINVAL for another mode; TKEF_ESTATE if ws is not
+ * the bound workspace. */
+int tkef_sparsify_approx_result(tkef_sparsify_plan plan, void *ws, double *out,
+                                int64_t *cnt, hipStream_t stream);
 
 /* Optional timing hook: with n_events >= nlaunch + 1, each execution records
  * events[0] at the start of its first kernel and events[i + 1] at the end of

@@ -27,9 +27,12 @@ LIB_PATH = os.path.join(PKG, "lib", "libtkef.so")
 
 GLOBAL = 0
 PER_TENSOR = 1
+APPROX = 2          # MSTopK (Alg. 1) over the concatenated list
 STATUS_NAN = 1
 STATUS_UNSORTED = 2
 STATUS_INDEX_RANGE = 4
+STATUS_TIMEOUT = 8
+STATUS_NONFINITE = 16
 VAL_F32 = 0
 VAL_F16 = 1
 
@@ -62,6 +65,8 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
         "tkef_sparsify_plan_set_events": ([vp, P(vp), i32], ctypes.c_int),
         "tkef_sparsify_plan_launch_name": ([vp, i32], ctypes.c_char_p),
         "tkef_sparsify_plan_set_value_format": ([vp, i32], ctypes.c_int),
+        "tkef_sparsify_plan_set_approx": ([vp, i32, ctypes.c_uint64], ctypes.c_int),
+        "tkef_sparsify_approx_result": ([vp, vp, P(f64), P(i64), vp], ctypes.c_int),
         "tkef_sparsify_workspace": ([P(i64), i32, i32, f64, i64, P(sz), P(i64)], ctypes.c_int),
         "tkef_sparsify": ([P(vp), P(vp), P(i64), i32, i32, f64, i64, vp, vp, vp, sz, vp, vp],
                           ctypes.c_int),
@@ -155,7 +160,7 @@ class SparsifyPlan:
     """Plan for sparsifying a fixed list of tensor sizes (see tkef.h)."""
 
     def __init__(self, numels: Sequence[int], mode: int = GLOBAL, rho: Optional[float] = None,
-                 k: Optional[int] = None, val_dtype=torch.float32):
+                 k: Optional[int] = None, val_dtype=torch.float32, n_search: int = 30):
         self._numels = [int(n) for n in numels]
         self._h = ctypes.c_void_p()
         L = lib()
@@ -165,6 +170,10 @@ class SparsifyPlan:
         self.val_dtype = val_dtype
         _check("tkef_sparsify_plan_set_value_format",
                L.tkef_sparsify_plan_set_value_format(self._h, _val_format(val_dtype)))
+        self.mode, self.n_search = int(mode), int(n_search)
+        if self.mode == APPROX:
+            _check("tkef_sparsify_plan_set_approx",
+                   L.tkef_sparsify_plan_set_approx(self._h, self.n_search, 0))
         ws, kt, d, ng, nl = (ctypes.c_size_t(), ctypes.c_int64(), ctypes.c_int64(),
                              ctypes.c_int32(), ctypes.c_int32())
         _check("tkef_sparsify_plan_info", L.tkef_sparsify_plan_info(
@@ -217,10 +226,17 @@ class SparsifyPlan:
 
     def execute(self, idx_out: Optional[torch.Tensor] = None,
                 val_out: Optional[torch.Tensor] = None,
-                status: Optional[torch.Tensor] = None, stream=None
-                ) -> Tuple[torch.Tensor, torch.Tensor]:
+                status: Optional[torch.Tensor] = None, stream=None,
+                window_word: Optional[int] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+        """window_word (APPROX plans): the 64-bit value the band offset of
+        this and later executions is drawn from."""
         if self._bound is None or self.ws is None:
             raise RuntimeError("plan is not bound")
+        if window_word is not None:
+            if self.mode != APPROX:
+                raise ValueError("window_word applies to APPROX plans only")
+            _check("tkef_sparsify_plan_set_approx", lib().tkef_sparsify_plan_set_approx(
+                self._h, self.n_search, int(window_word) & ((1 << 64) - 1)))
         dev = self.ws.device
         if idx_out is None:
             idx_out = torch.empty(max(self.k_total, 1), dtype=torch.int32, device=dev)
@@ -235,6 +251,18 @@ class SparsifyPlan:
             val_out.data_ptr(), status.data_ptr() if status is not None else None,
             _stream_handle(stream)))
         return idx_out[: self.k_total], val_out[: self.k_total]
+
+
+    def approx_result(self, stream=None) -> dict:
+        """Search result of the last APPROX execution (synchronizes the
+        stream): mean, u, k1, k2, offset, take, key1, key2."""
+        out = (ctypes.c_double * 2)()
+        cnt = (ctypes.c_int64 * 6)()
+        _check("tkef_sparsify_approx_result", lib().tkef_sparsify_approx_result(
+            self._h, self.ws.data_ptr() if self.ws is not None else None, out, cnt,
+            _stream_handle(stream)))
+        return {"mean": out[0], "u": out[1], "k1": cnt[0], "k2": cnt[1], "offset": cnt[2],
+                "take": cnt[3], "key1": cnt[4], "key2": cnt[5]}
 
 
 class UpdatePlan:

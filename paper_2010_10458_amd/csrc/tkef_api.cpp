@@ -102,9 +102,16 @@ static const char* const kSparsifyLaunchesMany[] = {"stream", "pick1", "gather",
                                                     "pick2",  "hist3", "pick3",
                                                     "groupscan", "emit"};
 constexpr int32_t kSparsifyNLaunchOne = 3, kSparsifyNLaunchMany = 8;
+// MSTopK: stream, count, refine x (passes - 1), emit
+static const char* const kApproxRefine[] = {"ms_refine1", "ms_refine2", "ms_refine3",
+                                            "ms_refine4", "ms_refine5", "ms_refine6",
+                                            "ms_refine7"};
+constexpr int32_t kMsMaxPasses = (kMsMaxRounds + kMsRoundsPerPass - 1) / kMsRoundsPerPass;
+static_assert(kMsMaxPasses - 1 <= 7, "refine names");
 
 struct tkef_sparsify_plan_s {
   int32_t ntensors = 0, mode = 0, ngroups = 0, ntiles = 0, nslots = 1, stream_grid = 1;
+  int32_t count_grid = 1;  // MSTopK first counting pass: eight workgroups per compute unit
   int64_t d = 0, k_total = 0, nlines = 0;
   std::vector<int64_t> numels, goff, kgroup;
   std::vector<TileDesc> tiles;   // pointers filled at bind
@@ -121,9 +128,18 @@ struct tkef_sparsify_plan_s {
          off_meta = 0, off_summ = 0, off_base = 0, off_cand = 0, off_rcand = 0, off_rband = 0,
          off_rsuf = 0, off_rcnt = 0, off_rbin = 0, ws_bytes = 0;
   int32_t val_format = TKEF_VAL_F32;  // value array written by execute
+  // MSTopK (TKEF_APPROX): rounds, offset word, scratch
+  int32_t ms_rounds = 30;
+  uint64_t ms_word = 0;
+  size_t off_ms_state = 0, off_ms_esum = 0, off_ms_emax = 0, off_ms_cnt = 0,
+         off_ms_flags = 0;  // state: kMsMaxPasses + 1 records, zeroed scratch: the rest
   uint64_t executions = 0;   // since the last bind
   bool needs_clear = true;   // both copies must be cleared before the next run
-  int32_t nlaunch() const { return ngroups == 1 ? kSparsifyNLaunchOne : kSparsifyNLaunchMany; }
+  int32_t ms_passes() const { return (ms_rounds + kMsRoundsPerPass - 1) / kMsRoundsPerPass; }
+  int32_t nlaunch() const {
+    if (mode == TKEF_APPROX) return 2 + ms_passes();
+    return ngroups == 1 ? kSparsifyNLaunchOne : kSparsifyNLaunchMany;
+  }
   void* bound_ws = nullptr;
   hipEvent_t* events = nullptr;
   int32_t n_events = 0;
@@ -136,10 +152,10 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
   int64_t d = 0;
   int rc = check_numels(numels, ntensors, &d);
   if (rc) return rc;
-  if (mode != TKEF_GLOBAL && mode != TKEF_PER_TENSOR) return TKEF_EINVAL;
+  if (mode != TKEF_GLOBAL && mode != TKEF_PER_TENSOR && mode != TKEF_APPROX) return TKEF_EINVAL;
   if (k < 0) return TKEF_ERANGE;
   if (k > 0) {
-    if (mode != TKEF_GLOBAL) return TKEF_EINVAL;
+    if (mode == TKEF_PER_TENSOR) return TKEF_EINVAL;
     if (k > d) return TKEF_ERANGE;
   } else if (!(rho > 0.0 && rho <= 1.0) || !std::isfinite(rho)) {
     return TKEF_ERANGE;
@@ -157,9 +173,9 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
       p->goff[t] = off;
       off += numels[t];
     }
-    p->ngroups = (mode == TKEF_GLOBAL) ? 1 : ntensors;
+    p->ngroups = (mode == TKEF_PER_TENSOR) ? ntensors : 1;
     p->kgroup.assign(p->ngroups, 0);
-    if (mode == TKEF_GLOBAL) {
+    if (mode != TKEF_PER_TENSOR) {
       p->kgroup[0] = (k > 0) ? k : tkef_k_from_rho(d, rho);
     } else {
       for (int32_t t = 0; t < ntensors; ++t) p->kgroup[t] = tkef_k_from_rho(numels[t], rho);
@@ -171,7 +187,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     p->groups.assign(p->ngroups, GroupDesc{0, 0, 0, 0});
     int64_t out = 0;
     for (int32_t t = 0; t < ntensors; ++t) {
-      const int32_t grp = (mode == TKEF_GLOBAL) ? 0 : t;
+      const int32_t grp = (mode == TKEF_PER_TENSOR) ? t : 0;
       if (mode == TKEF_PER_TENSOR || t == 0) {
         p->groups[grp].k = static_cast<uint32_t>(p->kgroup[grp]);
         p->groups[grp].tile_begin = static_cast<uint32_t>(p->tiles.size());
@@ -204,6 +220,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     p->sel_lpt = (int32_t)lpt;
     const int64_t g_lines = (p->nlines + sb * lpt - 1) / (sb * lpt);
     const bool one = p->ngroups == 1;
+    const bool approx = mode == TKEF_APPROX;
     // Candidates are the positions at or above the level-1 threshold bin:
     // about k plus one bin's worth. One group: each region (the lines of one
     // workgroup) stores up to rcap of them, several times the even share of
@@ -229,8 +246,16 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     p->off_groups = o;  o = align_up(o + p->groups.size() * sizeof(GroupDesc));
     p->off_state = o;   o = align_up(o + p->groups.size() * sizeof(GroupState));
     size_t z = 0;
-    p->off_hist1 = z;   z = align_up(z + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
-    p->off_hist2 = z;   z = align_up(z + (size_t)p->ngroups * kH2Bins * 4);
+    if (approx) {
+      p->off_ms_state = o;  o = align_up(o + (size_t)(kMsMaxPasses + 1) * sizeof(MsState));
+      p->off_ms_esum = z;   z = align_up(z + (size_t)kMsSlots * 256 * 8);
+      p->off_ms_emax = z;   z = align_up(z + (size_t)kMsSlots * 4);
+      p->off_ms_cnt = z;    z = align_up(z + (size_t)kMsMaxPasses * kMsSlots * 64 * 4);
+      p->off_ms_flags = z;  z = align_up(z + (size_t)p->sel_grid * 8);
+    } else {
+      p->off_hist1 = z;   z = align_up(z + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
+      p->off_hist2 = z;   z = align_up(z + (size_t)p->ngroups * kH2Bins * 4);
+    }
     if (!one) {
       p->off_hist3 = z;   z = align_up(z + (size_t)p->ngroups * kH3Bins * 4);
       p->off_flags1 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
@@ -241,7 +266,9 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     p->off_zero[0] = o; o = align_up(o + z);
     p->off_zero[1] = o; o = align_up(o + z);
     p->off_summ = o;    o = align_up(o + (size_t)p->nlines * sizeof(uint16_t));
-    if (one) {
+    if (approx) {
+      // no candidate tables: the passes read the lines again
+    } else if (one) {
       const size_t slots = (size_t)p->sel_grid * p->rcap;
       p->off_rcand = o;  o = align_up(o + slots * 16);
       p->off_rband = o;  o = align_up(o + slots * 4);
@@ -310,6 +337,7 @@ extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* con
     return TKEF_EHIP;
   const int64_t units = (int64_t)plan->ntiles * (kTile / kStreamUnit);
   plan->stream_grid = (int32_t)std::min<int64_t>((int64_t)4 * cus, units);
+  plan->count_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>((int64_t)8 * cus, (units + 1) / 2));
   char* base = static_cast<char*>(ws);
   hipError_t e = hipMemcpyAsync(base + plan->off_tiles, plan->tiles.data(),
                                 plan->tiles.size() * sizeof(TileDesc), hipMemcpyHostToDevice,
@@ -348,12 +376,53 @@ extern "C" int tkef_sparsify_plan_set_events(tkef_sparsify_plan plan, hipEvent_t
 
 extern "C" const char* tkef_sparsify_plan_launch_name(tkef_sparsify_plan plan, int32_t i) {
   if (!plan || i < 0 || i >= plan->nlaunch()) return nullptr;
+  if (plan->mode == TKEF_APPROX) {
+    if (i == 0) return "ms_stream";
+    if (i == 1) return "ms_count";
+    if (i == plan->nlaunch() - 1) return "ms_emit";
+    return kApproxRefine[i - 2];
+  }
   return plan->ngroups == 1 ? kSparsifyLaunchesOne[i] : kSparsifyLaunchesMany[i];
+}
+
+extern "C" int tkef_sparsify_plan_set_approx(tkef_sparsify_plan plan, int32_t n_search,
+                                             uint64_t window_word) {
+  if (!plan || plan->mode != TKEF_APPROX || n_search < 1 || n_search > kMsMaxRounds)
+    return TKEF_EINVAL;
+  plan->ms_rounds = n_search;
+  plan->ms_word = window_word;
+  return TKEF_OK;
 }
 
 extern "C" int tkef_sparsify_plan_set_value_format(tkef_sparsify_plan plan, int32_t format) {
   if (!plan || (format != TKEF_VAL_F32 && format != TKEF_VAL_F16)) return TKEF_EINVAL;
   plan->val_format = format;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_sparsify_approx_result(tkef_sparsify_plan plan, void* ws, double* out,
+                                           int64_t* cnt, hipStream_t s) {
+  if (!plan || plan->mode != TKEF_APPROX) return TKEF_EINVAL;
+  if (!ws || plan->bound_ws != ws) return TKEF_ESTATE;
+  MsState h;
+  const char* base = static_cast<const char*>(ws);
+  const size_t fin = plan->off_ms_state + (size_t)plan->ms_passes() * sizeof(MsState);
+  if (hipMemcpyAsync(&h, base + fin, sizeof(MsState), hipMemcpyDeviceToHost, s) !=
+          hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return TKEF_EHIP;
+  if (out) {
+    out[0] = h.abar;
+    out[1] = h.u;
+  }
+  if (cnt) {
+    cnt[0] = h.k1;
+    cnt[1] = h.k2;
+    cnt[2] = h.rand;
+    cnt[3] = h.take;
+    cnt[4] = h.K1;
+    cnt[5] = h.K2;
+  }
   return TKEF_OK;
 }
 
@@ -390,6 +459,39 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
                         s);
     if (e != hipSuccess) return TKEF_EHIP;
     plan->needs_clear = false;
+  }
+  if (plan->mode == TKEF_APPROX) {
+    MsState* ms = reinterpret_cast<MsState*>(base + plan->off_ms_state);
+    uint64_t* esum = reinterpret_cast<uint64_t*>(zb + plan->off_ms_esum);
+    uint32_t* emax = reinterpret_cast<uint32_t*>(zb + plan->off_ms_emax);
+    uint32_t* cnt = reinterpret_cast<uint32_t*>(zb + plan->off_ms_cnt);
+    uint64_t* flags = reinterpret_cast<uint64_t*>(zb + plan->off_ms_flags);
+    const uint32_t k = static_cast<uint32_t>(plan->k_total);
+    const int32_t N = plan->ms_rounds, passes = plan->ms_passes();
+    auto rounds_of = [&](int32_t b) {
+      return std::min(kMsRoundsPerPass, N - b * kMsRoundsPerPass);
+    };
+    auto cnt_of = [&](int32_t b) { return cnt + (size_t)b * kMsSlots * 64; };
+    e = launch_ms_stream(tiles, nt, plan->stream_grid, kMsSlots, esum, emax, summ, s,
+                         tr.at(li++));
+    if (e == hipSuccess)
+      e = launch_ms_count(tiles, nt, plan->count_grid, kMsSlots, esum, emax, summ, cnt_of(0),
+                          ms, plan->d, status, s, tr.at(li++));
+    for (int32_t b = 1; b < passes && e == hipSuccess; ++b)
+      e = launch_ms_refine(tiles, summ, nl, lpt, sg, kMsSlots, cnt_of(b - 1), cnt_of(b),
+                           ms + b - 1, ms + b, k, plan->d, rounds_of(b - 1), N, plan->ms_word, s,
+                           tr.at(li++));
+    if (e == hipSuccess)
+      e = launch_ms_emit(tiles, summ, nl, lpt, sg, kMsSlots, cnt_of(passes - 1),
+                         ms + passes - 1, ms + passes, k, plan->d, rounds_of(passes - 1), N,
+                         plan->ms_word, flags, idx_out, val_out, val16, status, clear_next,
+                         clear_words, s, tr.at(li++));
+    if (e != hipSuccess) {
+      plan->needs_clear = true;
+      return TKEF_EHIP;
+    }
+    plan->executions++;
+    return TKEF_OK;
   }
   e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s,
                     tr.at(li++));

@@ -55,6 +55,21 @@ struct GroupState {      // per group, rewritten by every execution
   uint32_t n_eq;         // elements with key == T
 };
 
+// ---- approximate selection (MSTopK) ------------------------------------------
+// State of one MSTopK run between counting passes: the mean and maximum of
+// |x|, the bisection bracket [l, r] of the ratio, the recorded counts and
+// their threshold keys, and (after the last round) the window.
+struct MsState {
+  double abar, u, l, r;
+  uint32_t k1, k2;       // largest count <= k, smallest count > k (start 0, d)
+  uint32_t K1, K2;       // their threshold keys (start: none = 2^31, 0)
+  uint32_t rand, take;   // window offset in the band, elements taken from it
+  uint32_t level, bad;   // rounds done; non-finite input seen
+};
+constexpr int kMsRoundsPerPass = 6;   // 63 thresholds = six bisection rounds
+constexpr int kMsMaxRounds = 48;      // ratios stay exact dyadic doubles
+constexpr int kMsSlots = 16;          // copies of the per-pass totals
+
 // ---- update tiling ------------------------------------------------------------
 // Update tiles are aligned blocks of kUTile global positions; one workgroup
 // accumulates a tile's sparse contributions in LDS and then applies the SGD
@@ -116,6 +131,27 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
                        const uint32_t* base, uint64_t* flags, int32_t* idx_out, void* val_out,
                        int val16, uint32_t* status, uint32_t* clear_next, int64_t clear_words,
                        hipStream_t s, const Ev& ev);
+// MSTopK (one group, TKEF_APPROX). st[b] = state before pass b (written by
+// pass b's kernel), st[passes] = the final state (written by emit).
+hipError_t launch_ms_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,
+                            uint64_t* esum, uint32_t* emax, uint16_t* summ, hipStream_t s,
+                            const Ev& ev);
+hipError_t launch_ms_count(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,
+                           const uint64_t* esum, const uint32_t* emax, const uint16_t* summ,
+                           uint32_t* cnt, MsState* st_out, int64_t d, uint32_t* status,
+                           hipStream_t s, const Ev& ev);
+hipError_t launch_ms_refine(const TileDesc* tiles, const uint16_t* summ, int64_t nlines, int lpt,
+                            int32_t grid, int32_t nslots, const uint32_t* cnt_prev,
+                            uint32_t* cnt, const MsState* st_prev, MsState* st_out, uint32_t k,
+                            int64_t d, int32_t rounds_prev, int32_t n_search,
+                            uint64_t window_word, hipStream_t s, const Ev& ev);
+hipError_t launch_ms_emit(const TileDesc* tiles, const uint16_t* summ, int64_t nlines, int lpt,
+                          int32_t grid, int32_t nslots, const uint32_t* cnt_prev,
+                          const MsState* st_prev, MsState* st_out, uint32_t k, int64_t d,
+                          int32_t rounds_prev, int32_t n_search, uint64_t window_word,
+                          uint64_t* flags, int32_t* idx_out, void* val_out, int val16,
+                          uint32_t* status, uint32_t* clear_next, int64_t clear_words,
+                          hipStream_t s, const Ev& ev);
 // launch-shape limits of the selection kernels
 int32_t select_max_groups();
 int32_t select_block();

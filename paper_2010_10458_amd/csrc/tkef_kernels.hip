@@ -1636,6 +1636,587 @@ __global__ __launch_bounds__(kUBlock) void k_update(
 }
 
 // ---------------------------------------------------------------------------
+// MSTopK (Alg. 1): the approximate selector. a = |x|; the mean and the
+// maximum of a give the trial thresholds mean + ratio * (u - mean); N rounds
+// bisect ratio on the count of elements at or above the threshold; the
+// result is every element at or above thres1 (the largest count <= k seen)
+// plus a run of k - k1 elements, in position order, of the band
+// thres2 <= a < thres1 starting at an offset drawn by the caller.
+//
+// GPU form. Thresholds are compared as magnitude keys: a >= t (a binary32
+// widened exactly, t a double) holds exactly when key(a) >= K(t), K(t) the
+// key of the smallest binary32 >= t. Bisection is a binary tree, so one pass
+// that counts the elements at or above each of the 63 thresholds of the next
+// six rounds lets the rounds be replayed afterwards exactly as the loop
+// would run them: N rounds take ceil(N / 6) passes.
+//   ms_stream  x = g + r into r, line summaries, per-exponent sums of the
+//              significands of |x| (exact, in integers) and the largest key
+//   ms_count   forms the mean (the exact sum rounded once to double, divided
+//              by d) and u, then counts every element against the 63 keys of
+//              rounds 1..6
+//   ms_refine  replays the previous pass's rounds from its counts, then
+//              counts against the next 63 keys over the lines whose summary
+//              can reach the lowest of them (later rounds only look at the
+//              top of the distribution)
+//   ms_emit    replays the last pass's rounds, fixes K1 = K(thres1),
+//              K2 = K(thres2), the window offset and length, and writes the
+//              ordered compaction of {key >= K1} and of the window of the
+//              band {K2 <= key < K1}; the selected residuals are set to +0
+// The small state between passes (mean, u, bracket, recorded counts and
+// keys) is recomputed by every workgroup of the next kernel from the totals
+// of the previous pass (identical double operations everywhere);
+// workgroup 0 also stores it, for the kernels after and for the caller.
+// No workgroup waits for another, and no kernel needs a device-wide fence.
+namespace {
+
+constexpr int kMsKeys = 64;                // keys[1..63] of one pass (keys[0] unused)
+constexpr uint32_t kMsNone = 0x80000000u;  // "no thres1": above every key
+
+// Key of the smallest binary32 >= t, for t >= 0 (0 for t <= 0 or NaN).
+__device__ __forceinline__ uint32_t ms_key_ceil(double t) {
+  if (!(t > 0.0)) return 0u;
+  if (t > 3.4028234663852886e38) return 0x7F800000u;
+  const float f = (float)t;  // round to nearest
+  uint32_t b = __float_as_uint(f);
+  if ((double)f < t) b += 1u;
+  return b;
+}
+
+// The exact sum of binary32 magnitudes, rounded once to double (nearest,
+// ties to even). es[E] = the sum of the significands (hidden bit included)
+// of the magnitudes with exponent field E, so the sum is
+// sum_E es[E] * 2^(max(E, 1) - 150). Called by a whole workgroup of at least
+// 256 threads (thread E adds its term as three 32-bit digits into dig[], 10
+// words of LDS, zeroed here; es < 2^55 and a shift < 254 fit in 10 digits).
+// Returns the double in every thread.
+__device__ double ms_exact_sum(const unsigned long long* es, unsigned long long* dig,
+                               double* out) {
+  const int tid = threadIdx.x;
+  if (tid < 10) dig[tid] = 0ull;
+  __syncthreads();
+  if (tid < 255) {
+    const unsigned long long m = es[tid];
+    if (m) {
+      const int sft = (tid ? tid : 1) - 1;  // units of 2^-149
+      const int q = sft >> 5, o = sft & 31;
+      // m << o spans 87 bits at most: three digits from q
+      const unsigned long long lo = m << o;                      // bits 0..63 of m << o
+      const unsigned long long hi = o ? (m >> (64 - o)) : 0ull;  // bits 64..
+      atomicAdd(&dig[q], lo & 0xFFFFFFFFull);
+      atomicAdd(&dig[q + 1], lo >> 32);
+      if (hi) atomicAdd(&dig[q + 2], hi);
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    // carries: every digit becomes < 2^32; then five 64-bit limbs
+    uint64_t L[5];
+    unsigned long long c = 0ull;
+    uint32_t d32[10];
+    for (int i = 0; i < 10; ++i) {
+      const unsigned long long t = dig[i] + c;
+      d32[i] = (uint32_t)t;
+      c = t >> 32;
+    }
+    for (int i = 0; i < 5; ++i) L[i] = (uint64_t)d32[2 * i] | ((uint64_t)d32[2 * i + 1] << 32);
+    int top = -1;
+    for (int i = 4; i >= 0 && top < 0; --i)
+      if (L[i]) top = 64 * i + 63 - __clzll((long long)L[i]);
+    double v = 0.0;
+    if (top >= 0 && top < 53) {
+      v = ldexp((double)L[0], -149);
+    } else if (top >= 53) {
+      const int lo = top - 52, rb = lo - 1;
+      auto bits64 = [&](int b) -> uint64_t {  // 64 bits of L from bit b
+        const int q = b >> 6, o = b & 63;
+        uint64_t x = L[q] >> o;
+        if (o && q + 1 < 5) x |= L[q + 1] << (64 - o);
+        return x;
+      };
+      uint64_t m = bits64(lo) & ((1ull << 53) - 1ull);
+      const bool rnd = (bits64(rb) & 1ull) != 0ull;
+      bool sticky = false;
+      for (int i = 0; i < 5; ++i) {
+        const int b0 = 64 * i;
+        if (b0 + 64 <= rb) sticky |= L[i] != 0ull;
+        else if (b0 < rb) sticky |= (L[i] & ((1ull << (rb - b0)) - 1ull)) != 0ull;
+      }
+      int e = lo;
+      if (rnd && (sticky || (m & 1ull))) {
+        ++m;
+        if (m == (1ull << 53)) {
+          m >>= 1;
+          ++e;
+        }
+      }
+      v = ldexp((double)m, e - 149);
+    }
+    *out = v;
+  }
+  __syncthreads();
+  return *out;
+}
+
+// Significand (hidden bit included) of |x| added into its bin of the top
+// 11 key bits (exponent field and three leading fraction bits: the same
+// spread of addresses as a level-1 histogram, so few lanes of a wavefront
+// collide). Infinities and NaNs are left out (they make the input invalid).
+__device__ __forceinline__ void ms_accum(uint32_t key, unsigned long long* es) {
+  const uint32_t E = key >> 23;
+  const uint32_t m = (key & 0x7FFFFFu) | (E ? 0x800000u : 0u);
+  if (E < 255u) atomicAdd(&es[key >> kH1Shift], (unsigned long long)m);
+}
+
+// Keys of the 63 thresholds of the next six rounds into K[] (LDS): ratio_j =
+// l + j (r - l) / 64 (exact: r - l is a power of two), thres_j = mean +
+// ratio_j (u - mean) (the same double operations as a round of the loop).
+// Threads 0..63; ends with a barrier.
+__device__ __forceinline__ void ms_keys(const MsState& s, uint32_t* K) {
+  const int j = threadIdx.x;
+  if (j < kMsKeys) {
+    const double ratio = s.l + ((s.r - s.l) / 64.0) * (double)j;
+    K[j] = j ? ms_key_ceil(s.abar + ratio * (s.u - s.abar)) : 0u;
+  }
+  __syncthreads();
+}
+
+// Bin of a key in a pass: the largest j with K[j] <= key (key >= K[1]; the
+// keys ascend). K[8], K[16], .., K[56] first (seven reads in flight
+// together), then the seven keys of that group of eight.
+__device__ __forceinline__ int ms_bin(const uint32_t* K, uint32_t key) {
+  int g = 0;
+#pragma unroll
+  for (int i = 1; i < 8; ++i) g += (K[8 * i] <= key) ? 1 : 0;
+  const int base = 8 * g;
+  int j = base;
+#pragma unroll
+  for (int i = 1; i < 8; ++i) j += (K[base + i] <= key) ? 1 : 0;
+  return j;
+}
+
+// The state before the first pass, from the stream's partial sums. Whole
+// workgroup (>= 256 threads). es: 256 words of LDS.
+__device__ void ms_first_state(const unsigned long long* __restrict__ esum,
+                               const uint32_t* __restrict__ emax, int nslots, int64_t d,
+                               MsState& s, unsigned long long* es, uint32_t* mk) {
+  __shared__ unsigned long long dig[10];
+  __shared__ double sh_sum;
+  const int tid = threadIdx.x;
+  if (tid == 0) *mk = 0u;
+  if (tid < 256) {
+    unsigned long long v[kMsSlots];
+#pragma unroll
+    for (int sl = 0; sl < kMsSlots; ++sl) v[sl] = sl < nslots ? esum[(size_t)sl * 256 + tid] : 0ull;
+    unsigned long long t = 0ull;
+#pragma unroll
+    for (int sl = 0; sl < kMsSlots; ++sl) t += v[sl];
+    es[tid] = t;
+  }
+  __syncthreads();
+  if (tid < nslots) atomicMax(mk, emax[tid]);
+  const double total = ms_exact_sum(es, dig, &sh_sum);  // (its barriers publish *mk)
+  if (tid == 0) {
+    const uint32_t m = *mk;
+    const bool bad = m >= 0x7F800000u;
+    s.abar = bad ? 0.0 : total / (double)d;
+    s.u = bad ? 0.0 : (double)__uint_as_float(m);
+    s.l = 0.0;
+    s.r = 1.0;
+    s.k1 = 0u;
+    s.k2 = (uint32_t)d;
+    s.K1 = kMsNone;
+    s.K2 = 0u;
+    s.rand = 0u;
+    s.take = 0u;
+    s.level = 0u;
+    s.bad = bad ? 1u : 0u;
+  }
+  __syncthreads();
+}
+
+// The state after a pass: its counts (nslots copies of 64 bins, summed),
+// suffix sums, and its rounds replayed (round i takes bin j = midpoint of
+// the bins still open, whose key was made from the same ratio). After round
+// n_search the window offset and length are fixed too. Whole workgroup.
+// h: 64 words of LDS.
+__device__ void ms_next_state(const MsState& prev, const uint32_t* __restrict__ cnt, int nslots,
+                              int32_t rounds, int32_t n_search, uint32_t k, int64_t d,
+                              uint64_t window_word, MsState& s, uint32_t* h) {
+  const int tid = threadIdx.x;
+  if (tid < kMsKeys) h[tid] = 0u;
+  __syncthreads();
+  for (int i = tid; i < nslots * kMsKeys; i += blockDim.x) {
+    const uint32_t c = cnt[i];
+    if (c) atomicAdd(&h[i & (kMsKeys - 1)], c);
+  }
+  __syncthreads();
+  // nnz[j] = elements with key >= K[j] = sum of h[j..63]: a suffix scan by
+  // the first wavefront (lane t holds bin 63 - t)
+  if (tid < 64) {
+    static_assert(kMsKeys == 64, "one bin per lane");
+    const uint32_t run = wave_incl_scan(h[63 - tid]);
+    __builtin_amdgcn_wave_barrier();
+    h[63 - tid] = run;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const double abar = prev.abar, u = prev.u;
+    double l = prev.l, r = prev.r;
+    uint32_t k1 = prev.k1, k2 = prev.k2, K1 = prev.K1, K2 = prev.K2;
+    int jl = 0, jh = kMsKeys;
+    for (int i = 0; i < rounds; ++i) {
+      const int j = (jl + jh) / 2;
+      const double ratio = l + (r - l) / 2;
+      const double thres = abar + ratio * (u - abar);
+      const uint32_t n = h[j];
+      if (n <= k) {
+        r = ratio;
+        jh = j;
+        if (n > k1) {
+          k1 = n;
+          K1 = ms_key_ceil(thres);
+        }
+      } else {
+        l = ratio;
+        jl = j;
+        if (n < k2) {
+          k2 = n;
+          K2 = ms_key_ceil(thres);
+        }
+      }
+    }
+    s = prev;
+    s.level = prev.level + (uint32_t)rounds;
+    if (s.level >= (uint32_t)n_search) {
+      if (prev.bad) {  // non-finite input: the first k positions
+        k1 = 0u;
+        k2 = (uint32_t)d;
+        K1 = kMsNone;
+        K2 = 0u;
+        s.rand = 0u;
+      } else {
+        // band = k2 - k1 elements, k - k1 taken from it: offsets 0 .. k2 - k
+        s.rand = (uint32_t)(window_word % ((uint64_t)(k2 - k) + 1ull));
+      }
+      s.take = k - k1;
+    }
+    s.l = l;
+    s.r = r;
+    s.k1 = k1;
+    s.k2 = k2;
+    s.K1 = K1;
+    s.K2 = K2;
+  }
+  __syncthreads();
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(kBlock) void k_ms_stream(const TileDesc* __restrict__ tiles,
+                                                      int32_t ntiles, int nslots,
+                                                      unsigned long long* __restrict__ esum,
+                                                      uint32_t* __restrict__ emax,
+                                                      uint16_t* __restrict__ summ) {
+  __shared__ unsigned long long es[kH1Bins];
+  __shared__ uint32_t lmax[kQuarterLines];
+  __shared__ uint32_t bmax;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kH1Bins; i += kBlock) es[i] = 0ull;
+  if (tid == 0) bmax = 0u;
+  __syncthreads();
+  const int slot = blockIdx.x % nslots;
+  const int nunits = ntiles * (kTile / kQuarter);
+  uint32_t tmax = 0u;
+  for (int unit = blockIdx.x; unit < nunits; unit += gridDim.x) {
+    const TileDesc t = tiles[unit / (kTile / kQuarter)];
+    const int s0 = (unit % (kTile / kQuarter)) * kQuarter;
+    if (s0 >= t.len) continue;
+    const int len = min(kQuarter, t.len - s0);
+    const float* __restrict__ g = t.g + s0;
+    float* __restrict__ r = t.r + s0;
+    uint16_t* __restrict__ sq = summ + (size_t)(unit / (kTile / kQuarter)) * kLinesPerTile +
+                                s0 / kLine;
+    const bool full = len == kQuarter &&
+        ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(r)) & 15u) == 0;
+    if (full) {
+      const float4* __restrict__ g4 = reinterpret_cast<const float4*>(g);
+      float4* __restrict__ r4 = reinterpret_cast<float4*>(r);
+      float4 a[kQV], b[kQV];
+#pragma unroll
+      for (int v = 0; v < kQV; ++v) a[v] = load_nt4(g4 + v * kBlock + tid);
+#pragma unroll
+      for (int v = 0; v < kQV; ++v) b[v] = load_nt4(r4 + v * kBlock + tid);
+#pragma unroll
+      for (int v = 0; v < kQV; ++v) {
+        float4 x;
+        x.x = a[v].x + b[v].x;
+        x.y = a[v].y + b[v].y;
+        x.z = a[v].z + b[v].z;
+        x.w = a[v].w + b[v].w;
+        store_nt4(r4 + v * kBlock + tid, x);
+        const uint32_t k0 = mag_key(x.x), k1 = mag_key(x.y), k2 = mag_key(x.z), k3 = mag_key(x.w);
+        ms_accum(k0, es);
+        ms_accum(k1, es);
+        ms_accum(k2, es);
+        ms_accum(k3, es);
+        uint32_t m = max(max(k0, k1), max(k2, k3));
+        tmax = max(tmax, m);
+        m = max(m, (uint32_t)__shfl_xor((int)m, 1));
+        m = max(m, (uint32_t)__shfl_xor((int)m, 2));
+        m = max(m, (uint32_t)__shfl_xor((int)m, 4));
+        if ((tid & 7) == 0) sq[(v * kBlock + tid) >> 3] = (uint16_t)(m >> 16);
+      }
+    } else {
+      constexpr int kPer = kQuarter / kBlock;
+      if (tid < kQuarterLines) lmax[tid] = 0u;
+      __syncthreads();
+      float gv[kPer], rv[kPer];
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int e = q * kBlock + tid;
+        gv[q] = (e < len) ? gptr(g)[e] : 0.0f;
+        rv[q] = (e < len) ? gptr(r)[e] : 0.0f;
+      }
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int e = q * kBlock + tid;
+        if (e < len) {
+          const float x = gv[q] + rv[q];
+          gptr(r)[e] = x;
+          const uint32_t k = mag_key(x);
+          ms_accum(k, es);
+          atomicMax(&lmax[e / kLine], k);
+          tmax = max(tmax, k);
+        }
+      }
+      __syncthreads();
+      const int nl = (len + kLine - 1) / kLine;
+      if (tid < nl) sq[tid] = (uint16_t)(lmax[tid] >> 16);
+      __syncthreads();
+    }
+  }
+  atomicMax(&bmax, tmax);
+  __syncthreads();
+  // thread E: the eight bins of exponent field E, added into this copy
+  static_assert(kBlock == 256 && kH1Bins == 8 * kBlock, "one exponent per thread");
+  unsigned long long v = 0ull;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v += es[8 * tid + i];
+  if (v) atomicAdd(&esum[(size_t)slot * 256 + tid], v);
+  if (tid == 0 && bmax) atomicMax(&emax[slot], bmax);
+}
+
+// First counting pass: the state before it (mean, u), then every element
+// against the 63 keys of rounds 1..6 (persistent grid of kBlock-thread
+// workgroups walking units of kQuarter elements, two units in flight). A
+// line whose summary is below the lowest key holds no element to count and
+// is not read. A thread's hits (key >= lowest key) are marked in a bit mask
+// and binned one per round, so a wavefront runs as many bin searches as its
+// busiest lane has hits.
+__global__ __launch_bounds__(kBlock) void k_ms_count(
+    const TileDesc* __restrict__ tiles, int32_t ntiles, int nslots,
+    const unsigned long long* __restrict__ esum, const uint32_t* __restrict__ emax,
+    const uint16_t* __restrict__ summ, uint32_t* __restrict__ cnt,
+    MsState* __restrict__ st_out, int64_t d, uint32_t* __restrict__ status) {
+  __shared__ MsState s;
+  __shared__ unsigned long long es[256];
+  __shared__ uint32_t K[kMsKeys];
+  __shared__ uint32_t h[kMsKeys];
+  __shared__ uint32_t mk;
+  const int tid = threadIdx.x;
+  ms_first_state(esum, emax, nslots, d, s, es, &mk);
+  if (blockIdx.x == 0 && tid == 0) {
+    *st_out = s;
+    if (s.bad && status) atomicOr(status, TKEF_STATUS_NONFINITE);
+  }
+  if (tid < kMsKeys) h[tid] = 0u;
+  ms_keys(s, K);
+  const uint32_t kmin = K[1];
+  const uint32_t smin = kmin >> 16;  // a line is read if its summary reaches this
+  const int per_tile = kTile / kQuarter;
+  const int nunits = ntiles * per_tile;
+  constexpr int kSlots = 2 * kQV * 4;  // elements per thread per iteration
+  static_assert(kSlots <= 32, "hit mask");
+  for (int u0 = blockIdx.x; u0 < nunits; u0 += 2 * gridDim.x) {
+    float4 f[2][kQV];
+    int len[2];
+    bool full[2];
+    const float* xs[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int unit = u0 + q * gridDim.x;
+      len[q] = 0;
+      full[q] = false;
+      xs[q] = nullptr;
+      if (unit < nunits) {
+        const int tile = unit / per_tile;
+        const int s0 = (unit % per_tile) * kQuarter;
+        // the summaries' address does not depend on the descriptor: both
+        // loads are issued together
+        const uint16_t* sq = summ + (size_t)tile * kLinesPerTile + s0 / kLine;
+        uint32_t sv[kQV];
+#pragma unroll
+        for (int v = 0; v < kQV; ++v) sv[v] = sq[(v * kBlock + tid) >> 3];
+        const TileDesc t = tiles[tile];
+        len[q] = s0 < t.len ? min(kQuarter, t.len - s0) : 0;
+        xs[q] = t.r + s0;
+        full[q] = len[q] == kQuarter && (reinterpret_cast<uintptr_t>(xs[q]) & 15u) == 0;
+        if (full[q]) {
+          const float4* x4 = reinterpret_cast<const float4*>(xs[q]);
+#pragma unroll
+          for (int v = 0; v < kQV; ++v) {
+            const int i4 = v * kBlock + tid;  // float4 index: line i4 / 8
+            f[q][v] = (sv[v] >= smin) ? load_nt4(x4 + i4) : make_float4(0.f, 0.f, 0.f, 0.f);
+          }
+        }
+      }
+    }
+    uint32_t keys[kSlots];
+    uint32_t hits = 0u;
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int v = 0; v < kQV; ++v) {
+        const int b = (q * kQV + v) * 4;
+        keys[b + 0] = mag_key(f[q][v].x);
+        keys[b + 1] = mag_key(f[q][v].y);
+        keys[b + 2] = mag_key(f[q][v].z);
+        keys[b + 3] = mag_key(f[q][v].w);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          hits |= (full[q] && keys[b + c] >= kmin) ? (1u << (b + c)) : 0u;
+      }
+#pragma unroll 1
+    while (hits) {
+      const int j = __ffs(hits) - 1;
+      hits &= hits - 1u;
+      uint32_t key = 0u;
+#pragma unroll
+      for (int c = 0; c < kSlots; ++c) key = (c == j) ? keys[c] : key;
+      atomicAdd(&h[ms_bin(K, key)], 1u);
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      if (!full[q] && len[q] > 0) {
+        for (int e = tid; e < len[q]; e += kBlock) {
+          const uint32_t key = mag_key(gptr(xs[q])[e]);
+          if (key >= kmin) atomicAdd(&h[ms_bin(K, key)], 1u);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int slot = blockIdx.x % nslots;
+  if (tid < kMsKeys && h[tid]) atomicAdd(&cnt[(size_t)slot * kMsKeys + tid], h[tid]);
+}
+
+// Later counting passes: the state after the previous pass, then the lines
+// whose summary reaches keys[1] (the lowest threshold left to try), read by
+// the selection regions.
+__global__ __launch_bounds__(kSBlock) void k_ms_refine(
+    const TileDesc* __restrict__ tiles, const uint16_t* __restrict__ summ, int64_t nlines,
+    int lpt, int nslots, const uint32_t* __restrict__ cnt_prev, uint32_t* __restrict__ cnt,
+    const MsState* __restrict__ st_prev, MsState* __restrict__ st_out, uint32_t k, int64_t d,
+    int32_t rounds_prev, int32_t n_search, uint64_t window_word) {
+  __shared__ MsState s;
+  __shared__ uint32_t K[kMsKeys];
+  __shared__ uint32_t h[kMsKeys];
+  const int tid = threadIdx.x;
+  const MsState prev = *st_prev;
+  ms_next_state(prev, cnt_prev, nslots, rounds_prev, n_search, k, d, window_word, s, h);
+  if (blockIdx.x == 0 && tid == 0) *st_out = s;
+  if (tid < kMsKeys) h[tid] = 0u;
+  ms_keys(s, K);
+  const uint32_t kmin = K[1];
+  LineSpan ls;
+  ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
+  const uint32_t mask = ls.flagged([&](int) -> uint32_t { return kmin; });
+  walk_mask(ls, mask, [&](int, uint32_t key) -> bool { return key >= kmin; },
+            [&](int, const TileDesc&, int, float, uint32_t key) {
+              atomicAdd(&h[ms_bin(K, key)], 1u);
+            });
+  __syncthreads();
+  const int slot = blockIdx.x % nslots;
+  if (tid < kMsKeys && h[tid]) atomicAdd(&cnt[(size_t)slot * kMsKeys + tid], h[tid]);
+}
+
+// Ordered compaction: an element with key >= K1 goes to slot (#key >= K1
+// before it) + (#window members before it); a band member (K2 <= key < K1)
+// whose rank in the band lies in [rand, rand + take) goes to slot (#key >= K1
+// before it) + rank - rand. Prefixes across workgroups come from a bounded
+// look-back over the regions before.
+__global__ __launch_bounds__(kSBlock) void k_ms_emit(
+    const TileDesc* __restrict__ tiles, const uint16_t* __restrict__ summ, int64_t nlines,
+    int lpt, int nslots, const uint32_t* __restrict__ cnt_prev,
+    const MsState* __restrict__ st_prev, MsState* __restrict__ st_out, uint32_t k, int64_t d,
+    int32_t rounds_prev, int32_t n_search, uint64_t window_word, uint64_t* __restrict__ flags,
+    int32_t* __restrict__ idx_out, void* __restrict__ val_out, int val16,
+    uint32_t* __restrict__ status, uint32_t* __restrict__ clear_next, int64_t clear_words) {
+  __shared__ MsState s;
+  __shared__ uint32_t h[kMsKeys];
+  __shared__ uint32_t wsum[2 * kSWaves];
+  __shared__ uint64_t red[kSWaves];
+  __shared__ int32_t stage_code[kStage * kSBlock];
+  __shared__ float stage_x[kStage * kSBlock];
+  const int tid = threadIdx.x;
+  const MsState prev = *st_prev;
+  ms_next_state(prev, cnt_prev, nslots, rounds_prev, n_search, k, d, window_word, s, h);
+  if (blockIdx.x == 0 && tid == 0) *st_out = s;
+#pragma unroll 1
+  for (int64_t i = (int64_t)blockIdx.x * kSBlock + tid; i < clear_words;
+       i += (int64_t)gridDim.x * kSBlock)
+    clear_next[i] = 0u;
+  const uint32_t K1 = s.K1, K2 = s.K2, rand = s.rand, take = s.take;
+  LineSpan ls;
+  ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
+  const uint32_t mask = ls.flagged([&](int) -> uint32_t { return K2; });
+  auto hit = [&](int, uint32_t key) -> bool { return key >= K2; };
+  uint32_t c1 = 0u, c2 = 0u, nst = 0u;
+  walk_mask(ls, mask, hit, [&](int tile, const TileDesc&, int e, float x, uint32_t key) {
+    if (nst < (uint32_t)kStage) {
+      stage_code[nst * kSBlock + tid] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
+      stage_x[nst * kSBlock + tid] = x;
+    }
+    ++nst;
+    if (key >= K1) ++c1;
+    else ++c2;
+  });
+  uint2 tot;
+  const uint2 ex = block_scan2<kSBlock>(c1, c2, wsum, &tot);
+  const uint64_t pre = group_prefix(flags, (uint64_t)tot.x | ((uint64_t)tot.y << 31), red, status);
+  if (nst == 0u) return;
+  uint32_t p1 = (uint32_t)(pre & 0x7FFFFFFFu) + ex.x;
+  uint32_t p2 = (uint32_t)((pre >> 31) & 0x7FFFFFFFu) + ex.y;
+  auto write = [&](int, const TileDesc& t, int e, float x, uint32_t key) {
+    uint32_t pos = 0xFFFFFFFFu;
+    if (key >= K1) {
+      pos = p1 + min(p2 > rand ? p2 - rand : 0u, take);
+      ++p1;
+    } else {
+      if (p2 >= rand && p2 - rand < take) pos = p1 + (p2 - rand);
+      ++p2;
+    }
+    if (pos < k) {
+      idx_out[pos] = t.gstart + e;
+      put_val(val_out, (size_t)pos, x, val16);
+      gptr(t.r)[e] = 0.0f;
+    }
+  };
+  if (nst <= (uint32_t)kStage) {
+#pragma unroll 1
+    for (uint32_t q = 0; q < nst; ++q) {
+      const uint32_t code = (uint32_t)stage_code[q * kSBlock + tid];
+      const int tile = (int)(code >> kCandShift);
+      const TileDesc t = tiles[tile];
+      const float x = stage_x[q * kSBlock + tid];
+      write(tile, t, (int)(code & (kTile - 1)), x, mag_key(x));
+    }
+  } else {
+    walk_mask(ls, mask, hit, write);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launchers (the timing events, when given, are recorded by the dispatch)
 
 template <typename K, typename... Args>
@@ -1726,6 +2307,44 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
   return launch(k_emit, dim3(grid), dim3(kSBlock), s, ev, tiles, ntiles, groups, st, summ, nlines,
                 lpt, cand, meta, base, flags, idx_out, val_out, val16, status, clear_next,
                 clear_words);
+}
+
+hipError_t launch_ms_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,
+                            uint64_t* esum, uint32_t* emax, uint16_t* summ, hipStream_t s,
+                            const Ev& ev) {
+  return launch(k_ms_stream, dim3(grid), dim3(kBlock), s, ev, tiles, ntiles, (int)nslots,
+                reinterpret_cast<unsigned long long*>(esum), emax, summ);
+}
+
+hipError_t launch_ms_count(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,
+                           const uint64_t* esum, const uint32_t* emax, const uint16_t* summ,
+                           uint32_t* cnt, MsState* st_out, int64_t d, uint32_t* status,
+                           hipStream_t s, const Ev& ev) {
+  return launch(k_ms_count, dim3(grid), dim3(kBlock), s, ev, tiles, ntiles, (int)nslots,
+                reinterpret_cast<const unsigned long long*>(esum), emax, summ, cnt, st_out, d,
+                status);
+}
+
+hipError_t launch_ms_refine(const TileDesc* tiles, const uint16_t* summ, int64_t nlines, int lpt,
+                            int32_t grid, int32_t nslots, const uint32_t* cnt_prev,
+                            uint32_t* cnt, const MsState* st_prev, MsState* st_out, uint32_t k,
+                            int64_t d, int32_t rounds_prev, int32_t n_search,
+                            uint64_t window_word, hipStream_t s, const Ev& ev) {
+  return launch(k_ms_refine, dim3(grid), dim3(kSBlock), s, ev, tiles, summ, nlines, lpt,
+                (int)nslots, cnt_prev, cnt, st_prev, st_out, k, d, rounds_prev, n_search,
+                window_word);
+}
+
+hipError_t launch_ms_emit(const TileDesc* tiles, const uint16_t* summ, int64_t nlines, int lpt,
+                          int32_t grid, int32_t nslots, const uint32_t* cnt_prev,
+                          const MsState* st_prev, MsState* st_out, uint32_t k, int64_t d,
+                          int32_t rounds_prev, int32_t n_search, uint64_t window_word,
+                          uint64_t* flags, int32_t* idx_out, void* val_out, int val16,
+                          uint32_t* status, uint32_t* clear_next, int64_t clear_words,
+                          hipStream_t s, const Ev& ev) {
+  return launch(k_ms_emit, dim3(grid), dim3(kSBlock), s, ev, tiles, summ, nlines, lpt,
+                (int)nslots, cnt_prev, st_prev, st_out, k, d, rounds_prev, n_search, window_word,
+                flags, idx_out, val_out, val16, status, clear_next, clear_words);
 }
 
 int32_t select_max_groups() { return kSMaxGroups; }

@@ -147,3 +147,31 @@ def test_no_cpu_fallback_when_library_missing(tmp_path, monkeypatch):
     monkeypatch.setattr(tk, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError):
         tk.lib()
+
+
+def test_approx_plan_host_side():
+    """MSTopK plans: parameters, kernel count and names, and the errors the
+    host can see (no GPU needed)."""
+    L = tk.lib()
+    assert _create([10, 20], mode=tk.APPROX) == tk.OK
+    assert _create([10], mode=tk.APPROX, k=10, rho=0.0) == tk.OK
+    assert _create([10], mode=tk.APPROX, k=11, rho=0.0) == tk.ERANGE
+    p = tk.SparsifyPlan([1000, 8192 * 3 + 5], mode=tk.APPROX, rho=0.001)
+    assert p.ngroups == 1 and p.k_total == tk.k_from_rho(1000 + 8192 * 3 + 5, 0.001)
+    assert p.nlaunch == 2 + 5
+    names = p.launch_names()
+    assert names[0] == "ms_stream" and names[1] == "ms_count" and names[-1] == "ms_emit"
+    assert names[2:-1] == ["ms_refine1", "ms_refine2", "ms_refine3", "ms_refine4"]
+    for n, launches in ((1, 3), (6, 3), (7, 4), (12, 4), (13, 5), (48, 10)):
+        q = tk.SparsifyPlan([5000], mode=tk.APPROX, k=7, n_search=n)
+        assert q.nlaunch == launches, n
+    h = p._h
+    assert L.tkef_sparsify_plan_set_approx(h, 0, 0) == tk.EINVAL
+    assert L.tkef_sparsify_plan_set_approx(h, 49, 0) == tk.EINVAL
+    assert L.tkef_sparsify_plan_set_approx(h, 30, 2**64 - 1) == tk.OK
+    assert L.tkef_sparsify_plan_set_approx(None, 30, 0) == tk.EINVAL
+    g = tk.SparsifyPlan([1000], rho=0.01)
+    assert L.tkef_sparsify_plan_set_approx(g._h, 30, 0) == tk.EINVAL
+    P = ctypes.c_void_p
+    assert L.tkef_sparsify_approx_result(g._h, P(0x10000), None, None, None) == tk.EINVAL
+    assert L.tkef_sparsify_approx_result(h, P(0x10000), None, None, None) == tk.ESTATE
