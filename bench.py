@@ -218,6 +218,62 @@ def extras(args, tk, gen, sizes, d, bank, resid, idx_all, val_all, nnz, k_total,
     ex["aggregate_kernels_us"] = kern
     del outs, aplans
 
+    log("extras: LARS (Eq. lars) step fused with the P = 128 aggregate; dense rates")
+    lw = [[t.clone() for t in bank[j % len(bank)]] for j in range(R)]   # parameters
+    lb = [[torch.zeros_like(t) for t in bank[0]] for _ in range(R)]     # momentum
+    lplans = [tk.UpdatePlan(sizes, P=P_WORKERS, stride=K_LIST).bind(lw[j], lb[j]) for j in range(R)]
+    names = list(tk.LARS_LAUNCHES)
+
+    def lars_run(i, t=None):
+        j = i % R
+        if t is not None:
+            lplans[j].set_events(t)
+        lplans[j].lars_execute(idx_all[j], val_all[j], 0.001, LR, WD, mu=MU, nnz=nnz)
+        if t is not None:
+            lplans[j].set_events(None)
+
+    for i in range(W):
+        lars_run(i)
+    evs = [make_events(len(names) + 1) for _ in range(K)]
+    torch.cuda.synchronize()
+    for t in range(K):
+        lars_run(W + t, evs[t])
+    torch.cuda.synchronize()
+    import numpy as np
+    ms = float(np.mean([e[0].elapsed_time(e[-1]) for e in evs]))
+    kern = {n: round(float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs])) * 1e3, 2)
+            for i, n in enumerate(names)}
+    pairs = k_total + (P_WORKERS - 1) * K_LIST
+    lbytes = 20 * d + 16 * pairs   # norm pass: w + lists; step: w, b in and out + lists
+    ex["lars_update"] = {"us": round(ms * 1e3, 2), "GBps": round(lbytes / (ms / 1e3) / 1e9, 1),
+                         "algorithmic_bytes": lbytes, "kernels_us": kern}
+    del lplans, lw, lb
+    for model, shapes in (("resnet50", gen.resnet50_shapes()), ("transformer", gen.transformer_shapes())):
+        szs = gen.numels(shapes)
+        dd = sum(szs)
+        ws_ = [torch.randn(n, device=dev) * 0.05 for n in szs]
+        gs_ = [torch.randn(n, device=dev) * 1e-3 for n in szs]
+        rp = tk.UpdatePlan(szs, P=1, stride=0).bind(ws_)
+        rp.bind_grads(gs_)
+        rates = torch.empty(len(szs), dtype=torch.float64, device=dev)
+        dn = list(tk.LARS_DENSE_LAUNCHES)
+        for _ in range(W):
+            rp.lars_rates(0.001, LR, WD, rates=rates)
+        evs = [make_events(len(dn) + 1) for _ in range(K)]
+        torch.cuda.synchronize()
+        for t in range(K):
+            rp.set_events(evs[t])
+            rp.lars_rates(0.001, LR, WD, rates=rates)
+            rp.set_events(None)
+        torch.cuda.synchronize()
+        ms = float(np.mean([e[0].elapsed_time(e[-1]) for e in evs]))
+        ex[f"lars_rates_{model}"] = {
+            "layers": len(szs), "d": dd, "us": round(ms * 1e3, 2),
+            "GBps": round(8 * dd / (ms / 1e3) / 1e9, 1),
+            "kernels_us": {n: round(float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs])) * 1e3, 2)
+                           for i, n in enumerate(dn)}}
+        del rp, ws_, gs_
+
     log("extras: shard-shaped sparsify (1 of 8 shards)")
     n_sh = 8
     shard = -(-d // n_sh)

@@ -271,6 +271,50 @@ int tkef_sparse_aggregate(float *const *outs, const int64_t *numels, int32_t nte
                           int64_t stride, const int32_t *nnz, void *ws, size_t ws_bytes,
                           uint32_t *status, hipStream_t stream);
 
+/* ========================================================================
+ * LARS (Eq. lars: the layer-wise rate rate_l = gamma * eta * ||w_l|| /
+ * (||g_l|| + eps * ||w_l||), eps being the weight decay; the step is the one
+ * of the LARS method the paper cites)
+ *
+ * A layer is one tensor of the update plan's list. Norms are Euclidean, summed
+ * in double (in a fixed order: the same inputs give the same rates on every
+ * run); when ||w_l|| or ||g_l|| is zero the rate is gamma * eta. The step, in
+ * binary32 with the rate rounded to binary32 once, for every position:
+ *   D = g + eps * w;  U = rate * D;
+ *   with momentum (mu != 0, momentum bound):  b = mu * b + U;  w = w - b
+ *   without:                                  w = w - U
+ * ====================================================================== */
+
+/* Fused sparse aggregate + LARS step: g is the sum of the P workers' lists
+ * (the layout and value format of tkef_update_execute). Four kernels: seg,
+ * lars_norm (the tile sums and the partial norms), lars_rates, lars_step
+ * (names from tkef_lars_launch_name(0, i); the timing hook of
+ * tkef_update_plan_set_events takes 5 events). rate_out: optional device
+ * array of ntensors doubles receiving the rates. mu != 0 needs momentum
+ * buffers bound. TKEF_ERANGE for non-finite gamma, eta, eps or mu. */
+int tkef_lars_update_execute(tkef_update_plan plan, const int32_t *idx, const void *val,
+                             const int32_t *nnz, double gamma, double eta, double eps,
+                             float mu, double *rate_out, void *ws, size_t ws_bytes,
+                             uint32_t *status, hipStream_t stream);
+
+/* Dense gradients for tkef_lars_rates_execute: grads[t] (host array of device
+ * pointers, non-null where numel > 0), same sizes as the bound parameters.
+ * Host; copies a pointer table into ws and synchronizes `stream`. ws must be
+ * the bound workspace (TKEF_ESTATE otherwise); a later bind forgets them. */
+int tkef_update_plan_bind_grads(tkef_update_plan plan, const float *const *grads, void *ws,
+                                size_t ws_bytes, hipStream_t stream);
+
+/* The layer-wise rates from the bound parameters and dense gradients (the
+ * computation the paper distributes over GPUs layer by layer, Sec. 4.2: one
+ * GPU's share is a plan over its layers). rate_out: device array of
+ * ntensors doubles. Two kernels (tkef_lars_launch_name(1, i)). */
+int tkef_lars_rates_execute(tkef_update_plan plan, double gamma, double eta, double eps,
+                            double *rate_out, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Kernel names of the LARS executions: dense = 0 for tkef_lars_update_execute
+ * (i = 0..3), 1 for tkef_lars_rates_execute (i = 0..1); NULL otherwise. */
+const char *tkef_lars_launch_name(int32_t dense, int32_t i);
+
 #ifdef __cplusplus
 }
 #endif

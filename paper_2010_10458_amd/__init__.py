@@ -82,6 +82,11 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
         "tkef_sparse_aggregate": ([P(vp), P(i64), i32, vp, vp, i32, i32, i64, vp, vp, sz, vp,
                                    vp], ctypes.c_int),
         "tkef_update_workspace": ([P(i64), i32, i32, i64, P(sz)], ctypes.c_int),
+        "tkef_lars_update_execute": ([vp, vp, vp, vp, f64, f64, f64, f32, vp, vp, sz, vp, vp],
+                                     ctypes.c_int),
+        "tkef_update_plan_bind_grads": ([vp, P(vp), vp, sz, vp], ctypes.c_int),
+        "tkef_lars_rates_execute": ([vp, f64, f64, f64, vp, vp, sz, vp], ctypes.c_int),
+        "tkef_lars_launch_name": ([i32, i32], ctypes.c_char_p),
         "tkef_sparse_aggregate_update": ([P(vp), P(vp), P(i64), i32, vp, vp, i32, i64, vp, f32,
                                           f32, f32, vp, sz, vp, vp], ctypes.c_int),
     }
@@ -265,6 +270,10 @@ class SparsifyPlan:
                 "take": cnt[3], "key1": cnt[4], "key2": cnt[5]}
 
 
+LARS_LAUNCHES = ["seg", "lars_norm", "lars_rates", "lars_step"]
+LARS_DENSE_LAUNCHES = ["lars_norm_dense", "lars_rates"]
+
+
 class UpdatePlan:
     """Plan for the sparse aggregate + SGD update of a fixed parameter list."""
 
@@ -341,6 +350,49 @@ class UpdatePlan:
             nnz.data_ptr() if nnz is not None else None, float(lr), float(mu), float(wd),
             self.ws.data_ptr(), self.ws.numel(),
             status.data_ptr() if status is not None else None, _stream_handle(stream)))
+
+    def lars_execute(self, idx: torch.Tensor, val: torch.Tensor, gamma: float, eta: float,
+                     eps: float, mu: float = 0.0, nnz: Optional[torch.Tensor] = None,
+                     status: Optional[torch.Tensor] = None,
+                     rates: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """Sum the lists and apply the LARS step (Eq. lars rates) to the bound
+        tensors. Returns the per-tensor rates (float64)."""
+        self._check_lists(idx, val, nnz)
+        if rates is None:
+            rates = torch.empty(len(self._numels), dtype=torch.float64, device=self.ws.device)
+        _check("tkef_lars_update_execute", lib().tkef_lars_update_execute(
+            self._h, idx.data_ptr(), val.data_ptr(),
+            nnz.data_ptr() if nnz is not None else None, float(gamma), float(eta), float(eps),
+            float(mu), rates.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
+            status.data_ptr() if status is not None else None, _stream_handle(stream)))
+        return rates
+
+    def bind_grads(self, grads: Sequence[torch.Tensor], stream=None) -> "UpdatePlan":
+        """Dense gradients (same sizes as the bound parameters) for lars_rates."""
+        if self._bound is None or self.ws is None:
+            raise RuntimeError("plan is not bound")
+        if len(grads) != len(self._numels):
+            raise ValueError("tensor count does not match the plan")
+        _check_f32_tensors(list(grads), "bind_grads")
+        for g, n in zip(grads, self._numels):
+            if g.numel() != n:
+                raise ValueError("tensor size does not match the plan")
+        _check("tkef_update_plan_bind_grads", lib().tkef_update_plan_bind_grads(
+            self._h, _ptr_array(grads), self.ws.data_ptr(), self.ws.numel(),
+            _stream_handle(stream)))
+        self._grads = list(grads)
+        return self
+
+    def lars_rates(self, gamma: float, eta: float, eps: float,
+                   rates: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """Layer-wise rates of Eq. (lars) from the bound parameters and the
+        dense gradients of bind_grads (float64, one per tensor)."""
+        if rates is None:
+            rates = torch.empty(len(self._numels), dtype=torch.float64, device=self.ws.device)
+        _check("tkef_lars_rates_execute", lib().tkef_lars_rates_execute(
+            self._h, float(gamma), float(eta), float(eps), rates.data_ptr(), self.ws.data_ptr(),
+            self.ws.numel(), _stream_handle(stream)))
+        return rates
 
     def aggregate(self, idx: torch.Tensor, val: torch.Tensor, nnz: Optional[torch.Tensor] = None,
                   status: Optional[torch.Tensor] = None, stream=None) -> None:

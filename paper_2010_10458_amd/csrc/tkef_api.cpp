@@ -566,6 +566,10 @@ extern "C" int tkef_sparsify(const float* const* grads, float* const* residuals,
 
 static const char* const kUpdateLaunches[] = {"seg", "update"};
 constexpr int32_t kUpdateNLaunch = 2;
+// LARS executions: the fused sparse update (seg, norms, rates, step) and the
+// rates from dense gradients (norms, rates)
+static const char* const kLarsLaunches[] = {"seg", "lars_norm", "lars_rates", "lars_step"};
+static const char* const kLarsDenseLaunches[] = {"lars_norm_dense", "lars_rates"};
 
 struct tkef_update_plan_s {
   int32_t ntensors = 0, P = 0, ntiles_u = 0;
@@ -573,9 +577,12 @@ struct tkef_update_plan_s {
   std::vector<int64_t> numels, goff;
   std::vector<UpdTensor> tens;
   std::vector<int32_t> tile_first;
-  size_t off_tens = 0, off_first = 0, off_seg = 0, ws_bytes = 0;
+  std::vector<int32_t> tpair;  // LARS: first (tile, tensor) pair of each tensor; [T] = pairs
+  size_t off_tens = 0, off_first = 0, off_seg = 0, off_tpair = 0, off_part = 0, off_rate = 0,
+         off_gptr = 0, ws_bytes = 0;
   void* bound_ws = nullptr;
   bool has_mom = false;
+  bool has_grads = false;  // dense gradients bound (LARS rates)
   int32_t val_format = TKEF_VAL_F32;  // value arrays read by execute / aggregate
   hipEvent_t* events = nullptr;
   int32_t n_events = 0;
@@ -614,11 +621,24 @@ extern "C" int tkef_update_plan_create(const int64_t* numels, int32_t ntensors, 
       while (t < ntensors && p->goff[t] + numels[t] <= pos) ++t;
       p->tile_first[u] = t;
     }
+    // LARS pairs: tensor t overlaps update tiles goff_t >> kUShift ..
+    // (goff_t + n_t - 1) >> kUShift
+    p->tpair.assign(ntensors + 1, 0);
+    for (int32_t t = 0; t < ntensors; ++t) {
+      const int64_t n = numels[t];
+      const int64_t tiles = n > 0 ? ((p->goff[t] + n - 1) >> kUShift) - (p->goff[t] >> kUShift) + 1
+                                  : 0;
+      p->tpair[t + 1] = p->tpair[t] + (int32_t)tiles;
+    }
     p->tens.resize(ntensors);
     size_t o = 0;
     p->off_tens = o;   o = align_up(o + p->tens.size() * sizeof(UpdTensor));
     p->off_first = o;  o = align_up(o + p->tile_first.size() * sizeof(int32_t));
     p->off_seg = o;    o = align_up(o + (size_t)P * (p->ntiles_u + 1) * sizeof(int32_t));
+    p->off_tpair = o;  o = align_up(o + p->tpair.size() * sizeof(int32_t));
+    p->off_part = o;   o = align_up(o + (size_t)p->tpair[ntensors] * 16);
+    p->off_rate = o;   o = align_up(o + (size_t)ntensors * sizeof(double));
+    p->off_gptr = o;   o = align_up(o + (size_t)ntensors * sizeof(float*));
     p->ws_bytes = o;
   } catch (const std::bad_alloc&) {
     delete p;
@@ -670,6 +690,9 @@ extern "C" int tkef_update_plan_bind(tkef_update_plan plan, float* const* params
     e = hipMemcpyAsync(base + plan->off_first, plan->tile_first.data(),
                        plan->tile_first.size() * sizeof(int32_t), hipMemcpyHostToDevice,
                        stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(base + plan->off_tpair, plan->tpair.data(),
+                       plan->tpair.size() * sizeof(int32_t), hipMemcpyHostToDevice, stream);
   if (e == hipSuccess) e = hipStreamSynchronize(stream);
   if (e != hipSuccess) {
     plan->bound_ws = nullptr;
@@ -677,6 +700,27 @@ extern "C" int tkef_update_plan_bind(tkef_update_plan plan, float* const* params
   }
   plan->bound_ws = ws;
   plan->has_mom = momentum != nullptr;
+  plan->has_grads = false;
+  return TKEF_OK;
+}
+
+extern "C" int tkef_update_plan_bind_grads(tkef_update_plan plan, const float* const* grads,
+                                           void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!plan || !grads) return TKEF_EINVAL;
+  if (!ws || ws_bytes < plan->ws_bytes || !aligned_ws(ws)) return TKEF_EWORKSPACE;
+  if (plan->bound_ws != ws) return TKEF_ESTATE;
+  std::vector<const float*> g(plan->ntensors, nullptr);
+  for (int32_t t = 0; t < plan->ntensors; ++t) {
+    if (plan->numels[t] == 0) continue;
+    if (!grads[t]) return TKEF_EINVAL;
+    g[t] = grads[t];
+  }
+  char* base = static_cast<char*>(ws);
+  hipError_t e = hipMemcpyAsync(base + plan->off_gptr, g.data(), g.size() * sizeof(float*),
+                                hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return TKEF_EHIP;
+  plan->has_grads = true;
   return TKEF_OK;
 }
 
@@ -720,9 +764,13 @@ int update_run(tkef_update_plan plan, const int32_t* idx, const void* val, const
                             seg, status, s, tr.at(0));
   if (e == hipSuccess)
     e = launch_update(tens, first, plan->ntensors, (int32_t)plan->d, plan->ntiles_u, idx, val,
-                      val16, plan->stride, nnz, plan->P, seg, lr, mu, wd, op, has_mom, s,
-                      tr.at(1));
+                      val16, plan->stride, nnz, plan->P, seg, lr, mu, wd, op, has_mom,
+                      LarsArgs{nullptr, nullptr, nullptr, 0.0f}, s, tr.at(1));
   return hip_rc(e);
+}
+
+bool finite_all(double a, double b, double c) {
+  return std::isfinite(a) && std::isfinite(b) && std::isfinite(c);
 }
 
 }  // namespace
@@ -741,6 +789,72 @@ extern "C" int tkef_aggregate_execute(tkef_update_plan plan, const int32_t* idx,
                                       const int32_t* nnz, void* ws, size_t ws_bytes,
                                       uint32_t* status, hipStream_t s) {
   return update_run(plan, idx, val, nnz, 0.0f, 0.0f, 0.0f, kOpAggregate, ws, ws_bytes, status, s);
+}
+
+extern "C" int tkef_lars_update_execute(tkef_update_plan plan, const int32_t* idx,
+                                        const void* val, const int32_t* nnz, double gamma,
+                                        double eta, double eps, float mu, double* rate_out,
+                                        void* ws, size_t ws_bytes, uint32_t* status,
+                                        hipStream_t s) {
+  if (!plan) return TKEF_EINVAL;
+  if (!finite_all(gamma, eta, eps) || !std::isfinite(mu)) return TKEF_ERANGE;
+  if (mu != 0.0f && !plan->has_mom) return TKEF_EINVAL;
+  if (!ws || ws_bytes < plan->ws_bytes || !aligned_ws(ws)) return TKEF_EWORKSPACE;
+  if (plan->bound_ws != ws) return TKEF_ESTATE;
+  if (plan->stride > 0 && (!idx || !val)) return TKEF_EINVAL;
+  char* base = static_cast<char*>(ws);
+  const UpdTensor* tens = reinterpret_cast<const UpdTensor*>(base + plan->off_tens);
+  const int32_t* first = reinterpret_cast<const int32_t*>(base + plan->off_first);
+  int32_t* seg = reinterpret_cast<int32_t*>(base + plan->off_seg);
+  const int32_t* tpair = reinterpret_cast<const int32_t*>(base + plan->off_tpair);
+  double2* part = reinterpret_cast<double2*>(base + plan->off_part);
+  double* rate = reinterpret_cast<double*>(base + plan->off_rate);
+  const int has_mom = mu != 0.0f ? 1 : 0;
+  const int val16 = plan->val_format == TKEF_VAL_F16 ? 1 : 0;
+  const float eps32 = static_cast<float>(eps);
+  const Tracer tr{plan->events, plan->n_events};
+  const int32_t d = (int32_t)plan->d, T = plan->ntensors;
+  hipError_t e = launch_seg(idx, plan->stride, nnz, plan->P, d, plan->ntiles_u, seg, status, s,
+                            tr.at(0));
+  if (e == hipSuccess)
+    e = launch_update(tens, first, T, d, plan->ntiles_u, idx, val, val16, plan->stride, nnz,
+                      plan->P, seg, 0.0f, 0.0f, 0.0f, kOpLarsNorm, 0,
+                      LarsArgs{part, tpair, nullptr, eps32}, s, tr.at(1));
+  if (e == hipSuccess)
+    e = launch_lars_rates(tpair, part, T, gamma, eta, eps, rate, rate_out, s, tr.at(2));
+  if (e == hipSuccess)
+    e = launch_update(tens, first, T, d, plan->ntiles_u, idx, val, val16, plan->stride, nnz,
+                      plan->P, seg, 0.0f, mu, 0.0f, kOpLarsApply, has_mom,
+                      LarsArgs{part, tpair, rate, eps32}, s, tr.at(3));
+  return hip_rc(e);
+}
+
+extern "C" int tkef_lars_rates_execute(tkef_update_plan plan, double gamma, double eta,
+                                       double eps, double* rate_out, void* ws, size_t ws_bytes,
+                                       hipStream_t s) {
+  if (!plan) return TKEF_EINVAL;
+  if (!finite_all(gamma, eta, eps)) return TKEF_ERANGE;
+  if (!ws || ws_bytes < plan->ws_bytes || !aligned_ws(ws)) return TKEF_EWORKSPACE;
+  if (plan->bound_ws != ws || !plan->has_grads) return TKEF_ESTATE;
+  char* base = static_cast<char*>(ws);
+  const UpdTensor* tens = reinterpret_cast<const UpdTensor*>(base + plan->off_tens);
+  const int32_t* first = reinterpret_cast<const int32_t*>(base + plan->off_first);
+  const int32_t* tpair = reinterpret_cast<const int32_t*>(base + plan->off_tpair);
+  double2* part = reinterpret_cast<double2*>(base + plan->off_part);
+  double* rate = reinterpret_cast<double*>(base + plan->off_rate);
+  const float* const* gptrs = reinterpret_cast<const float* const*>(base + plan->off_gptr);
+  const Tracer tr{plan->events, plan->n_events};
+  hipError_t e = launch_lars_norm_dense(tens, gptrs, first, plan->ntensors, (int32_t)plan->d,
+                                        plan->ntiles_u, part, tpair, s, tr.at(0));
+  if (e == hipSuccess)
+    e = launch_lars_rates(tpair, part, plan->ntensors, gamma, eta, eps, rate, rate_out, s,
+                          tr.at(1));
+  return hip_rc(e);
+}
+
+extern "C" const char* tkef_lars_launch_name(int32_t dense, int32_t i) {
+  if (dense) return (i >= 0 && i < 2) ? kLarsDenseLaunches[i] : nullptr;
+  return (i >= 0 && i < 4) ? kLarsLaunches[i] : nullptr;
 }
 
 extern "C" int tkef_update_workspace(const int64_t* numels, int32_t ntensors, int32_t P,

@@ -79,7 +79,18 @@ constexpr int kUShift = 12;
 constexpr int kUTile = 1 << kUShift;  // 4096 positions, 16 KB of LDS
 
 // what the update kernel does with the tile sums G
-enum { kOpSgd = 0, kOpSparseSgd = 1, kOpAggregate = 2 };
+enum { kOpSgd = 0, kOpSparseSgd = 1, kOpAggregate = 2, kOpLarsNorm = 3, kOpLarsApply = 4 };
+
+// LARS (Eq. lars): per (update tile, tensor) pair the partial sums of w^2 and
+// G^2 (double); pairs are tensor-major, tensor t owning [tpair[t],
+// tpair[t + 1]), one per update tile it overlaps, in tile order. rate[t] is
+// the tensor's rate (double).
+struct LarsArgs {
+  double2* part;
+  const int32_t* tpair;
+  const double* rate;
+  float eps;
+};
 
 struct UpdTensor {       // 32 B, one per parameter tensor, written at bind
   float* w;
@@ -164,6 +175,15 @@ hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32
                          int32_t d, int32_t ntiles_u, const int32_t* idx, const void* val,
                          int val16, int64_t stride, const int32_t* nnz, int32_t P,
                          const int32_t* seg, float lr, float mu, float wd, int op, int has_mom,
-                         hipStream_t s, const Ev& ev);
+                         const LarsArgs& lars, hipStream_t s, const Ev& ev);
+// LARS: partial sums of w^2 and g^2 from dense gradients (g pointer per
+// tensor), and the per-tensor rates from the partial sums
+hipError_t launch_lars_norm_dense(const UpdTensor* tens, const float* const* gptrs,
+                                  const int32_t* tile_first, int32_t ntens, int32_t d,
+                                  int32_t ntiles_u, double2* part, const int32_t* tpair,
+                                  hipStream_t s, const Ev& ev);
+hipError_t launch_lars_rates(const int32_t* tpair, const double2* part, int32_t ntens,
+                             double gamma, double eta, double eps, double* rate,
+                             double* rate_out, hipStream_t s, const Ev& ev);
 
 }  // namespace tkef

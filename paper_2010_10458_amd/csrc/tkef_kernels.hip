@@ -1439,17 +1439,65 @@ __device__ __forceinline__ float sgd_step(float G, float w, float& b, bool mom, 
   return w - stepv;
 }
 
+// LARS step (the cited method's update with the rate of Eq. lars):
+// D = G + eps w; U = rate D; b = mu b + U and w - b (momentum), else w - U.
+__device__ __forceinline__ float lars_step(float G, float w, float& b, bool mom, float rate,
+                                           float mu, float eps) {
+  const float decay = eps * w;
+  const float D = G + decay;
+  const float U = rate * D;
+  if (mom) {
+    const float keep = mu * b;
+    b = keep + U;
+    return w - b;
+  }
+  return w - U;
+}
+
+// Sum of two doubles per thread over a kUBlock-thread workgroup, in a fixed
+// order (wave butterflies, then the waves in order). red: 2 * kUBlock / 64
+// doubles of LDS. Result valid in thread 0; ends with a barrier.
+__device__ __forceinline__ double2 ublock_sum2(double a, double b, double* red) {
+  constexpr int NW = kUBlock / 64;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    a += __shfl_xor(a, off);
+    b += __shfl_xor(b, off);
+  }
+  if ((tid & 63) == 0) {
+    red[tid >> 6] = a;
+    red[NW + (tid >> 6)] = b;
+  }
+  __syncthreads();
+  double2 r = make_double2(0.0, 0.0);
+  if (tid == 0) {
+    for (int i = 0; i < NW; ++i) {
+      r.x += red[i];
+      r.y += red[NW + i];
+    }
+  }
+  __syncthreads();
+  return r;
+}
+
 constexpr int kXcds = 8;                      // MI355X: 8 accelerator dies
 constexpr int kUVecPerThread = kUTile / 4 / kUBlock;  // float4 per thread per tile
 
+// kLars: the LARS norm and step passes (a separate instantiation, so the SGD
+// and aggregation passes keep their register budget).
+template <bool kLars>
 __global__ __launch_bounds__(kUBlock) void k_update(
     const UpdTensor* __restrict__ tens, const int32_t* __restrict__ tile_first, int32_t ntens,
     int32_t d, int32_t ntiles_u, int32_t per_xcd, const int32_t* __restrict__ idx,
     const void* __restrict__ val, int val16, int64_t stride, const int32_t* __restrict__ nnz,
     int32_t P, const int32_t* __restrict__ seg, float lr, float mu, float wd, int op,
-    int has_mom) {
+    int has_mom, LarsArgs lars) {
   const bool sparse_mode = op == kOpSparseSgd;
   const bool densify = op == kOpAggregate;
+  const bool lnorm = kLars && op == kOpLarsNorm;
+  const bool lapply = kLars && op == kOpLarsApply;
+  __shared__ double lred[2 * kUBlock / 64];
   __shared__ __align__(16) float acc[kUTile];
   __shared__ uint32_t mask[kUTile / 32];
   __shared__ int32_t sbeg[kUBlock];
@@ -1481,8 +1529,9 @@ __global__ __launch_bounds__(kUBlock) void k_update(
     const float4* b4 = reinterpret_cast<const float4*>(b_tile);
 #pragma unroll
     for (int q = 0; q < kUVecPerThread; ++q) {
-      wv[q] = load_nt4(w4 + q * kUBlock + tid);
-      if (mom) bv[q] = load_nt4(b4 + q * kUBlock + tid);
+      // (the norm pass reads w again in the step pass: keep it cached)
+      wv[q] = lnorm ? w4[q * kUBlock + tid] : load_nt4(w4 + q * kUBlock + tid);
+      if (mom && !lnorm) bv[q] = load_nt4(b4 + q * kUBlock + tid);
     }
   }
 
@@ -1545,7 +1594,41 @@ __global__ __launch_bounds__(kUBlock) void k_update(
     __syncthreads();
   }
 
-  // 2. apply the SGD step
+  // 2a. LARS norms: per tensor of the tile, sum w^2 and G^2 (double) into
+  // its pair
+  if (lnorm) {
+    const int32_t tl = fast ? t0 : min(tile_first[u + 1], ntens - 1);
+    for (int ti = t0; ti <= tl; ++ti) {
+      const UpdTensor tt = tens[ti];
+      const int64_t a = max((int64_t)base, tt.goff);
+      const int64_t z = min((int64_t)base + len, tt.goff + tt.n);
+      if (z <= a) continue;  // (uniform in the workgroup)
+      double sw = 0.0, sg = 0.0;
+      if (fast) {
+        const float4* a4 = reinterpret_cast<const float4*>(acc);
+#pragma unroll
+        for (int q = 0; q < kUVecPerThread; ++q) {
+          const float4 G = a4[q * kUBlock + tid];
+          const float4 w = wv[q];
+          sw += (double)w.x * w.x + (double)w.y * w.y + (double)w.z * w.z + (double)w.w * w.w;
+          sg += (double)G.x * G.x + (double)G.y * G.y + (double)G.z * G.z + (double)G.w * G.w;
+        }
+      } else {
+        const gfloat* w = gptr(tt.w + (a - tt.goff));
+        const int la = (int)(a - base), cnt = (int)(z - a);
+        for (int q = tid; q < cnt; q += kUBlock) {
+          const double wq = w[q], gq = acc[la + q];
+          sw += wq * wq;
+          sg += gq * gq;
+        }
+      }
+      const double2 r = ublock_sum2(sw, sg, lred);
+      if (tid == 0) lars.part[lars.tpair[ti] + (u - (int32_t)(tt.goff >> kUShift))] = r;
+    }
+    return;
+  }
+
+  // 2. apply the SGD (or LARS) step
   if (fast) {
     float4* w4 = reinterpret_cast<float4*>(w_tile);
     float4* b4 = reinterpret_cast<float4*>(b_tile);
@@ -1559,10 +1642,18 @@ __global__ __launch_bounds__(kUBlock) void k_update(
         continue;
       }
       float4 w = wv[q], bb = mom ? bv[q] : make_float4(0.f, 0.f, 0.f, 0.f);
-      w.x = sgd_step(G.x, w.x, bb.x, mom, lr, mu, wd);
-      w.y = sgd_step(G.y, w.y, bb.y, mom, lr, mu, wd);
-      w.z = sgd_step(G.z, w.z, bb.z, mom, lr, mu, wd);
-      w.w = sgd_step(G.w, w.w, bb.w, mom, lr, mu, wd);
+      if (lapply) {
+        const float rate = (float)lars.rate[t0];
+        w.x = lars_step(G.x, w.x, bb.x, mom, rate, mu, lars.eps);
+        w.y = lars_step(G.y, w.y, bb.y, mom, rate, mu, lars.eps);
+        w.z = lars_step(G.z, w.z, bb.z, mom, rate, mu, lars.eps);
+        w.w = lars_step(G.w, w.w, bb.w, mom, rate, mu, lars.eps);
+      } else {
+        w.x = sgd_step(G.x, w.x, bb.x, mom, lr, mu, wd);
+        w.y = sgd_step(G.y, w.y, bb.y, mom, lr, mu, wd);
+        w.z = sgd_step(G.z, w.z, bb.z, mom, lr, mu, wd);
+        w.w = sgd_step(G.w, w.w, bb.w, mom, lr, mu, wd);
+      }
       store_nt4(w4 + v, w);
       if (mom) store_nt4(b4 + v, bb);
     }
@@ -1601,6 +1692,11 @@ __global__ __launch_bounds__(kUBlock) void k_update(
     gfloat* __restrict__ bm = mom ? gptr(tt.b + (a - tt.goff)) : nullptr;
     const bool vec = ((reinterpret_cast<uintptr_t>(w) |
                        (bm ? reinterpret_cast<uintptr_t>(bm) : 0u)) & 15u) == 0;
+    const float rate = lapply ? (float)lars.rate[ti] : 0.0f;
+    auto step = [&](float G, float wq, float& bq) -> float {
+      return lapply ? lars_step(G, wq, bq, mom, rate, mu, lars.eps)
+                    : sgd_step(G, wq, bq, mom, lr, mu, wd);
+    };
     int done = 0;
     if (vec) {
       const int nv = cnt >> 2;
@@ -1617,7 +1713,7 @@ __global__ __launch_bounds__(kUBlock) void k_update(
         float wq[4] = {wv4.x, wv4.y, wv4.z, wv4.w}, bq[4] = {bv4.x, bv4.y, bv4.z, bv4.w};
         const int l = la + 4 * q;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) wq[c] = sgd_step(acc[l + c], wq[c], bq[c], mom, lr, mu, wd);
+        for (int c = 0; c < 4; ++c) wq[c] = step(acc[l + c], wq[c], bq[c]);
         w4[q] = v4f{wq[0], wq[1], wq[2], wq[3]};
         if (mom) b4[q] = v4f{bq[0], bq[1], bq[2], bq[3]};
       }
@@ -1629,9 +1725,83 @@ __global__ __launch_bounds__(kUBlock) void k_update(
         continue;
       }
       float bq = mom ? bm[q] : 0.0f;
-      w[q] = sgd_step(acc[la + q], w[q], bq, mom, lr, mu, wd);
+      w[q] = step(acc[la + q], w[q], bq);
       if (mom) bm[q] = bq;
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LARS rates from dense gradients (the layer-wise rates of Eq. lars computed
+// for a list of layers): per update tile and tensor, the sums of w^2 and g^2.
+__global__ __launch_bounds__(kUBlock) void k_lars_norm_dense(
+    const UpdTensor* __restrict__ tens, const float* const* __restrict__ gptrs,
+    const int32_t* __restrict__ tile_first, int32_t ntens, int32_t d, int32_t ntiles_u,
+    int32_t per_xcd, double2* __restrict__ part, const int32_t* __restrict__ tpair) {
+  __shared__ double lred[2 * kUBlock / 64];
+  const int tid = threadIdx.x;
+  const int u = (int)(blockIdx.x % kXcds) * per_xcd + (int)(blockIdx.x / kXcds);
+  if (u >= ntiles_u) return;
+  const int32_t base = u << kUShift;
+  const int32_t len = min(kUTile, d - base);
+  const int32_t t0 = tile_first[u], tl = min(tile_first[u + 1], ntens - 1);
+  for (int ti = t0; ti <= tl; ++ti) {
+    const UpdTensor tt = tens[ti];
+    const int64_t a = max((int64_t)base, tt.goff);
+    const int64_t z = min((int64_t)base + len, tt.goff + tt.n);
+    if (z <= a) continue;
+    const gfloat* w = gptr(tt.w + (a - tt.goff));
+    const gfloat* g = gptr(gptrs[ti] + (a - tt.goff));
+    const int cnt = (int)(z - a);
+    double sw = 0.0, sg = 0.0;
+    const bool vec = ((reinterpret_cast<uintptr_t>(w) | reinterpret_cast<uintptr_t>(g)) & 15u) == 0;
+    int done = 0;
+    if (vec) {
+      const int nv = cnt >> 2;
+      const gv4f* w4 = (const gv4f*)w;
+      const gv4f* g4 = (const gv4f*)g;
+      for (int q = tid; q < nv; q += kUBlock) {
+        const v4f x = __builtin_nontemporal_load(w4 + q);
+        const v4f y = __builtin_nontemporal_load(g4 + q);
+        sw += (double)x.x * x.x + (double)x.y * x.y + (double)x.z * x.z + (double)x.w * x.w;
+        sg += (double)y.x * y.x + (double)y.y * y.y + (double)y.z * y.z + (double)y.w * y.w;
+      }
+      done = nv << 2;
+    }
+    for (int q = done + tid; q < cnt; q += kUBlock) {
+      const double x = w[q], y = g[q];
+      sw += x * x;
+      sg += y * y;
+    }
+    const double2 r = ublock_sum2(sw, sg, lred);
+    if (tid == 0) part[tpair[ti] + (u - (int32_t)(tt.goff >> kUShift))] = r;
+  }
+}
+
+// One workgroup per tensor: its pairs summed in a fixed order, the norms,
+// and the rate gamma eta ||w|| / (||g|| + eps ||w||) (gamma eta when either
+// norm is zero).
+__global__ __launch_bounds__(kUBlock) void k_lars_rates(const int32_t* __restrict__ tpair,
+                                                        const double2* __restrict__ part,
+                                                        double gamma, double eta, double eps,
+                                                        double* __restrict__ rate,
+                                                        double* __restrict__ rate_out) {
+  __shared__ double lred[2 * kUBlock / 64];
+  const int t = blockIdx.x, tid = threadIdx.x;
+  const int32_t pb = tpair[t], pe = tpair[t + 1];
+  double sw = 0.0, sg = 0.0;
+  for (int32_t i = pb + tid; i < pe; i += kUBlock) {
+    const double2 v = part[i];
+    sw += v.x;
+    sg += v.y;
+  }
+  const double2 r = ublock_sum2(sw, sg, lred);
+  if (tid == 0) {
+    const double nw = sqrt(r.x), ng = sqrt(r.y);
+    const double lam = (nw > 0.0 && ng > 0.0) ? (gamma * eta * nw) / (ng + eps * nw)
+                                               : gamma * eta;
+    rate[t] = lam;
+    if (rate_out) rate_out[t] = lam;
   }
 }
 
@@ -2364,11 +2534,28 @@ hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32
                          int32_t d, int32_t ntiles_u, const int32_t* idx, const void* val,
                          int val16, int64_t stride, const int32_t* nnz, int32_t P,
                          const int32_t* seg, float lr, float mu, float wd, int op, int has_mom,
-                         hipStream_t s, const Ev& ev) {
+                         const LarsArgs& lars, hipStream_t s, const Ev& ev) {
   const int32_t per_xcd = (ntiles_u + kXcds - 1) / kXcds;
-  return launch(k_update, dim3(per_xcd * kXcds), dim3(kUBlock), s, ev, tens, tile_first, ntens, d,
-                ntiles_u, per_xcd, idx, val, val16, stride, nnz, P, seg, lr, mu, wd, op,
-                has_mom);
+  const bool is_lars = op == kOpLarsNorm || op == kOpLarsApply;
+  return launch(is_lars ? k_update<true> : k_update<false>, dim3(per_xcd * kXcds), dim3(kUBlock),
+                s, ev, tens, tile_first, ntens, d, ntiles_u, per_xcd, idx, val, val16, stride, nnz,
+                P, seg, lr, mu, wd, op, has_mom, lars);
+}
+
+hipError_t launch_lars_norm_dense(const UpdTensor* tens, const float* const* gptrs,
+                                  const int32_t* tile_first, int32_t ntens, int32_t d,
+                                  int32_t ntiles_u, double2* part, const int32_t* tpair,
+                                  hipStream_t s, const Ev& ev) {
+  const int32_t per_xcd = (ntiles_u + kXcds - 1) / kXcds;
+  return launch(k_lars_norm_dense, dim3(per_xcd * kXcds), dim3(kUBlock), s, ev, tens, gptrs,
+                tile_first, ntens, d, ntiles_u, per_xcd, part, tpair);
+}
+
+hipError_t launch_lars_rates(const int32_t* tpair, const double2* part, int32_t ntens,
+                             double gamma, double eta, double eps, double* rate,
+                             double* rate_out, hipStream_t s, const Ev& ev) {
+  return launch(k_lars_rates, dim3(ntens), dim3(kUBlock), s, ev, tpair, part, gamma, eta, eps,
+                rate, rate_out);
 }
 
 }  // namespace tkef

@@ -175,3 +175,29 @@ def test_approx_plan_host_side():
     P = ctypes.c_void_p
     assert L.tkef_sparsify_approx_result(g._h, P(0x10000), None, None, None) == tk.EINVAL
     assert L.tkef_sparsify_approx_result(h, P(0x10000), None, None, None) == tk.ESTATE
+
+
+def test_lars_host_side():
+    """LARS entry points: the errors the host can see (no GPU needed)."""
+    L = tk.lib()
+    p = tk.UpdatePlan([100, 5000], P=2, stride=10)
+    h = p._h
+    P_ = ctypes.c_void_p
+    ws = P_(0x10000)
+    assert L.tkef_lars_update_execute(None, None, None, None, 1.0, 1.0, 0.0, 0.0, None, ws,
+                                      10**9, None, None) == tk.EINVAL
+    assert L.tkef_lars_update_execute(h, P_(0x100), P_(0x200), None, float("nan"), 1.0, 0.0,
+                                      0.0, None, ws, 10**9, None, None) == tk.ERANGE
+    assert L.tkef_lars_update_execute(h, P_(0x100), P_(0x200), None, 1.0, 1.0, 0.0, 0.0, None,
+                                      ws, 10**9, None, None) == tk.ESTATE
+    assert L.tkef_lars_update_execute(h, P_(0x100), P_(0x200), None, 1.0, 1.0, 0.0, 0.0, None,
+                                      None, 10**9, None, None) == tk.EWORKSPACE
+    g = (P_ * 2)(P_(0x1000), P_(0x2000))
+    assert L.tkef_update_plan_bind_grads(h, g, ws, 10**9, None) == tk.ESTATE
+    assert L.tkef_update_plan_bind_grads(h, None, ws, 10**9, None) == tk.EINVAL
+    assert L.tkef_lars_rates_execute(h, 1.0, 1.0, 0.0, P_(0x3000), ws, 10**9, None) == tk.ESTATE
+    assert L.tkef_lars_rates_execute(h, 1.0, float("inf"), 0.0, P_(0x3000), ws, 10**9,
+                                     None) == tk.ERANGE
+    names = [L.tkef_lars_launch_name(0, i).decode() for i in range(4)]
+    assert names == tk.LARS_LAUNCHES and L.tkef_lars_launch_name(0, 4) is None
+    assert [L.tkef_lars_launch_name(1, i).decode() for i in range(2)] == tk.LARS_DENSE_LAUNCHES
