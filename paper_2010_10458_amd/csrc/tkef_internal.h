@@ -29,7 +29,7 @@ constexpr int kH2Bins = 1024, kH2Shift = 10;
 constexpr int kH3Bins = 1024;
 // copies of the level-1 histogram (the stream's workgroups add into copy
 // blockIdx % copies): one global selection, per-tensor selections
-constexpr int kSlotsOne = 16, kSlotsMany = 4;
+constexpr int kSlotsOne = 4, kSlotsMany = 4;
 
 struct TileDesc {        // 32 B, one per tile, written at bind
   const float* g;        // gradient, first element of the tile
