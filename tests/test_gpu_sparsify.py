@@ -314,3 +314,19 @@ def test_bert_large_340m_tie_stressed():
     x = xs
     rng = np.random.default_rng(800)
     _sampled_ranks(x, idx, k, rng, nsamp=3)
+
+
+@pytest.mark.parametrize("mode", [tk.GLOBAL, tk.PER_TENSOR])
+def test_ragged_list_between_one_and_two_units_per_workgroup(mode):
+    """A ragged list of 2.8 M elements (1,025 to 2,048 stream units: some
+    workgroups of the stream take two units, others one), global and per
+    tensor, where a workgroup's units can belong to different tensors."""
+    rng = np.random.default_rng(700 + mode)
+    sizes = [2_500_000, 777, 8193, 1, 300_000]
+    grads = [rng.standard_normal(n).astype(np.float32) for n in sizes]
+    res = [(rng.standard_normal(n) * 0.1).astype(np.float32) for n in sizes]
+    units = sum(-(-n // 8192) for n in sizes) * 4
+    assert 1024 < units <= 2048
+    compare_with_oracle(grads, res, rho=0.001, mode=mode, label="2.8 M ragged")
+    if mode == tk.GLOBAL:
+        compare_with_oracle(grads, res, k=250_000, label="2.8 M ragged, large k")
