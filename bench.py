@@ -46,6 +46,13 @@ def parse_args():
     ap.add_argument("--replicas", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip timing the CPU oracle")
+    ap.add_argument("--workload", default="resnet50",
+                    choices=["resnet50", "c1", "transformer", "bert"],
+                    help="resnet50: the headline step (default); c1: one 1 M-element tensor, "
+                         "rho 0.001, then a one-worker plain update; transformer: the 110 M "
+                         "Transformer-shaped set, Laplace(0, 1e-3), rho 0.001 and 0.01, global "
+                         "and per tensor; bert: one 340 M-element tie-stressed buffer, rho 0.001 "
+                         "(these three print sparsify rates only, no extras)")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the variant paths timed after the step (fp16 values, dense "
                          "aggregation, shard-shaped sparsify)")
@@ -299,6 +306,129 @@ def extras(args, tk, gen, sizes, d, bank, resid, idx_all, val_all, nnz, k_total,
     return ex
 
 
+def time_sparsify(tk, plans, K, W, make_events, idx_out=None, val_out=None):
+    """Mean total and per-kernel times (ms) of plans[i % len(plans)].execute()."""
+    import numpy as np
+    import torch
+    names = plans[0].launch_names()
+    for i in range(W):
+        plans[i % len(plans)].execute(idx_out, val_out)
+    evs = [make_events(len(names) + 1) for _ in range(K)]
+    torch.cuda.synchronize()
+    for t in range(K):
+        pl = plans[(W + t) % len(plans)]
+        pl.set_events(evs[t])
+        pl.execute(idx_out, val_out)
+        pl.set_events(None)
+    torch.cuda.synchronize()
+    total = float(np.mean([e[0].elapsed_time(e[-1]) for e in evs]))
+    kern = {n: round(float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs])) * 1e3, 2)
+            for i, n in enumerate(names)}
+    return total, kern
+
+
+def other_workload(args) -> int:
+    """The other configurations: sparsify rates (and, for c1, the one-worker
+    plain update), inputs resident, rotating buffers larger than the last-
+    level cache."""
+    import numpy as np
+    import torch
+
+    import gen
+    import paper_2010_10458_amd as tk
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    K, W = args.steps, args.warmup
+
+    def make_events(n):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in evs:
+            e.record()
+        return evs
+
+    def line(metric_value, d, ms, kern, workload, extra):
+        frac = (12 * d) / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS
+        out = {"metric": METRIC, "value": round(metric_value, 3), "unit": "Gelem/s", "n_gpus": 1,
+               "steps": K, "warmup": W, "ms_per_step": round(ms, 4), "higher_is_better": True,
+               "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+               "config": {"workload": workload, "d": d}, "sparsify_us": round(ms * 1e3, 2),
+               "sparsify_frac_hbm_peak": round(frac, 4), "kernels_us": kern}
+        out.update(extra)
+        print(json.dumps(out), flush=True)
+
+    if args.workload == "c1":
+        d = gen.C1_D
+        R = 64   # 64 x (g, r, w) of 4 MB: more than the 256 MB last-level cache
+        gs = [[torch.from_numpy(gen.flat_normal(d, config=1, step=j % 4)).to(dev)] for j in range(R)]
+        rs = [[torch.zeros(d, device=dev)] for _ in range(R)]
+        ws = [[torch.from_numpy(gen.params_like([d], config=1)[0]).to(dev)] for _ in range(R)]
+        sps = [tk.SparsifyPlan([d], rho=RHO).bind(gs[j], rs[j]) for j in range(R)]
+        k = sps[0].k_total
+        ups = [tk.UpdatePlan([d], P=1, stride=k).bind(ws[j]) for j in range(R)]
+        idx = [torch.empty(k, dtype=torch.int32, device=dev) for _ in range(R)]
+        val = [torch.empty(k, device=dev) for _ in range(R)]
+        n_sp, n_up = len(sps[0].launch_names()), len(ups[0].launch_names())
+        for i in range(W):
+            sps[i % R].execute(idx[i % R], val[i % R])
+            ups[i % R].execute(idx[i % R], val[i % R], lr=0.1)
+        e_sp = [make_events(n_sp + 1) for _ in range(K)]
+        e_up = [make_events(n_up + 1) for _ in range(K)]
+        torch.cuda.synchronize()
+        for t in range(K):
+            j = (W + t) % R
+            sps[j].set_events(e_sp[t])
+            sps[j].execute(idx[j], val[j])
+            sps[j].set_events(None)
+            ups[j].set_events(e_up[t])
+            ups[j].execute(idx[j], val[j], lr=0.1)
+            ups[j].set_events(None)
+        torch.cuda.synchronize()
+        sp_ms = float(np.mean([e[0].elapsed_time(e[-1]) for e in e_sp]))
+        up_ms = float(np.mean([e[0].elapsed_time(e[-1]) for e in e_up]))
+        kern = {n: round(float(np.mean([e[i].elapsed_time(e[i + 1]) for e in e_sp])) * 1e3, 2)
+                for i, n in enumerate(sps[0].launch_names())}
+        line(d / (sp_ms / 1e3) / 1e9, d, sp_ms, kern,
+             "single fp32 tensor d=1048576, N(0,1), residual zero, rho=0.001 (k=1049); then a "
+             "one-worker plain SGD update, lr 0.1", {"k": k, "update_us": round(up_ms * 1e3, 2)})
+        return 0
+
+    if args.workload == "transformer":
+        sizes = gen.numels(gen.transformer_shapes())
+        d = sum(sizes)
+        bank = [[torch.from_numpy(a).to(dev) for a in gen.laplace_grads(s, sizes)] for s in range(2)]
+        resid = [[torch.zeros(n, device=dev) for n in sizes] for _ in range(2)]
+        res = {}
+        for mode, mname in ((tk.GLOBAL, "global"), (tk.PER_TENSOR, "per_tensor")):
+            for rho in (0.001, 0.01):
+                plans = [tk.SparsifyPlan(sizes, mode=mode, rho=rho).bind(bank[s], resid[j])
+                         for s in range(2) for j in range(2)]
+                ms, kern = time_sparsify(tk, plans, K, W, make_events)
+                res[f"{mname}_rho{rho}"] = {"k": plans[0].k_total, "sparsify_us": round(ms * 1e3, 2),
+                                            "Gelem_per_s": round(d / (ms / 1e3) / 1e9, 2),
+                                            "frac_hbm_peak": round((12 * d + 8 * plans[0].k_total) / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
+                                            "kernels_us": kern}
+                del plans
+        head = res["global_rho0.001"]
+        line(head["Gelem_per_s"], d, head["sparsify_us"] / 1e3, head["kernels_us"],
+             "transformer-base-shaped set: 261 fp32 tensors, d=109708544, Laplace(0, 1e-3); rho "
+             "0.001 and 0.01, global and per-tensor top-k", {"variants": res})
+        return 0
+
+    # bert: one 340 M-element buffer with exact-duplicate magnitudes
+    d = gen.BERT_LARGE_D
+    log("generating the 340 M-element tie-stressed buffer")
+    g = [torch.from_numpy(gen.tie_stressed(d)).to(dev)]
+    resid = [[torch.zeros(d, device=dev)] for _ in range(2)]
+    plans = [tk.SparsifyPlan([d], rho=RHO).bind(g, resid[j]) for j in range(2)]
+    ms, kern = time_sparsify(tk, plans, K, W, make_events)
+    line(d / (ms / 1e3) / 1e9, d, ms, kern,
+         "bert-large-sized flat fp32 buffer d=340000000, N(0,1) with 10% bfloat16-truncated "
+         "exact-duplicate magnitudes and a tie class at the rho=0.001 boundary",
+         {"k": plans[0].k_total})
+    return 0
+
+
 def main() -> int:
     args = parse_args()
     if args.probe_copy:
@@ -307,6 +437,8 @@ def main() -> int:
         print(f"bench.py measures one GPU only (this build has no multi-GPU path); "
               f"got --gpus {args.gpus}", file=sys.stderr)
         return 2
+    if args.workload != "resnet50":
+        return other_workload(args)
     import numpy as np
     import torch
 

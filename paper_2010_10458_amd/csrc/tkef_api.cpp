@@ -126,7 +126,7 @@ struct tkef_sparsify_plan_s {
   size_t off_tiles = 0, off_groups = 0, off_state = 0, off_zero[2] = {0, 0}, zero_bytes = 0,
          off_hist1 = 0, off_hist2 = 0, off_hist3 = 0, off_flags1 = 0, off_flags2 = 0,
          off_meta = 0, off_summ = 0, off_base = 0, off_cand = 0, off_rcand = 0, off_rband = 0,
-         off_rsuf = 0, off_rcnt = 0, off_rbin = 0, ws_bytes = 0;
+         off_rsuf = 0, off_rcnt = 0, off_rbin = 0, off_rbtmp = 0, ws_bytes = 0;
   int32_t val_format = TKEF_VAL_F32;  // value array written by execute
   // MSTopK (TKEF_APPROX): rounds, offset word, scratch
   int32_t ms_rounds = 30;
@@ -272,6 +272,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
       const size_t slots = (size_t)p->sel_grid * p->rcap;
       p->off_rcand = o;  o = align_up(o + slots * 16);
       p->off_rband = o;  o = align_up(o + slots * 4);
+      p->off_rbtmp = o;  o = align_up(o + slots * 4);
       p->off_rsuf = o;   o = align_up(o + (size_t)p->sel_grid * kH2Bins * 4);
       p->off_rcnt = o;   o = align_up(o + (size_t)p->sel_grid * 8);
       p->off_rbin = o;   o = align_up(o + (size_t)kH2Bins * p->sel_grid * kPerBin * 4);
@@ -498,12 +499,13 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   if (ng == 1) {
     uint32_t* rcand = reinterpret_cast<uint32_t*>(base + plan->off_rcand);
     uint32_t* rband = reinterpret_cast<uint32_t*>(base + plan->off_rband);
+    uint32_t* rbtmp = reinterpret_cast<uint32_t*>(base + plan->off_rbtmp);
     uint32_t* rsuf = reinterpret_cast<uint32_t*>(base + plan->off_rsuf);
     uint32_t* rcnt = reinterpret_cast<uint32_t*>(base + plan->off_rcnt);
     uint32_t* rbin = reinterpret_cast<uint32_t*>(base + plan->off_rbin);
     if (e == hipSuccess)
       e = launch_collect(tiles, groups, st, hist1, plan->nslots, summ, nl, lpt, sg, plan->rcap,
-                         hist2, rbin, rcand, rband, rsuf, rcnt, s, tr.at(li++));
+                         hist2, rbin, rcand, rband, rbtmp, rsuf, rcnt, s, tr.at(li++));
     if (e == hipSuccess)
       e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, plan->rcap, hist2, rbin, rcand,
                         rband, rsuf, rcnt, idx_out, val_out, val16, clear_next, clear_words, s,

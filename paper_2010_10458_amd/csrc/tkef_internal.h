@@ -117,8 +117,8 @@ constexpr int kPerBin = 4;  // band keys per (level-2 bin, region) kept in the r
 hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
                           const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
                           int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* rbin,
-                          uint32_t* rcand, uint32_t* rband, uint32_t* rsuf, uint32_t* rcnt,
-                          hipStream_t s, const Ev& ev);
+                          uint32_t* rcand, uint32_t* rband, uint32_t* rbtmp, uint32_t* rsuf,
+                          uint32_t* rcnt, hipStream_t s, const Ev& ev);
 hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
                          int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,

@@ -700,8 +700,9 @@ __device__ __forceinline__ void walk_cands(const TileDesc* __restrict__ tiles, i
 //                band members | (band not stored) << 31}, counts exact;
 //   hist2       += the region's level-2 histogram.
 // A region with more than rcap candidates leaves rcand incomplete; one with
-// more than kBandCap band members stores no band keys (rband, rbin). finish
-// then reads that region's lines instead.
+// more than kBandCap band members keeps the rest in rbtmp[w] (global
+// scratch) until they are placed; one with more than rcap stores no band keys
+// (rband, rbin), and finish then reads that region's lines instead.
 //
 // finish makes the level-2 pick (bin B2) from hist2, builds the level-3
 // histogram in LDS from the band members in bin B2 of all regions (from rbin
@@ -726,8 +727,8 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
     GroupState* __restrict__ st, const uint32_t* __restrict__ hist1,
     const uint16_t* __restrict__ summ, uint32_t* __restrict__ hist2,
     uint32_t* __restrict__ rbin, uint4* __restrict__ rcand, uint32_t* __restrict__ rband,
-    uint32_t* __restrict__ rsuf, uint2* __restrict__ rcnt, uint32_t rcap, int lpt,
-    int64_t nlines) {
+    uint32_t* __restrict__ rbtmp, uint32_t* __restrict__ rsuf, uint2* __restrict__ rcnt,
+    uint32_t rcap, int lpt, int64_t nlines) {
   static_assert(kH2Bins == kSBlock, "one level-2 bin per thread");
   __shared__ uint32_t h[kH2Bins];
   __shared__ uint32_t hoff[kH2Bins];
@@ -795,12 +796,22 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
           hm |= (j < n && key >= lo) ? (1u << j) : 0u;
           bm |= (j < n && (key >> kH1Shift) == B1) ? (1u << j) : 0u;
         }
+      }
+      {
+        // band slots: one atomic per wavefront, shared out by a wave scan
+        const uint32_t bc = (uint32_t)__popc(bm);
+        const uint32_t incl = wave_incl_scan(bc);
+        const uint32_t wtot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+        uint32_t wbase = 0u;
+        if ((tid & 63) == 63 && wtot) wbase = atomicAdd(&nband, wtot);
+        wbase = (uint32_t)__builtin_amdgcn_readlane((int)wbase, 63);
+        uint32_t slot = wbase + incl - bc;
 #pragma unroll 1
-        for (uint32_t m2 = bm; m2; m2 &= m2 - 1u) {
+        for (uint32_t m2 = bm; m2; m2 &= m2 - 1u, ++slot) {
           const uint32_t key = mag_key(pick_elem(v, __ffs(m2) - 1));
           atomicAdd(&h[(key >> kH2Shift) & (kH2Bins - 1)], 1u);
-          const uint32_t slot = atomicAdd(&nband, 1u);
           if (slot < (uint32_t)kBandCap) bandk[slot] = key;
+          else if (slot < rcap) rbtmp[(size_t)w * rcap + slot] = key;
         }
       }
       uint32_t tot;
@@ -829,23 +840,27 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
   const uint32_t cb = h[bin];
   uint32_t bw;
   const uint32_t above = sblock_scan(cb, wsum, &bw);
-  const bool band_ok = bw <= (uint32_t)kBandCap;  // every band key is in bandk
+  const bool band_ok = bw <= rcap;  // the band fits rband[w] (and rbtmp[w])
   h[bin] = above;     // from here on: the bin's next slot in rband[w]
   hoff[bin] = above;  // the bin's first slot
   __syncthreads();
   // (global stores after the last barrier: a barrier waits for them)
   if (cb) atomicAdd(&hist2[bin], cb);
   if (bw) rsuf[(size_t)w * kH2Bins + bin] = above;
+  uint32_t* __restrict__ dst = rband + (size_t)w * rcap;
+  auto place = [&](uint32_t key) {
+    const uint32_t b2 = (key >> kH2Shift) & (kH2Bins - 1);
+    const uint32_t slot = atomicAdd(&h[b2], 1u);
+    dst[slot] = key;
+    const uint32_t rank = slot - hoff[b2];
+    if (rank < (uint32_t)kPerBin) rbin[((size_t)b2 * gridDim.x + w) * kPerBin + rank] = key;
+  };
   if (band_ok) {
-    uint32_t* __restrict__ dst = rband + (size_t)w * rcap;
-    for (uint32_t j = tid; j < bw; j += kSBlock) {
-      const uint32_t key = bandk[j];
-      const uint32_t b2 = (key >> kH2Shift) & (kH2Bins - 1);
-      const uint32_t slot = atomicAdd(&h[b2], 1u);
-      dst[slot] = key;
-      const uint32_t rank = slot - hoff[b2];
-      if (rank < (uint32_t)kPerBin) rbin[((size_t)b2 * gridDim.x + w) * kPerBin + rank] = key;
-    }
+    // the first kBandCap from LDS, the rest (a dense selection) from the
+    // region's scratch in rbtmp, written before the barriers above
+    const uint32_t* __restrict__ tmp = rbtmp + (size_t)w * rcap;
+    for (uint32_t j = tid; j < bw; j += kSBlock)
+      place(j < (uint32_t)kBandCap ? bandk[j] : tmp[j]);
   }
   if (tid == 0)
     rcnt[w] = make_uint2(cw | ((fits ? 0u : 1u) << 31), bw | ((band_ok ? 0u : 1u) << 31));
@@ -1094,9 +1109,19 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   if (own_ov) {
     walk_mask(ls, mask, at_least_T,
               [&](int, const TileDesc&, int, float x, uint32_t) { count(x); });
-  } else {
+  } else if (cb < ce) {
+    // the run of candidates: the first was fetched at the start, the rest
+    // (dense selections) four loads in flight at a time (clamped indices)
+    count(__uint_as_float(v0.y));
 #pragma unroll 1
-    for (uint32_t j = cb; j < ce; ++j) count(__uint_as_float(((j == cb) ? v0 : mc[j]).y));
+    for (uint32_t j = cb + 1; j < ce; j += 4) {
+      uint4 q[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) q[c] = mc[min(j + (uint32_t)c, ce - 1u)];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (j + (uint32_t)c < ce) count(__uint_as_float(q[c].y));
+    }
   }
   const uint32_t sv[4] = {gt, eq, gtb, eqb};
   uint32_t pre[4], tot[4];
@@ -1131,11 +1156,19 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
     walk_mask(ls, mask, at_least_T, [&](int, const TileDesc& t, int e, float x, uint32_t) {
       write((uint32_t)(t.gstart + e), t.r + e, x);
     });
-  } else {
-#pragma unroll 1
-    for (uint32_t j = cb; j < ce; ++j) {
-      const uint4 v = (j == cb) ? v0 : mc[j];
+  } else if (cb < ce) {
+    auto write_c = [&](const uint4& v) {
       write(v.x, reinterpret_cast<float*>(((uint64_t)v.w << 32) | v.z), __uint_as_float(v.y));
+    };
+    write_c(v0);
+#pragma unroll 1
+    for (uint32_t j = cb + 1; j < ce; j += 4) {
+      uint4 q[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) q[c] = mc[min(j + (uint32_t)c, ce - 1u)];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (j + (uint32_t)c < ce) write_c(q[c]);
     }
   }
 }
@@ -2426,11 +2459,11 @@ hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
 hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
                           const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
                           int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* rbin,
-                          uint32_t* rcand, uint32_t* rband, uint32_t* rsuf, uint32_t* rcnt,
-                          hipStream_t s, const Ev& ev) {
+                          uint32_t* rcand, uint32_t* rband, uint32_t* rbtmp, uint32_t* rsuf,
+                          uint32_t* rcnt, hipStream_t s, const Ev& ev) {
   if (nslots != kSlotsOne) return hipErrorInvalidValue;
   return launch(k_collect, dim3(grid), dim3(kSBlock), s, ev, tiles, groups, st, hist1, summ,
-                hist2, rbin, reinterpret_cast<uint4*>(rcand), rband, rsuf,
+                hist2, rbin, reinterpret_cast<uint4*>(rcand), rband, rbtmp, rsuf,
                 reinterpret_cast<uint2*>(rcnt), rcap, lpt, nlines);
 }
 

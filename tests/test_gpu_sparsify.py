@@ -330,3 +330,16 @@ def test_ragged_list_between_one_and_two_units_per_workgroup(mode):
     compare_with_oracle(grads, res, rho=0.001, mode=mode, label="2.8 M ragged")
     if mode == tk.GLOBAL:
         compare_with_oracle(grads, res, k=250_000, label="2.8 M ragged, large k")
+
+
+@pytest.mark.parametrize("rho", [0.01, 0.05])
+def test_dense_selection_band_beyond_lds(rho):
+    """A dense selection on 10 M N(0, 1) elements: at rho = 0.05 a region of
+    the global selection holds about 8 K members of the threshold's level-1
+    bin, more than its workgroup keeps in LDS, so they are placed from a
+    second read of its lines."""
+    rng = np.random.default_rng(int(rho * 1000))
+    n = 10_000_000
+    g = rng.standard_normal(n).astype(np.float32)
+    r = (rng.standard_normal(n) * 0.01).astype(np.float32)
+    compare_with_oracle([g], [r], rho=rho, label=f"dense rho={rho}")
