@@ -278,8 +278,9 @@ int tkef_sparse_aggregate(float *const *outs, const int64_t *numels, int32_t nte
  *
  * A layer is one tensor of the update plan's list. Norms are Euclidean, summed
  * in double (in a fixed order: the same inputs give the same rates on every
- * run); when ||w_l|| or ||g_l|| is zero the rate is gamma * eta. The step, in
- * binary32 with the rate rounded to binary32 once, for every position:
+ * run); when ||w_l|| or ||g_l|| is zero the rate is gamma * eta (gamma, eta
+ * and eps enter the rate in double). The step, in binary32 with the rate and
+ * eps each rounded to binary32 once, for every position:
  *   D = g + eps * w;  U = rate * D;
  *   with momentum (mu != 0, momentum bound):  b = mu * b + U;  w = w - b
  *   without:                                  w = w - U
