@@ -631,8 +631,8 @@ struct LineSpan {
 
 // For every element of the flagged lines in `mask`, in position order, for
 // which hit(group, key) holds: f(tile, TileDesc, e, x, key). The hit test runs
-// over all 32 elements of a line at once; the (few) hits are then visited one
-// by one, re-reading the element from the line just loaded.
+// over all 32 elements of a line at once; the hits are then visited one by
+// one, each taken from the line already in registers.
 template <typename Hit, typename F>
 __device__ __forceinline__ void walk_mask(const LineSpan& ls, uint32_t mask, Hit hit, F f) {
 #pragma unroll 1
@@ -652,7 +652,7 @@ __device__ __forceinline__ void walk_mask(const LineSpan& ls, uint32_t mask, Hit
     while (hm) {
       const int j = __ffs(hm) - 1;
       hm &= hm - 1u;
-      const float x = gptr(t.r)[e0 + j];
+      const float x = pick_elem(v, j);
       f(tile, t, e0 + j, x, mag_key(x));
     }
   }
