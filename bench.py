@@ -397,10 +397,11 @@ def other_workload(args) -> int:
         sizes = gen.numels(gen.transformer_shapes())
         d = sum(sizes)
         bank = [[torch.from_numpy(a).to(dev) for a in gen.laplace_grads(s, sizes)] for s in range(2)]
-        resid = [[torch.zeros(n, device=dev) for n in sizes] for _ in range(2)]
         res = {}
         for mode, mname in ((tk.GLOBAL, "global"), (tk.PER_TENSOR, "per_tensor")):
             for rho in (0.001, 0.01):
+                # fresh residuals per configuration (each carries its own error feedback)
+                resid = [[torch.zeros(n, device=dev) for n in sizes] for _ in range(2)]
                 plans = [tk.SparsifyPlan(sizes, mode=mode, rho=rho).bind(bank[s], resid[j])
                          for s in range(2) for j in range(2)]
                 ms, kern = time_sparsify(tk, plans, K, W, make_events)
@@ -408,7 +409,7 @@ def other_workload(args) -> int:
                                             "Gelem_per_s": round(d / (ms / 1e3) / 1e9, 2),
                                             "frac_hbm_peak": round((12 * d + 8 * plans[0].k_total) / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4),
                                             "kernels_us": kern}
-                del plans
+                del plans, resid
         head = res["global_rho0.001"]
         line(head["Gelem_per_s"], d, head["sparsify_us"] / 1e3, head["kernels_us"],
              "transformer-base-shaped set: 261 fp32 tensors, d=109708544, Laplace(0, 1e-3); rho "

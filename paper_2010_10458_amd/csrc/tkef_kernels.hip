@@ -467,6 +467,7 @@ static_assert((1 << kCandShift) == kTile, "candidate encoding");
 constexpr uint64_t kFlagValid = 1ull << 63, kFlagVal = (1ull << 63) - 1;
 constexpr uint32_t kSpinLimit = 1u << 22;
 constexpr int kStage = 8;       // candidates a thread stages in LDS
+constexpr int kGStage = 32;     // ... in gather (dense per-tensor selections; 128 KB)
 
 __device__ __forceinline__ uint64_t flag_load(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1193,7 +1194,7 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
                                                     uint32_t* __restrict__ status) {
   __shared__ uint32_t wsum[2 * kSWaves];
   __shared__ uint64_t red[kSWaves];
-  __shared__ int32_t stage[kStage * kSBlock];  // [slot][thread]
+  __shared__ int32_t stage[kGStage * kSBlock];  // [slot][thread]
   const int tid = threadIdx.x;
   LineSpan ls;
   ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
@@ -1205,7 +1206,7 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
   auto is_cand = [&](int g, uint32_t k) -> bool { return k >= (b1_of(g) << kH1Shift); };
   uint32_t c = 0u;
   walk_mask(ls, mask, is_cand, [&](int tile, const TileDesc& t, int e, float, uint32_t k) {
-    if (c < (uint32_t)kStage)
+    if (c < (uint32_t)kGStage)
       stage[c * kSBlock + tid] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
     ++c;
     if ((k >> kH1Shift) == b1_of(t.group))
@@ -1223,13 +1224,13 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
   }
   if (fits && c) {
     const uint64_t pos = pre + ex;
-    const uint32_t ns = min(c, (uint32_t)kStage);
+    const uint32_t ns = min(c, (uint32_t)kGStage);
 #pragma unroll 1
     for (uint32_t q = 0; q < ns; ++q) cand[pos + q] = stage[q * kSBlock + tid];
-    if (c > (uint32_t)kStage) {  // rare: read the lines again for the rest
+    if (c > (uint32_t)kGStage) {  // rare: read the lines again for the rest
       uint32_t i = 0u;
       walk_mask(ls, mask, is_cand, [&](int tile, const TileDesc&, int e, float, uint32_t) {
-        if (i >= (uint32_t)kStage)
+        if (i >= (uint32_t)kGStage)
           cand[pos + i] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
         ++i;
       });
