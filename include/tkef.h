@@ -136,8 +136,8 @@ int tkef_sparsify_plan_set_value_format(tkef_sparsify_plan plan, int32_t format)
 
 /* MSTopK parameters of a TKEF_APPROX plan (Alg. 1). n_search: rounds of the
  * threshold bisection, 1..48 (the paper runs 30, which is the default; the
- * kernel count, 2 + ceil(n_search / 6), is reported by *_info after this
- * call). window_word: the 64-bit value the band offset is drawn from for the
+ * kernel count, 3 + ceil(max(0, n_search - 6) / 12), is reported by *_info
+ * after this call). window_word: the 64-bit value the band offset is drawn from for the
  * next executions: offset = window_word mod (band - (k - k1) + 1), so a
  * caller wanting the paper's random offset passes a fresh random word per
  * execution. Host only; TKEF_EINVAL for another mode or n_search outside

@@ -106,8 +106,18 @@ constexpr int32_t kSparsifyNLaunchOne = 3, kSparsifyNLaunchMany = 8;
 static const char* const kApproxRefine[] = {"ms_refine1", "ms_refine2", "ms_refine3",
                                             "ms_refine4", "ms_refine5", "ms_refine6",
                                             "ms_refine7"};
-constexpr int32_t kMsMaxPasses = (kMsMaxRounds + kMsRoundsPerPass - 1) / kMsRoundsPerPass;
+// passes for n rounds: six in the first, twelve in each later one
+constexpr int32_t ms_passes_for(int32_t n) {
+  return 1 + (n > kMsRoundsPerPass
+                  ? (n - kMsRoundsPerPass + kMsRoundsPerRefine - 1) / kMsRoundsPerRefine
+                  : 0);
+}
+constexpr int32_t kMsMaxPasses = ms_passes_for(kMsMaxRounds);
 static_assert(kMsMaxPasses - 1 <= 7, "refine names");
+// counters of the first pass (kMsSlots copies of 64), then one copy of
+// kMsRefineBins per later pass
+constexpr size_t kMsCntWords =
+    (size_t)kMsSlots * 64 + (size_t)(kMsMaxPasses - 1) * kMsRefineBins;
 
 struct tkef_sparsify_plan_s {
   int32_t ntensors = 0, mode = 0, ngroups = 0, ntiles = 0, nslots = 1, stream_grid = 1;
@@ -135,7 +145,7 @@ struct tkef_sparsify_plan_s {
          off_ms_flags = 0;  // state: kMsMaxPasses + 1 records, zeroed scratch: the rest
   uint64_t executions = 0;   // since the last bind
   bool needs_clear = true;   // both copies must be cleared before the next run
-  int32_t ms_passes() const { return (ms_rounds + kMsRoundsPerPass - 1) / kMsRoundsPerPass; }
+  int32_t ms_passes() const { return ms_passes_for(ms_rounds); }
   int32_t nlaunch() const {
     if (mode == TKEF_APPROX) return 2 + ms_passes();
     return ngroups == 1 ? kSparsifyNLaunchOne : kSparsifyNLaunchMany;
@@ -250,7 +260,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
       p->off_ms_state = o;  o = align_up(o + (size_t)(kMsMaxPasses + 1) * sizeof(MsState));
       p->off_ms_esum = z;   z = align_up(z + (size_t)kMsSlots * 256 * 8);
       p->off_ms_emax = z;   z = align_up(z + (size_t)kMsSlots * 4);
-      p->off_ms_cnt = z;    z = align_up(z + (size_t)kMsMaxPasses * kMsSlots * 64 * 4);
+      p->off_ms_cnt = z;    z = align_up(z + kMsCntWords * 4);
       p->off_ms_flags = z;  z = align_up(z + (size_t)p->sel_grid * 8);
     } else {
       p->off_hist1 = z;   z = align_up(z + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
@@ -470,21 +480,28 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     const uint32_t k = static_cast<uint32_t>(plan->k_total);
     const int32_t N = plan->ms_rounds, passes = plan->ms_passes();
     auto rounds_of = [&](int32_t b) {
-      return std::min(kMsRoundsPerPass, N - b * kMsRoundsPerPass);
+      return b == 0 ? std::min(kMsRoundsPerPass, N)
+                    : std::min(kMsRoundsPerRefine,
+                               N - kMsRoundsPerPass - (b - 1) * kMsRoundsPerRefine);
     };
-    auto cnt_of = [&](int32_t b) { return cnt + (size_t)b * kMsSlots * 64; };
+    auto cnt_of = [&](int32_t b) {
+      return b == 0 ? cnt : cnt + (size_t)kMsSlots * 64 + (size_t)(b - 1) * kMsRefineBins;
+    };
+    auto slots_of = [&](int32_t b) { return b == 0 ? kMsSlots : 1; };
+    auto bins_of = [&](int32_t b) { return b == 0 ? 64 : kMsRefineBins; };
     e = launch_ms_stream(tiles, nt, plan->stream_grid, kMsSlots, esum, emax, summ, s,
                          tr.at(li++));
     if (e == hipSuccess)
       e = launch_ms_count(tiles, nt, plan->count_grid, kMsSlots, esum, emax, summ, cnt_of(0),
                           ms, plan->d, status, s, tr.at(li++));
     for (int32_t b = 1; b < passes && e == hipSuccess; ++b)
-      e = launch_ms_refine(tiles, summ, nl, lpt, sg, kMsSlots, cnt_of(b - 1), cnt_of(b),
-                           ms + b - 1, ms + b, k, plan->d, rounds_of(b - 1), N, plan->ms_word, s,
-                           tr.at(li++));
+      e = launch_ms_refine(tiles, summ, nl, lpt, sg, slots_of(b - 1), bins_of(b - 1),
+                           cnt_of(b - 1), cnt_of(b), ms + b - 1, ms + b, k, plan->d,
+                           rounds_of(b - 1), N, plan->ms_word, s, tr.at(li++));
     if (e == hipSuccess)
-      e = launch_ms_emit(tiles, summ, nl, lpt, sg, kMsSlots, cnt_of(passes - 1),
-                         ms + passes - 1, ms + passes, k, plan->d, rounds_of(passes - 1), N,
+      e = launch_ms_emit(tiles, summ, nl, lpt, sg, slots_of(passes - 1), bins_of(passes - 1),
+                         cnt_of(passes - 1), ms + passes - 1, ms + passes, k, plan->d,
+                         rounds_of(passes - 1), N,
                          plan->ms_word, flags, idx_out, val_out, val16, status, clear_next,
                          clear_words, s, tr.at(li++));
     if (e != hipSuccess) {

@@ -66,8 +66,10 @@ struct MsState {
   uint32_t rand, take;   // window offset in the band, elements taken from it
   uint32_t level, bad;   // rounds done; non-finite input seen
 };
-constexpr int kMsRoundsPerPass = 6;   // 63 thresholds = six bisection rounds
-constexpr int kMsMaxRounds = 48;      // ratios stay exact dyadic doubles
+constexpr int kMsRoundsPerPass = 6;     // first pass: 63 thresholds = six bisection rounds
+constexpr int kMsRoundsPerRefine = 12;  // later passes: 4095 thresholds = twelve rounds
+constexpr int kMsRefineBins = 1 << kMsRoundsPerRefine;
+constexpr int kMsMaxRounds = 48;        // ratios stay exact dyadic doubles
 constexpr int kMsSlots = 16;          // copies of the per-pass totals
 
 // ---- update tiling ------------------------------------------------------------
@@ -151,18 +153,21 @@ hipError_t launch_ms_count(const TileDesc* tiles, int32_t ntiles, int32_t grid, 
                            const uint64_t* esum, const uint32_t* emax, const uint16_t* summ,
                            uint32_t* cnt, MsState* st_out, int64_t d, uint32_t* status,
                            hipStream_t s, const Ev& ev);
+// The previous pass left prev_slots copies of prev_nb counters at cnt_prev
+// (the first pass: kMsSlots x 64, a refine pass: 1 x kMsRefineBins).
 hipError_t launch_ms_refine(const TileDesc* tiles, const uint16_t* summ, int64_t nlines, int lpt,
-                            int32_t grid, int32_t nslots, const uint32_t* cnt_prev,
-                            uint32_t* cnt, const MsState* st_prev, MsState* st_out, uint32_t k,
-                            int64_t d, int32_t rounds_prev, int32_t n_search,
-                            uint64_t window_word, hipStream_t s, const Ev& ev);
+                            int32_t grid, int32_t prev_slots, int32_t prev_nb,
+                            const uint32_t* cnt_prev, uint32_t* cnt, const MsState* st_prev,
+                            MsState* st_out, uint32_t k, int64_t d, int32_t rounds_prev,
+                            int32_t n_search, uint64_t window_word, hipStream_t s,
+                            const Ev& ev);
 hipError_t launch_ms_emit(const TileDesc* tiles, const uint16_t* summ, int64_t nlines, int lpt,
-                          int32_t grid, int32_t nslots, const uint32_t* cnt_prev,
-                          const MsState* st_prev, MsState* st_out, uint32_t k, int64_t d,
-                          int32_t rounds_prev, int32_t n_search, uint64_t window_word,
-                          uint64_t* flags, int32_t* idx_out, void* val_out, int val16,
-                          uint32_t* status, uint32_t* clear_next, int64_t clear_words,
-                          hipStream_t s, const Ev& ev);
+                          int32_t grid, int32_t prev_slots, int32_t prev_nb,
+                          const uint32_t* cnt_prev, const MsState* st_prev, MsState* st_out,
+                          uint32_t k, int64_t d, int32_t rounds_prev, int32_t n_search,
+                          uint64_t window_word, uint64_t* flags, int32_t* idx_out,
+                          void* val_out, int val16, uint32_t* status, uint32_t* clear_next,
+                          int64_t clear_words, hipStream_t s, const Ev& ev);
 // launch-shape limits of the selection kernels
 int32_t select_max_groups();
 int32_t select_block();

@@ -1850,16 +1850,18 @@ __global__ __launch_bounds__(kUBlock) void k_lars_rates(const int32_t* __restric
 // GPU form. Thresholds are compared as magnitude keys: a >= t (a binary32
 // widened exactly, t a double) holds exactly when key(a) >= K(t), K(t) the
 // key of the smallest binary32 >= t. Bisection is a binary tree, so one pass
-// that counts the elements at or above each of the 63 thresholds of the next
-// six rounds lets the rounds be replayed afterwards exactly as the loop
-// would run them: N rounds take ceil(N / 6) passes.
+// that counts the elements at or above each of the 2^m - 1 thresholds of the
+// next m rounds lets the rounds be replayed afterwards exactly as the loop
+// would run them. The first pass, over every element, takes m = 6; the later
+// ones, over the few lines that reach the bracket, take m = 12: N rounds take
+// 1 + ceil((N - 6) / 12) passes (three for N = 30).
 //   ms_stream  x = g + r into r, line summaries, per-exponent sums of the
 //              significands of |x| (exact, in integers) and the largest key
 //   ms_count   forms the mean (the exact sum rounded once to double, divided
 //              by d) and u, then counts every element against the 63 keys of
 //              rounds 1..6
 //   ms_refine  replays the previous pass's rounds from its counts, then
-//              counts against the next 63 keys over the lines whose summary
+//              counts against the next 4095 keys over the lines whose summary
 //              can reach the lowest of them (later rounds only look at the
 //              top of the distribution)
 //   ms_emit    replays the last pass's rounds, fixes K1 = K(thres1),
@@ -1873,7 +1875,8 @@ __global__ __launch_bounds__(kUBlock) void k_lars_rates(const int32_t* __restric
 // No workgroup waits for another, and no kernel needs a device-wide fence.
 namespace {
 
-constexpr int kMsKeys = 64;                // keys[1..63] of one pass (keys[0] unused)
+constexpr int kMsKeys = 64;                // first pass: keys[1..63] (keys[0] unused)
+constexpr int kMsRefineKeys = kMsRefineBins;  // later passes: keys[1..4095]
 constexpr uint32_t kMsNone = 0x80000000u;  // "no thres1": above every key
 
 // Key of the smallest binary32 >= t, for t >= 0 (0 for t <= 0 or NaN).
@@ -1971,16 +1974,21 @@ __device__ __forceinline__ void ms_accum(uint32_t key, unsigned long long* es) {
   if (E < 255u) atomicAdd(&es[key >> kH1Shift], (unsigned long long)m);
 }
 
-// Keys of the 63 thresholds of the next six rounds into K[] (LDS): ratio_j =
-// l + j (r - l) / 64 (exact: r - l is a power of two), thres_j = mean +
-// ratio_j (u - mean) (the same double operations as a round of the loop).
-// Threads 0..63; ends with a barrier.
-__device__ __forceinline__ void ms_keys(const MsState& s, uint32_t* K) {
-  const int j = threadIdx.x;
-  if (j < kMsKeys) {
-    const double ratio = s.l + ((s.r - s.l) / 64.0) * (double)j;
-    K[j] = j ? ms_key_ceil(s.abar + ratio * (s.u - s.abar)) : 0u;
-  }
+// Keys of the nb - 1 thresholds of the next log2(nb) rounds into K[] (LDS):
+// ratio_j = l + j (r - l) / nb (exact: r - l is a power of two), thres_j =
+// mean + ratio_j (u - mean) (the same double operations as a round of the
+// loop). A pass that runs fewer rounds uses the nodes of the same grid that
+// its rounds reach. Whole workgroup; ends with a barrier.
+__device__ __forceinline__ double ms_step(const MsState& s, int nb) {
+  return (s.r - s.l) * (1.0 / (double)nb);  // exact: both factors are powers of two
+}
+__device__ __forceinline__ uint32_t ms_key_at(const MsState& s, double step, int j) {
+  const double ratio = s.l + step * (double)j;
+  return ms_key_ceil(s.abar + ratio * (s.u - s.abar));
+}
+__device__ __forceinline__ void ms_keys(const MsState& s, uint32_t* K, int nb) {
+  const double step = ms_step(s, nb);
+  for (int j = threadIdx.x; j < nb; j += blockDim.x) K[j] = j ? ms_key_at(s, step, j) : 0u;
   __syncthreads();
 }
 
@@ -1996,6 +2004,21 @@ __device__ __forceinline__ int ms_bin(const uint32_t* K, uint32_t key) {
 #pragma unroll
   for (int i = 1; i < 8; ++i) j += (K[base + i] <= key) ? 1 : 0;
   return j;
+}
+
+// The same over the 4095 keys of a later pass: three levels of fifteen
+// comparisons (K[256 i], then K[base + 16 i], then K[base + i]).
+__device__ __forceinline__ int ms_bin_big(const uint32_t* K, uint32_t key) {
+  static_assert(kMsRefineKeys == 4096, "three levels of 16");
+  int base = 0;
+#pragma unroll
+  for (int lvl = 256; lvl >= 1; lvl >>= 4) {
+    int g = 0;
+#pragma unroll
+    for (int i = 1; i < 16; ++i) g += (K[base + lvl * i] <= key) ? 1 : 0;
+    base += lvl * g;
+  }
+  return base;
 }
 
 // The state before the first pass, from the stream's partial sums. Whole
@@ -2038,57 +2061,74 @@ __device__ void ms_first_state(const unsigned long long* __restrict__ esum,
   __syncthreads();
 }
 
-// The state after a pass: its counts (nslots copies of 64 bins, summed),
+// The state after a pass: its counts (nslots copies of nb bins, summed),
 // suffix sums, and its rounds replayed (round i takes bin j = midpoint of
-// the bins still open, whose key was made from the same ratio). After round
-// n_search the window offset and length are fixed too. Whole workgroup.
-// h: 64 words of LDS.
+// the bins still open, whose ratio l + (r - l) / 2 equals l0 + j (r0 - l0) /
+// nb exactly, so its threshold and key are the ones the pass counted
+// against; the replay itself only moves bin indices and forms the keys of
+// the recorded counts at the end). After round n_search the window offset
+// and length are fixed too. Whole workgroup of kSBlock threads. h: nb words
+// of LDS (64 or 4096).
 __device__ void ms_next_state(const MsState& prev, const uint32_t* __restrict__ cnt, int nslots,
-                              int32_t rounds, int32_t n_search, uint32_t k, int64_t d,
-                              uint64_t window_word, MsState& s, uint32_t* h) {
+                              int nb, int32_t rounds, int32_t n_search, uint32_t k, int64_t d,
+                              uint64_t window_word, MsState& s, uint32_t* h, uint32_t* wsum) {
   const int tid = threadIdx.x;
-  if (tid < kMsKeys) h[tid] = 0u;
+  for (int i = tid; i < nb; i += kSBlock) h[i] = 0u;
   __syncthreads();
-  for (int i = tid; i < nslots * kMsKeys; i += blockDim.x) {
+  for (int i = tid; i < nslots * nb; i += kSBlock) {
     const uint32_t c = cnt[i];
-    if (c) atomicAdd(&h[i & (kMsKeys - 1)], c);
+    if (c) atomicAdd(&h[i & (nb - 1)], c);
   }
   __syncthreads();
-  // nnz[j] = elements with key >= K[j] = sum of h[j..63]: a suffix scan by
-  // the first wavefront (lane t holds bin 63 - t)
-  if (tid < 64) {
-    static_assert(kMsKeys == 64, "one bin per lane");
-    const uint32_t run = wave_incl_scan(h[63 - tid]);
-    __builtin_amdgcn_wave_barrier();
-    h[63 - tid] = run;
+  // nnz[j] = elements with key >= K[j] = sum of h[j..nb-1]
+  if (nb == kMsKeys) {
+    // the first wavefront, lane t holding bin 63 - t
+    if (tid < 64) {
+      const uint32_t run = wave_incl_scan(h[63 - tid]);
+      __builtin_amdgcn_wave_barrier();
+      h[63 - tid] = run;
+    }
+  } else {
+    // thread t owns the four bins 4095 - 4t .. 4092 - 4t (from the top)
+    static_assert(kMsRefineKeys == 4 * kSBlock, "four bins per thread");
+    const int b0 = kMsRefineKeys - 4 * (tid + 1);
+    uint32_t c[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) c[q] = h[b0 + 3 - q];  // c[0] = highest bin
+    uint32_t tot;
+    const uint32_t ex = sblock_scan(c[0] + c[1] + c[2] + c[3], wsum, &tot);
+    uint32_t run = ex;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      run += c[q];
+      h[b0 + 3 - q] = run;
+    }
   }
   __syncthreads();
   if (tid == 0) {
-    const double abar = prev.abar, u = prev.u;
-    double l = prev.l, r = prev.r;
     uint32_t k1 = prev.k1, k2 = prev.k2, K1 = prev.K1, K2 = prev.K2;
-    int jl = 0, jh = kMsKeys;
+    int jl = 0, jh = nb, j1 = -1, j2 = -1;
     for (int i = 0; i < rounds; ++i) {
-      const int j = (jl + jh) / 2;
-      const double ratio = l + (r - l) / 2;
-      const double thres = abar + ratio * (u - abar);
+      const int j = (jl + jh) >> 1;
       const uint32_t n = h[j];
       if (n <= k) {
-        r = ratio;
         jh = j;
         if (n > k1) {
           k1 = n;
-          K1 = ms_key_ceil(thres);
+          j1 = j;
         }
       } else {
-        l = ratio;
         jl = j;
         if (n < k2) {
           k2 = n;
-          K2 = ms_key_ceil(thres);
+          j2 = j;
         }
       }
     }
+    const double step = ms_step(prev, nb);
+    if (j1 >= 0) K1 = ms_key_at(prev, step, j1);
+    if (j2 >= 0) K2 = ms_key_at(prev, step, j2);
+    const double l = prev.l + step * (double)jl, r = prev.l + step * (double)jh;
     s = prev;
     s.level = prev.level + (uint32_t)rounds;
     if (s.level >= (uint32_t)n_search) {
@@ -2234,7 +2274,7 @@ __global__ __launch_bounds__(kBlock) void k_ms_count(
     if (s.bad && status) atomicOr(status, TKEF_STATUS_NONFINITE);
   }
   if (tid < kMsKeys) h[tid] = 0u;
-  ms_keys(s, K);
+  ms_keys(s, K, kMsKeys);
   const uint32_t kmin = K[1];
   const uint32_t smin = kmin >> 16;  // a line is read if its summary reaches this
   const int per_tile = kTile / kQuarter;
@@ -2315,33 +2355,37 @@ __global__ __launch_bounds__(kBlock) void k_ms_count(
 }
 
 // Later counting passes: the state after the previous pass, then the lines
-// whose summary reaches keys[1] (the lowest threshold left to try), read by
-// the selection regions.
+// whose summary reaches keys[1] (the lowest threshold left to try), counted
+// against 4095 keys (up to twelve rounds), read by the selection regions.
+// The previous pass left prev_slots copies of prev_nb bins; this pass adds
+// into one copy of 4096.
 __global__ __launch_bounds__(kSBlock) void k_ms_refine(
     const TileDesc* __restrict__ tiles, const uint16_t* __restrict__ summ, int64_t nlines,
-    int lpt, int nslots, const uint32_t* __restrict__ cnt_prev, uint32_t* __restrict__ cnt,
-    const MsState* __restrict__ st_prev, MsState* __restrict__ st_out, uint32_t k, int64_t d,
-    int32_t rounds_prev, int32_t n_search, uint64_t window_word) {
+    int lpt, int prev_slots, int prev_nb, const uint32_t* __restrict__ cnt_prev,
+    uint32_t* __restrict__ cnt, const MsState* __restrict__ st_prev, MsState* __restrict__ st_out,
+    uint32_t k, int64_t d, int32_t rounds_prev, int32_t n_search, uint64_t window_word) {
   __shared__ MsState s;
-  __shared__ uint32_t K[kMsKeys];
-  __shared__ uint32_t h[kMsKeys];
+  __shared__ uint32_t K[kMsRefineKeys];
+  __shared__ uint32_t h[kMsRefineKeys];
+  __shared__ uint32_t wsum[kSWaves];
   const int tid = threadIdx.x;
   const MsState prev = *st_prev;
-  ms_next_state(prev, cnt_prev, nslots, rounds_prev, n_search, k, d, window_word, s, h);
+  ms_next_state(prev, cnt_prev, prev_slots, prev_nb, rounds_prev, n_search, k, d, window_word, s,
+                h, wsum);
   if (blockIdx.x == 0 && tid == 0) *st_out = s;
-  if (tid < kMsKeys) h[tid] = 0u;
-  ms_keys(s, K);
+  for (int i = tid; i < kMsRefineKeys; i += kSBlock) h[i] = 0u;
+  ms_keys(s, K, kMsRefineKeys);
   const uint32_t kmin = K[1];
   LineSpan ls;
   ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
   const uint32_t mask = ls.flagged([&](int) -> uint32_t { return kmin; });
   walk_mask(ls, mask, [&](int, uint32_t key) -> bool { return key >= kmin; },
             [&](int, const TileDesc&, int, float, uint32_t key) {
-              atomicAdd(&h[ms_bin(K, key)], 1u);
+              atomicAdd(&h[ms_bin_big(K, key)], 1u);
             });
   __syncthreads();
-  const int slot = blockIdx.x % nslots;
-  if (tid < kMsKeys && h[tid]) atomicAdd(&cnt[(size_t)slot * kMsKeys + tid], h[tid]);
+  for (int i = tid; i < kMsRefineKeys; i += kSBlock)
+    if (h[i]) atomicAdd(&cnt[i], h[i]);
 }
 
 // Ordered compaction: an element with key >= K1 goes to slot (#key >= K1
@@ -2351,20 +2395,21 @@ __global__ __launch_bounds__(kSBlock) void k_ms_refine(
 // look-back over the regions before.
 __global__ __launch_bounds__(kSBlock) void k_ms_emit(
     const TileDesc* __restrict__ tiles, const uint16_t* __restrict__ summ, int64_t nlines,
-    int lpt, int nslots, const uint32_t* __restrict__ cnt_prev,
+    int lpt, int prev_slots, int prev_nb, const uint32_t* __restrict__ cnt_prev,
     const MsState* __restrict__ st_prev, MsState* __restrict__ st_out, uint32_t k, int64_t d,
     int32_t rounds_prev, int32_t n_search, uint64_t window_word, uint64_t* __restrict__ flags,
     int32_t* __restrict__ idx_out, void* __restrict__ val_out, int val16,
     uint32_t* __restrict__ status, uint32_t* __restrict__ clear_next, int64_t clear_words) {
   __shared__ MsState s;
-  __shared__ uint32_t h[kMsKeys];
+  __shared__ uint32_t h[kMsRefineKeys];
   __shared__ uint32_t wsum[2 * kSWaves];
   __shared__ uint64_t red[kSWaves];
   __shared__ int32_t stage_code[kStage * kSBlock];
   __shared__ float stage_x[kStage * kSBlock];
   const int tid = threadIdx.x;
   const MsState prev = *st_prev;
-  ms_next_state(prev, cnt_prev, nslots, rounds_prev, n_search, k, d, window_word, s, h);
+  ms_next_state(prev, cnt_prev, prev_slots, prev_nb, rounds_prev, n_search, k, d, window_word, s,
+                h, wsum);
   if (blockIdx.x == 0 && tid == 0) *st_out = s;
 #pragma unroll 1
   for (int64_t i = (int64_t)blockIdx.x * kSBlock + tid; i < clear_words;
@@ -2530,25 +2575,27 @@ hipError_t launch_ms_count(const TileDesc* tiles, int32_t ntiles, int32_t grid, 
 }
 
 hipError_t launch_ms_refine(const TileDesc* tiles, const uint16_t* summ, int64_t nlines, int lpt,
-                            int32_t grid, int32_t nslots, const uint32_t* cnt_prev,
-                            uint32_t* cnt, const MsState* st_prev, MsState* st_out, uint32_t k,
-                            int64_t d, int32_t rounds_prev, int32_t n_search,
-                            uint64_t window_word, hipStream_t s, const Ev& ev) {
+                            int32_t grid, int32_t prev_slots, int32_t prev_nb,
+                            const uint32_t* cnt_prev, uint32_t* cnt, const MsState* st_prev,
+                            MsState* st_out, uint32_t k, int64_t d, int32_t rounds_prev,
+                            int32_t n_search, uint64_t window_word, hipStream_t s,
+                            const Ev& ev) {
   return launch(k_ms_refine, dim3(grid), dim3(kSBlock), s, ev, tiles, summ, nlines, lpt,
-                (int)nslots, cnt_prev, cnt, st_prev, st_out, k, d, rounds_prev, n_search,
-                window_word);
+                (int)prev_slots, (int)prev_nb, cnt_prev, cnt, st_prev, st_out, k, d, rounds_prev,
+                n_search, window_word);
 }
 
 hipError_t launch_ms_emit(const TileDesc* tiles, const uint16_t* summ, int64_t nlines, int lpt,
-                          int32_t grid, int32_t nslots, const uint32_t* cnt_prev,
-                          const MsState* st_prev, MsState* st_out, uint32_t k, int64_t d,
-                          int32_t rounds_prev, int32_t n_search, uint64_t window_word,
-                          uint64_t* flags, int32_t* idx_out, void* val_out, int val16,
-                          uint32_t* status, uint32_t* clear_next, int64_t clear_words,
-                          hipStream_t s, const Ev& ev) {
+                          int32_t grid, int32_t prev_slots, int32_t prev_nb,
+                          const uint32_t* cnt_prev, const MsState* st_prev, MsState* st_out,
+                          uint32_t k, int64_t d, int32_t rounds_prev, int32_t n_search,
+                          uint64_t window_word, uint64_t* flags, int32_t* idx_out,
+                          void* val_out, int val16, uint32_t* status, uint32_t* clear_next,
+                          int64_t clear_words, hipStream_t s, const Ev& ev) {
   return launch(k_ms_emit, dim3(grid), dim3(kSBlock), s, ev, tiles, summ, nlines, lpt,
-                (int)nslots, cnt_prev, st_prev, st_out, k, d, rounds_prev, n_search, window_word,
-                flags, idx_out, val_out, val16, status, clear_next, clear_words);
+                (int)prev_slots, (int)prev_nb, cnt_prev, st_prev, st_out, k, d, rounds_prev,
+                n_search, window_word, flags, idx_out, val_out, val16, status, clear_next,
+                clear_words);
 }
 
 int32_t select_max_groups() { return kSMaxGroups; }

@@ -158,11 +158,11 @@ def test_approx_plan_host_side():
     assert _create([10], mode=tk.APPROX, k=11, rho=0.0) == tk.ERANGE
     p = tk.SparsifyPlan([1000, 8192 * 3 + 5], mode=tk.APPROX, rho=0.001)
     assert p.ngroups == 1 and p.k_total == tk.k_from_rho(1000 + 8192 * 3 + 5, 0.001)
-    assert p.nlaunch == 2 + 5
+    assert p.nlaunch == 3 + 2  # 30 rounds: 6 in the first pass, 12 in each later one
     names = p.launch_names()
     assert names[0] == "ms_stream" and names[1] == "ms_count" and names[-1] == "ms_emit"
-    assert names[2:-1] == ["ms_refine1", "ms_refine2", "ms_refine3", "ms_refine4"]
-    for n, launches in ((1, 3), (6, 3), (7, 4), (12, 4), (13, 5), (48, 10)):
+    assert names[2:-1] == ["ms_refine1", "ms_refine2"]
+    for n, launches in ((1, 3), (6, 3), (7, 4), (18, 4), (19, 5), (30, 5), (31, 6), (48, 7)):
         q = tk.SparsifyPlan([5000], mode=tk.APPROX, k=7, n_search=n)
         assert q.nlaunch == launches, n
     h = p._h
