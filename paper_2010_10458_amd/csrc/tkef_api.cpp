@@ -128,7 +128,8 @@ struct tkef_sparsify_plan_s {
   std::vector<GroupDesc> groups;
   uint32_t cand_cap = 0;  // per-tensor path: capacity of the compacted candidate list
   uint32_t rcap = 0;      // one-group path: candidates stored per region
-  int32_t sel_lpt = 1, sel_grid = 1;  // selection kernels: lines per thread, workgroups
+  int32_t sel_lpt = 1, sel_grid = 1, sel_block = 1;  // selection kernels: lines per thread,
+                                                    // workgroups, threads per workgroup
   // Scratch that must start at zero (histograms, prefix flags, overflow and
   // count words) exists twice; execution n uses copy n % 2 and its last kernel
   // clears the other copy for execution n + 1. Offsets below are relative to
@@ -218,19 +219,23 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     p->ntiles = static_cast<int32_t>(p->tiles.size());
     p->nlines = (int64_t)p->ntiles * kLinesPerTile;
     // selection kernels: `lpt` consecutive summary lines per thread, at most
-    // select_max_groups() workgroups of select_block() threads. Aim for about
+    // select_max_groups() workgroups of sb threads (collect_block() for the
+    // exact one-group kernels, select_block() for the others). Aim for about
     // 256 workgroups (one per compute unit); lpt is a power of two from 4 up
     // (the kernels fetch four 16-bit summaries per load, and a thread's lines
     // must lie in one tile).
-    const int64_t sb = select_block(), sg = select_max_groups();
+    const bool one = p->ngroups == 1;
+    const bool approx = mode == TKEF_APPROX;
+    const bool coll = one && !approx;
+    const int64_t sb = coll ? collect_block(p->nlines) : select_block();
+    p->sel_block = (int32_t)sb;
+    const int64_t sg = select_max_groups();
     const int64_t want = (p->nlines + sb * 256 - 1) / (sb * 256);
     int64_t lpt = 4;  // a power of two from 4 to select_max_lpt()
     while (lpt < want && lpt < select_max_lpt()) lpt *= 2;
     if ((p->nlines + sb * lpt - 1) / (sb * lpt) > sg) throw std::bad_alloc();  // d < 2^31
     p->sel_lpt = (int32_t)lpt;
     const int64_t g_lines = (p->nlines + sb * lpt - 1) / (sb * lpt);
-    const bool one = p->ngroups == 1;
-    const bool approx = mode == TKEF_APPROX;
     // Candidates are the positions at or above the level-1 threshold bin:
     // about k plus one bin's worth. One group: each region (the lines of one
     // workgroup) stores up to rcap of them, several times the even share of
@@ -521,12 +526,13 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     uint32_t* rcnt = reinterpret_cast<uint32_t*>(base + plan->off_rcnt);
     uint32_t* rbin = reinterpret_cast<uint32_t*>(base + plan->off_rbin);
     if (e == hipSuccess)
-      e = launch_collect(tiles, groups, st, hist1, plan->nslots, summ, nl, lpt, sg, plan->rcap,
-                         hist2, rbin, rcand, rband, rbtmp, rsuf, rcnt, s, tr.at(li++));
+      e = launch_collect(tiles, groups, st, hist1, plan->nslots, summ, nl, lpt, sg,
+                         plan->sel_block, plan->rcap, hist2, rbin, rcand, rband, rbtmp, rsuf,
+                         rcnt, s, tr.at(li++));
     if (e == hipSuccess)
-      e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, plan->rcap, hist2, rbin, rcand,
-                        rband, rsuf, rcnt, idx_out, val_out, val16, clear_next, clear_words, s,
-                        tr.at(li++));
+      e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, plan->sel_block, plan->rcap, hist2,
+                        rbin, rcand, rband, rsuf, rcnt, idx_out, val_out, val16, clear_next,
+                        clear_words, s, tr.at(li++));
   } else {
     uint32_t* hist3 = reinterpret_cast<uint32_t*>(zb + plan->off_hist3);
     uint64_t* flags1 = reinterpret_cast<uint64_t*>(zb + plan->off_flags1);

@@ -116,15 +116,17 @@ hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
                        const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s, const Ev& ev);
 // one selection group
 constexpr int kPerBin = 4;  // band keys per (level-2 bin, region) kept in the rbin table
+// block: collect_block(nlines) threads per workgroup
 hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
                           const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
-                          int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* rbin,
-                          uint32_t* rcand, uint32_t* rband, uint32_t* rbtmp, uint32_t* rsuf,
-                          uint32_t* rcnt, hipStream_t s, const Ev& ev);
+                          int lpt, int32_t grid, int32_t block, uint32_t rcap, uint32_t* hist2,
+                          uint32_t* rbin, uint32_t* rcand, uint32_t* rband, uint32_t* rbtmp,
+                          uint32_t* rsuf, uint32_t* rcnt, hipStream_t s, const Ev& ev);
 hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
-                         int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
-                         const uint32_t* rcand, const uint32_t* rband, const uint32_t* rsuf,
+                         int32_t grid, int32_t block, uint32_t rcap, const uint32_t* hist2,
+                         const uint32_t* rbin, const uint32_t* rcand, const uint32_t* rband,
+                         const uint32_t* rsuf,
                          const uint32_t* rcnt, int32_t* idx_out, void* val_out, int val16,
                          uint32_t* clear_next, int64_t clear_words, hipStream_t s, const Ev& ev);
 // several selection groups
@@ -171,6 +173,7 @@ hipError_t launch_ms_emit(const TileDesc* tiles, const uint16_t* summ, int64_t n
 // launch-shape limits of the selection kernels
 int32_t select_max_groups();
 int32_t select_block();
+int32_t collect_block(int64_t nlines);  // collect and finish (one exact selection group)
 int32_t select_max_lpt();
 
 hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, int32_t P,

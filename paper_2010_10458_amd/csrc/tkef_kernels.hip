@@ -459,6 +459,14 @@ __global__ __launch_bounds__(kBlock) void k_pick(int level, const GroupDesc* __r
 // the workgroup goes on. Flag words are cleared before every execution.
 constexpr int kSBlock = 1024;
 constexpr int kSWaves = kSBlock / 64;
+// collect and finish (one selection group) run kCBlockSmall threads per
+// workgroup, with more lines per thread, for inputs of up to kCSmallLines
+// summary lines: their per-thread steps (summaries, scans, bins) are short
+// instruction runs over every thread of a region, so fewer threads per
+// compute unit finish them sooner. Larger inputs take kSBlock threads, whose
+// regions hold more flagged lines, so each thread walks fewer of them.
+constexpr int kCBlockSmall = 512;
+constexpr int64_t kCSmallLines = (int64_t)256 * kCBlockSmall * 8;
 constexpr int kSMaxGroups = 4096;
 constexpr int kSMaxLpt = 16;     // lines per thread at most
 static_assert(kLinesPerTile % kSMaxLpt == 0, "a thread's lines lie in one tile");
@@ -526,61 +534,46 @@ __device__ uint64_t group_prefix(uint64_t* __restrict__ flags, uint64_t mine, ui
   return sblock_sum_u64(v, red);
 }
 
-// Within one workgroup: the bin of a 1024-bin histogram (highest bin first)
-// where the running count reaches `need`. res[] (LDS): bin, count above it,
-// count in it; all zero if no bin does (need == 0 or above the total). Exactly
-// one thread writes res[], after the scan's barriers (so every reader of an
-// earlier result is done); ends with a barrier.
-__device__ __forceinline__ void sblock_pick(const uint32_t* __restrict__ hist, uint32_t need,
-                                            uint32_t* wsum, uint32_t* res) {
-  static_assert(kH2Bins == kSBlock && kH3Bins == kSBlock, "one bin per thread");
+// Within one NT-thread workgroup: the bin of an NB-bin histogram, held in
+// NSLOT copies NB words apart (summed), where the running count from the
+// highest bin reaches `need`. Thread t owns the NB / NT bins from
+// NB - 1 - t NB / NT downwards; all its loads are issued before the first is
+// used. res[] (LDS): bin, count above it, count in it; all zero if no bin
+// does (need == 0 or above the total). Exactly one thread writes res[], after
+// the scan's barriers (so every reader of an earlier result is done); ends
+// with a barrier.
+template <int NT, int NB, int NSLOT>
+__device__ __forceinline__ void block_pick(const uint32_t* __restrict__ hist, uint32_t need,
+                                           uint32_t* wsum, uint32_t* res) {
+  constexpr int BPT = NB / NT;
+  static_assert(BPT >= 1 && BPT * NT == NB, "whole bins per thread");
   const int tid = threadIdx.x;
-  const int bin = kSBlock - 1 - tid;
-  const uint32_t c = hist[bin];
-  uint32_t total;
-  const uint32_t ex = sblock_scan(c, wsum, &total);
-  const bool found = ex < need && need <= ex + c;
-  const bool none = (need == 0u || need > total) && tid == kSBlock - 1;
-  if (found || none) {
-    res[0] = found ? (uint32_t)bin : 0u;
-    res[1] = found ? ex : 0u;
-    res[2] = found ? c : 0u;
-  }
-  __syncthreads();
-}
-
-// Within one workgroup: level-1 pick over a 2048-bin histogram held in
-// NSLOT copies (two bins per thread; every copy's load is issued before the
-// first is used). Returns via res[] as sblock_pick does. Ends with a barrier.
-template <int NSLOT>
-__device__ __forceinline__ void sblock_pick1(const uint32_t* __restrict__ hist1, uint32_t need,
-                                             uint32_t* wsum, uint32_t* res) {
-  static_assert(kH1Bins == 2 * kSBlock, "two bins per thread");
-  const int tid = threadIdx.x;
-  const int lo = kH1Bins - 2 * (tid + 1);  // this thread's bins: lo, lo + 1 (from the top)
-  uint2 v[NSLOT];
+  const int top = NB - 1 - BPT * tid;
+  uint32_t v[NSLOT][BPT];
 #pragma unroll
   for (int sl = 0; sl < NSLOT; ++sl)
-    v[sl] = *reinterpret_cast<const uint2*>(hist1 + (size_t)sl * kH1Bins + lo);
-  uint32_t c0 = 0u, c1 = 0u;
 #pragma unroll
-  for (int sl = 0; sl < NSLOT; ++sl) {
-    c0 += v[sl].x;
-    c1 += v[sl].y;
+    for (int b = 0; b < BPT; ++b) v[sl][b] = hist[(size_t)sl * NB + top - b];
+  uint32_t c[BPT], sum = 0u;
+#pragma unroll
+  for (int b = 0; b < BPT; ++b) {
+    c[b] = 0u;
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl) c[b] += v[sl][b];
+    sum += c[b];
   }
   uint32_t total;
-  const uint32_t ex = sblock_scan(c0 + c1, wsum, &total);
-  if (ex < need && need <= ex + c0 + c1) {
-    if (ex + c1 >= need) {  // higher bin first
-      res[0] = (uint32_t)(lo + 1);
-      res[1] = ex;
-      res[2] = c1;
-    } else {
-      res[0] = (uint32_t)lo;
-      res[1] = ex + c1;
-      res[2] = c0;
+  uint32_t run = block_scan<NT>(sum, wsum, &total);
+#pragma unroll
+  for (int b = 0; b < BPT; ++b) {
+    if (run < need && need <= run + c[b]) {
+      res[0] = (uint32_t)(top - b);
+      res[1] = run;
+      res[2] = c[b];
     }
-  } else if ((need == 0u || need > total) && tid == kSBlock - 1) {
+    run += c[b];
+  }
+  if ((need == 0u || need > total) && tid == NT - 1) {
     res[0] = 0u;
     res[1] = 0u;
     res[2] = 0u;
@@ -589,16 +582,18 @@ __device__ __forceinline__ void sblock_pick1(const uint32_t* __restrict__ hist1,
 }
 
 // The thread's `lpt` consecutive summary lines starting at line l0. lpt is a
-// power of two up to kSMaxLpt and divides kLinesPerTile, so all of them lie
-// in one tile. flagged() gives the lines whose summary reaches thr(group).
-// Lines past a tile's elements keep the summary 0 that bind writes (the
-// stream never writes them), so they are flagged only for thr < 2^16, and
-// hold no elements then. Summaries and the descriptor are fetched together
-// up front.
+// power of two from 4 up to kSMaxLpt and divides kLinesPerTile, so all of
+// them lie in one tile. flagged() gives the lines whose summary reaches
+// thr(group). Lines past a tile's elements keep the summary 0 that bind
+// writes (the stream never writes them), so they are flagged only for
+// thr < 2^16, and hold no elements then. Summaries (two per register) and the
+// descriptor are fetched together up front.
 struct LineSpan {
+  static constexpr int MAXL = kSMaxLpt;
+  static_assert(MAXL % 4 == 0 && MAXL <= 32, "line mask width");
   int tile, e0, lim;  // tile, position of the first line's first element, lines held
   TileDesc t;
-  uint16_t sv[kSMaxLpt];
+  uint32_t sp[MAXL / 2];
 
   __device__ __forceinline__ void load(const TileDesc* __restrict__ tiles,
                                        const uint16_t* __restrict__ summ, int64_t nlines,
@@ -608,13 +603,11 @@ struct LineSpan {
     e0 = (int)(l0 % kLinesPerTile) * kLine;
     // four summaries per 8-byte load (l0 and lpt are multiples of 4)
 #pragma unroll
-    for (int c = 0; c < kSMaxLpt / 4; ++c) {
+    for (int c = 0; c < MAXL / 4; ++c) {
       uint2 v = make_uint2(0u, 0u);
       if (has && 4 * c < lpt) v = *reinterpret_cast<const uint2*>(summ + l0 + 4 * c);
-      sv[4 * c + 0] = (uint16_t)(v.x & 0xFFFFu);
-      sv[4 * c + 1] = (uint16_t)(v.x >> 16);
-      sv[4 * c + 2] = (uint16_t)(v.y & 0xFFFFu);
-      sv[4 * c + 3] = (uint16_t)(v.y >> 16);
+      sp[2 * c] = v.x;
+      sp[2 * c + 1] = v.y;
     }
     t = tiles[tile];
     lim = has ? lpt : 0;
@@ -625,7 +618,10 @@ struct LineSpan {
     const uint32_t th = thr(t.group) >> 16;
     uint32_t m = 0u;
 #pragma unroll
-    for (int q = 0; q < kSMaxLpt; ++q) m |= (q < lim && (uint32_t)sv[q] >= th) ? (1u << q) : 0u;
+    for (int q = 0; q < MAXL; ++q) {
+      const uint32_t sv = (sp[q >> 1] >> (16 * (q & 1))) & 0xFFFFu;
+      m |= (q < lim && sv >= th) ? (1u << q) : 0u;
+    }
     return m;
   }
 };
@@ -723,17 +719,17 @@ static_assert(kSMaxGroups <= 65536, "region numbers fit 16 bits");
 // (The sizes come last among the arguments: they are used at the start, so
 // both cache lines of the argument block are fetched then, and later reloads
 // of the pointers hit.)
-__global__ __launch_bounds__(kSBlock) void k_collect(
+template <int NT>
+__global__ __launch_bounds__(NT) void k_collect(
     const TileDesc* __restrict__ tiles, const GroupDesc* __restrict__ groups,
     GroupState* __restrict__ st, const uint32_t* __restrict__ hist1,
     const uint16_t* __restrict__ summ, uint32_t* __restrict__ hist2,
     uint32_t* __restrict__ rbin, uint4* __restrict__ rcand, uint32_t* __restrict__ rband,
     uint32_t* __restrict__ rbtmp, uint32_t* __restrict__ rsuf, uint2* __restrict__ rcnt,
     uint32_t rcap, int lpt, int64_t nlines) {
-  static_assert(kH2Bins == kSBlock, "one level-2 bin per thread");
   __shared__ uint32_t h[kH2Bins];
   __shared__ uint32_t hoff[kH2Bins];
-  __shared__ uint32_t wsum[2 * kSWaves];
+  __shared__ uint32_t wsum[2 * (NT / 64)];
   __shared__ uint32_t res[3];
   __shared__ float* lptr[kFlCap];        // flagged lines: first element
   __shared__ uint32_t lgidx[kFlCap];     // global index of the first element
@@ -741,16 +737,16 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
   __shared__ uint32_t bandk[kBandCap];
   __shared__ uint32_t nband;
   const int tid = threadIdx.x, w = blockIdx.x;
-  h[tid] = 0u;
+  for (int i = tid; i < kH2Bins; i += NT) h[i] = 0u;
   if (tid == 0) nband = 0u;
 
   // summaries of this thread's lines (independent of the pick), then the
   // level-1 pick, whose barriers also publish the cleared LDS
   LineSpan ls;
-  ls.load(tiles, summ, nlines, ((int64_t)w * kSBlock + tid) * lpt, lpt);
+  ls.load(tiles, summ, nlines, ((int64_t)w * NT + tid) * lpt, lpt);
   __builtin_amdgcn_sched_barrier(0);  // keep those loads ahead of the histogram's
   const uint32_t k = groups[0].k;
-  sblock_pick1<kSlotsOne>(hist1, k, wsum, res);
+  block_pick<NT, kH1Bins, kSlotsOne>(hist1, k, wsum, res);
   const uint32_t B1 = res[0];
   const uint32_t above1 = res[1];
   const uint32_t lo = B1 << kH1Shift;
@@ -758,7 +754,7 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
   // flagged lines in position order: thread order, then line order
   const uint32_t mask = ls.flagged([&](int) -> uint32_t { return lo; });
   uint32_t F;
-  const uint32_t fex = sblock_scan((uint32_t)__popc(mask), wsum, &F);
+  const uint32_t fex = block_scan<NT>((uint32_t)__popc(mask), wsum, &F);
   uint32_t cw = 0u;   // candidates so far (workgroup-uniform)
   bool fits = true;   // workgroup-uniform
   uint4* __restrict__ cdst = rcand + (size_t)w * rcap;
@@ -781,7 +777,7 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
     __syncthreads();
     const uint32_t nl = min((uint32_t)kFlCap, F - c0);
 #pragma unroll 1
-    for (uint32_t b0 = 0; b0 < nl; b0 += kSBlock) {
+    for (uint32_t b0 = 0; b0 < nl; b0 += NT) {
       const uint32_t i = b0 + tid;
       float v[kLine];
       uint32_t hm = 0u, bm = 0u, gidx0 = 0u;  // candidates, band members of the line
@@ -816,7 +812,7 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
         }
       }
       uint32_t tot;
-      const uint32_t ex = sblock_scan((uint32_t)__popc(hm), wsum, &tot);
+      const uint32_t ex = block_scan<NT>((uint32_t)__popc(hm), wsum, &tot);
       if (cw + tot > rcap) fits = false;
       if (fits && hm) {
         uint4* __restrict__ dst = cdst + cw + ex;
@@ -835,19 +831,34 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
     if (c0 + (uint32_t)kFlCap < F) __syncthreads();
   }
 
-  // band members by level-2 bin from the top (thread tid owns bin 1023 - tid):
-  // sorted into rband[w], and the first kPerBin of each bin also into rbin
-  const int bin = kH2Bins - 1 - tid;
-  const uint32_t cb = h[bin];
+  // band members by level-2 bin from the top (thread t owns the kB2 bins
+  // from 1023 - kB2 t downwards): sorted into rband[w], and the first
+  // kPerBin of each bin also into rbin
+  constexpr int kB2 = kH2Bins / NT;
+  const int top = kH2Bins - 1 - kB2 * tid;
+  uint32_t cb[kB2], ab[kB2], csum = 0u;
+#pragma unroll
+  for (int b = 0; b < kB2; ++b) {
+    cb[b] = h[top - b];
+    csum += cb[b];
+  }
   uint32_t bw;
-  const uint32_t above = sblock_scan(cb, wsum, &bw);
+  uint32_t above = block_scan<NT>(csum, wsum, &bw);
   const bool band_ok = bw <= rcap;  // the band fits rband[w] (and rbtmp[w])
-  h[bin] = above;     // from here on: the bin's next slot in rband[w]
-  hoff[bin] = above;  // the bin's first slot
+#pragma unroll
+  for (int b = 0; b < kB2; ++b) {
+    ab[b] = above;
+    h[top - b] = above;     // from here on: the bin's next slot in rband[w]
+    hoff[top - b] = above;  // the bin's first slot
+    above += cb[b];
+  }
   __syncthreads();
   // (global stores after the last barrier: a barrier waits for them)
-  if (cb) atomicAdd(&hist2[bin], cb);
-  if (bw) rsuf[(size_t)w * kH2Bins + bin] = above;
+#pragma unroll
+  for (int b = 0; b < kB2; ++b) {
+    if (cb[b]) atomicAdd(&hist2[top - b], cb[b]);
+    if (bw) rsuf[(size_t)w * kH2Bins + top - b] = ab[b];
+  }
   uint32_t* __restrict__ dst = rband + (size_t)w * rcap;
   auto place = [&](uint32_t key) {
     const uint32_t b2 = (key >> kH2Shift) & (kH2Bins - 1);
@@ -858,10 +869,13 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
   };
   if (band_ok) {
     // the first kBandCap from LDS, the rest (a dense selection) from the
-    // region's scratch in rbtmp, written before the barriers above
+    // region's scratch in rbtmp, written before the barriers above. Two loops:
+    // a read through a pointer that may point to either would be a flat load,
+    // which waits for every global store and atomic issued above.
+    const uint32_t nlds = min(bw, (uint32_t)kBandCap);
+    for (uint32_t j = tid; j < nlds; j += NT) place(bandk[j]);
     const uint32_t* __restrict__ tmp = rbtmp + (size_t)w * rcap;
-    for (uint32_t j = tid; j < bw; j += kSBlock)
-      place(j < (uint32_t)kBandCap ? bandk[j] : tmp[j]);
+    for (uint32_t j = (uint32_t)kBandCap + tid; j < bw; j += NT) place(tmp[j]);
   }
   if (tid == 0)
     rcnt[w] = make_uint2(cw | ((fits ? 0u : 1u) << 31), bw | ((band_ok ? 0u : 1u) << 31));
@@ -877,10 +891,10 @@ __global__ __launch_bounds__(kSBlock) void k_collect(
 
 // Calls f(key) for the level-2 class members (band members in bin B2) of the
 // stored regions among [0, wlim), reading them again from rband. Regions are
-// taken kSBlock at a time and their members spread over the workgroup through
-// a scan of the per-region counts. off, abv: kSBlock words of LDS each.
+// taken NT at a time and their members spread over the workgroup through
+// a scan of the per-region counts. off, abv: NT words of LDS each.
 // Uniform in the workgroup.
-template <typename F>
+template <int NT, typename F>
 __device__ __forceinline__ void for_class2(int wlim, uint32_t B2, uint32_t rcap,
                                            const uint2* __restrict__ rcnt,
                                            const uint32_t* __restrict__ rsuf,
@@ -888,7 +902,7 @@ __device__ __forceinline__ void for_class2(int wlim, uint32_t B2, uint32_t rcap,
                                            uint32_t* abv, uint32_t* wsum, F f) {
   const int tid = threadIdx.x;
 #pragma unroll 1
-  for (int r0 = 0; r0 < wlim; r0 += kSBlock) {
+  for (int r0 = 0; r0 < wlim; r0 += NT) {
     const int r = r0 + tid;
     uint32_t above = 0u, at = 0u;
     if (r < wlim) {
@@ -901,13 +915,13 @@ __device__ __forceinline__ void for_class2(int wlim, uint32_t B2, uint32_t rcap,
       }
     }
     uint32_t tot;
-    const uint32_t ex = sblock_scan(at, wsum, &tot);
+    const uint32_t ex = block_scan<NT>(at, wsum, &tot);
     off[tid] = ex;
     abv[tid] = above;
     __syncthreads();
 #pragma unroll 1
-    for (uint32_t j = tid; j < tot; j += kSBlock) {
-      int a = 0, b = kSBlock - 1;  // the last region slot with off <= j holds member j
+    for (uint32_t j = tid; j < tot; j += NT) {
+      int a = 0, b = NT - 1;  // the last region slot with off <= j holds member j
       while (a < b) {
         const int m = (a + b + 1) >> 1;
         if (off[m] <= j) a = m; else b = m - 1;
@@ -918,9 +932,8 @@ __device__ __forceinline__ void for_class2(int wlim, uint32_t B2, uint32_t rcap,
   }
 }
 
-constexpr int kRegPerThread = kSMaxGroups / kSBlock;
-
-__global__ __launch_bounds__(kSBlock) void k_finish(
+template <int NT>
+__global__ __launch_bounds__(NT) void k_finish(
     const TileDesc* __restrict__ tiles, const GroupDesc* __restrict__ groups,
     const GroupState* __restrict__ st, const uint16_t* __restrict__ summ, int64_t nlines,
     int lpt, uint32_t rcap, const uint32_t* __restrict__ hist2,
@@ -930,16 +943,17 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
     int32_t* __restrict__ idx_out, void* __restrict__ val_out, int val16,
     uint32_t* __restrict__ clear_next, int64_t clear_words) {
   __shared__ uint32_t h[kH3Bins];
-  __shared__ uint32_t wsum[4 * kSWaves];
+  __shared__ uint32_t wsum[4 * (NT / 64)];
   __shared__ uint32_t res[3];
-  __shared__ uint32_t off[kSBlock], abv[kSBlock];
+  __shared__ uint32_t off[NT], abv[NT];
   __shared__ uint32_t ovbits[kOvWords];  // regions whose band keys were not stored
   __shared__ uint32_t c2key[kC2Cap];     // level-2 class members of the stored regions
   __shared__ uint16_t c2reg[kC2Cap];     // ... and their regions
   __shared__ uint32_t n2;
+  constexpr int kRegPerThread = kSMaxGroups / NT;
   const int tid = threadIdx.x, w = blockIdx.x, G = gridDim.x;
-  h[tid] = 0u;
-  for (int i = tid; i < kOvWords; i += kSBlock) ovbits[i] = 0u;
+  for (int i = tid; i < kH3Bins; i += NT) h[i] = 0u;
+  for (int i = tid; i < kOvWords; i += NT) ovbits[i] = 0u;
   if (tid == 0) n2 = 0u;
 
   // fetched together: level-1 state, this region's counts and first
@@ -951,7 +965,7 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   const uint4* __restrict__ mc = rcand + (size_t)w * rcap;
   uint32_t cb = 0u, ce = 0u;
   if (!own_ov) {
-    const uint32_t per = (mine.x + kSBlock - 1) / kSBlock;
+    const uint32_t per = (mine.x + NT - 1) / NT;
     cb = min(mine.x, tid * per);
     ce = min(mine.x, cb + per);
   }
@@ -959,13 +973,13 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   uint2 cr[kRegPerThread];
 #pragma unroll
   for (int q = 0; q < kRegPerThread; ++q) {
-    const int r = q * kSBlock + tid;
+    const int r = q * NT + tid;
     cr[q] = make_uint2(0u, 0u);
-    if (q * kSBlock < G && r < G) cr[q] = rcnt[r];
+    if (q * NT < G && r < G) cr[q] = rcnt[r];
   }
 
   // level 2 (the pick's barriers also publish the cleared LDS above)
-  sblock_pick(hist2, s0.need, wsum, res);
+  block_pick<NT, kH2Bins, 1>(hist2, s0.need, wsum, res);
   const uint32_t B2 = res[0];
   const uint32_t need2 = (res[1] < s0.need) ? s0.need - res[1] : 0u;
   const uint32_t cls21 = (s0.prefix << 10) | B2;
@@ -978,8 +992,8 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   bool slow = false;  // some region has more than kPerBin class-2 members
 #pragma unroll
   for (int q = 0; q < kRegPerThread; ++q) {
-    if (q * kSBlock >= G) break;
-    const int r = q * kSBlock + tid;
+    if (q * NT >= G) break;
+    const int r = q * NT + tid;
     if (r >= G) continue;
     const uint32_t bw = cr[q].y & 0x7FFFFFFFu;
     const bool ov = (cr[q].y >> 31) != 0u;
@@ -1016,9 +1030,9 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   if (n2 & 0x80000000u) {
     __syncthreads();  // every thread has read n2
     if (tid == 0) n2 = 0u;
-    for (int i = tid; i < kH3Bins; i += kSBlock) h[i] = 0u;
+    for (int i = tid; i < kH3Bins; i += NT) h[i] = 0u;
 #pragma unroll 1
-    for (int r0 = 0; r0 < G; r0 += kSBlock) {
+    for (int r0 = 0; r0 < G; r0 += NT) {
       const int r = r0 + tid;
       uint32_t above = 0u, at = 0u;
       if (r < G) {
@@ -1031,13 +1045,13 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
         }
       }
       uint32_t tot;
-      const uint32_t ex = sblock_scan(at, wsum, &tot);  // (its barriers order the reset above)
+      const uint32_t ex = block_scan<NT>(at, wsum, &tot);  // (its barriers order the reset above)
       off[tid] = ex;
       abv[tid] = above;
       __syncthreads();
 #pragma unroll 1
-      for (uint32_t j = tid; j < tot; j += kSBlock) {
-        int a = 0, b = kSBlock - 1;  // the last region slot with off <= j holds member j
+      for (uint32_t j = tid; j < tot; j += NT) {
+        int a = 0, b = NT - 1;  // the last region slot with off <= j holds member j
         while (a < b) {
           const int m = (a + b + 1) >> 1;
           if (off[m] <= j) a = m; else b = m - 1;
@@ -1066,7 +1080,7 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
         m &= m - 1u;
         if (r >= wlim) break;
         LineSpan lr;
-        lr.load(tiles, summ, nlines, ((int64_t)r * kSBlock + tid) * lpt, lpt);
+        lr.load(tiles, summ, nlines, ((int64_t)r * NT + tid) * lpt, lpt);
         walk_mask(lr, lr.flagged([&](int) -> uint32_t { return thr2; }), in_cls2,
                   [&](int, const TileDesc&, int, float, uint32_t key) { f(key); });
       }
@@ -1074,7 +1088,7 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   };
   lines_class2(G, [&](uint32_t key) { atomicAdd(&h[key & (kH3Bins - 1)], 1u); });
   __syncthreads();
-  sblock_pick(h, need2, wsum, res);
+  block_pick<NT, kH3Bins, 1>(h, need2, wsum, res);
   const uint32_t T = (cls21 << 10) | res[0];
   const uint32_t need3 = (res[1] < need2) ? need2 - res[1] : 0u;
 
@@ -1085,10 +1099,10 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
     eqb += (key == T) ? 1u : 0u;
   };
   if (n2 <= (uint32_t)kC2Cap) {
-    for (uint32_t j = tid; j < n2; j += kSBlock)
+    for (uint32_t j = tid; j < n2; j += NT)
       if ((int)c2reg[j] < w) tally(c2key[j]);
   } else {
-    for_class2(w, B2, rcap, rcnt, rsuf, rband, off, abv, wsum, tally);
+    for_class2<NT>(w, B2, rcap, rcnt, rsuf, rband, off, abv, wsum, tally);
   }
   lines_class2(w, tally);
 
@@ -1097,7 +1111,7 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   LineSpan ls;
   uint32_t mask = 0u;
   if (own_ov) {
-    ls.load(tiles, summ, nlines, ((int64_t)w * kSBlock + tid) * lpt, lpt);
+    ls.load(tiles, summ, nlines, ((int64_t)w * NT + tid) * lpt, lpt);
     mask = ls.flagged([&](int) -> uint32_t { return T; });
   }
   auto at_least_T = [&](int, uint32_t key) -> bool { return key >= T; };
@@ -1126,11 +1140,11 @@ __global__ __launch_bounds__(kSBlock) void k_finish(
   }
   const uint32_t sv[4] = {gt, eq, gtb, eqb};
   uint32_t pre[4], tot[4];
-  block_scan4<kSBlock>(sv, wsum, pre, tot);
+  block_scan4<NT>(sv, wsum, pre, tot);
   // clear the other copy of the zero-initialised scratch for the next run
   // (after the last barrier, which would wait for these stores)
 #pragma unroll 1
-  for (int64_t i = (int64_t)w * kSBlock + tid; i < clear_words; i += (int64_t)G * kSBlock)
+  for (int64_t i = (int64_t)w * NT + tid; i < clear_words; i += (int64_t)G * NT)
     clear_next[i] = 0u;
   if (gt + eq == 0u) return;
   uint32_t gtr = tot[2] + pre[0];
@@ -2504,26 +2518,39 @@ hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
 
 hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
                           const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
-                          int lpt, int32_t grid, uint32_t rcap, uint32_t* hist2, uint32_t* rbin,
+                          int lpt, int32_t grid, int32_t block, uint32_t rcap, uint32_t* hist2, uint32_t* rbin,
                           uint32_t* rcand, uint32_t* rband, uint32_t* rbtmp, uint32_t* rsuf,
                           uint32_t* rcnt, hipStream_t s, const Ev& ev) {
   if (nslots != kSlotsOne) return hipErrorInvalidValue;
-  return launch(k_collect, dim3(grid), dim3(kSBlock), s, ev, tiles, groups, st, hist1, summ,
-                hist2, rbin, reinterpret_cast<uint4*>(rcand), rband, rbtmp, rsuf,
-                reinterpret_cast<uint2*>(rcnt), rcap, lpt, nlines);
+  if (block == kCBlockSmall)
+    return launch(k_collect<kCBlockSmall>, dim3(grid), dim3(block), s, ev, tiles, groups, st,
+                  hist1, summ, hist2, rbin, reinterpret_cast<uint4*>(rcand), rband, rbtmp, rsuf,
+                  reinterpret_cast<uint2*>(rcnt), rcap, lpt, nlines);
+  if (block == kSBlock)
+    return launch(k_collect<kSBlock>, dim3(grid), dim3(block), s, ev, tiles, groups, st, hist1,
+                  summ, hist2, rbin, reinterpret_cast<uint4*>(rcand), rband, rbtmp, rsuf,
+                  reinterpret_cast<uint2*>(rcnt), rcap, lpt, nlines);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
-                         int32_t grid, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
+                         int32_t grid, int32_t block, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
                          const uint32_t* rcand, const uint32_t* rband, const uint32_t* rsuf,
                          const uint32_t* rcnt, int32_t* idx_out, void* val_out, int val16,
                          uint32_t* clear_next, int64_t clear_words, hipStream_t s,
                          const Ev& ev) {
-  return launch(k_finish, dim3(grid), dim3(kSBlock), s, ev, tiles, groups, st, summ, nlines, lpt,
-                rcap, hist2, rbin, reinterpret_cast<const uint4*>(rcand), rband, rsuf,
-                reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, val16, clear_next,
-                clear_words);
+  if (block == kCBlockSmall)
+    return launch(k_finish<kCBlockSmall>, dim3(grid), dim3(block), s, ev, tiles, groups, st, summ,
+                  nlines, lpt, rcap, hist2, rbin, reinterpret_cast<const uint4*>(rcand), rband,
+                  rsuf, reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, val16,
+                  clear_next, clear_words);
+  if (block == kSBlock)
+    return launch(k_finish<kSBlock>, dim3(grid), dim3(block), s, ev, tiles, groups, st, summ,
+                  nlines, lpt, rcap, hist2, rbin, reinterpret_cast<const uint4*>(rcand), rband,
+                  rsuf, reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, val16,
+                  clear_next, clear_words);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
@@ -2600,6 +2627,9 @@ hipError_t launch_ms_emit(const TileDesc* tiles, const uint16_t* summ, int64_t n
 
 int32_t select_max_groups() { return kSMaxGroups; }
 int32_t select_block() { return kSBlock; }
+int32_t collect_block(int64_t nlines) {
+  return nlines <= kCSmallLines ? kCBlockSmall : kSBlock;
+}
 int32_t select_max_lpt() { return kSMaxLpt; }
 
 hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, int32_t P,

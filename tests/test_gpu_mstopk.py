@@ -76,7 +76,7 @@ def test_flat_sizes(n):
         compare([g], [r], k, word=int(rng.integers(0, 2**63)), label=f"normal n={n}")
 
 
-@pytest.mark.parametrize("n_search", [1, 5, 6, 7, 12, 13, 30, 48])
+@pytest.mark.parametrize("n_search", [1, 5, 6, 7, 12, 13, 18, 19, 30, 31, 42, 48])
 def test_rounds(n_search):
     rng = np.random.default_rng(400 + n_search)
     n = 200_003
