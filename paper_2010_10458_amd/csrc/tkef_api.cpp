@@ -263,7 +263,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     size_t z = 0;
     if (approx) {
       p->off_ms_state = o;  o = align_up(o + (size_t)(kMsMaxPasses + 1) * sizeof(MsState));
-      p->off_ms_esum = z;   z = align_up(z + (size_t)kMsSlots * 256 * 8);
+      p->off_ms_esum = z;   z = align_up(z + (size_t)kMsSlots * kMsDigitStride * 8);
       p->off_ms_emax = z;   z = align_up(z + (size_t)kMsSlots * 4);
       p->off_ms_cnt = z;    z = align_up(z + kMsCntWords * 4);
       p->off_ms_flags = z;  z = align_up(z + (size_t)p->sel_grid * 8);

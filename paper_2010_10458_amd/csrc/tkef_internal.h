@@ -71,6 +71,7 @@ constexpr int kMsRoundsPerRefine = 12;  // later passes: 4095 thresholds = twelv
 constexpr int kMsRefineBins = 1 << kMsRoundsPerRefine;
 constexpr int kMsMaxRounds = 48;        // ratios stay exact dyadic doubles
 constexpr int kMsSlots = 16;          // copies of the per-pass totals
+constexpr int kMsDigitStride = 16;    // words per copy of the exact-sum digits
 
 // ---- update tiling ------------------------------------------------------------
 // Update tiles are aligned blocks of kUTile global positions; one workgroup

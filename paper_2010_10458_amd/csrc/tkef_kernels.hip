@@ -537,8 +537,8 @@ __device__ uint64_t group_prefix(uint64_t* __restrict__ flags, uint64_t mine, ui
 // Within one NT-thread workgroup: the bin of an NB-bin histogram, held in
 // NSLOT copies NB words apart (summed), where the running count from the
 // highest bin reaches `need`. Thread t owns the NB / NT bins from
-// NB - 1 - t NB / NT downwards; all its loads are issued before the first is
-// used. res[] (LDS): bin, count above it, count in it; all zero if no bin
+// NB - 1 - t NB / NT downwards, read as one 8- or 16-byte load per copy (hist
+// 16-byte aligned); all its loads are issued before the first is used. res[] (LDS): bin, count above it, count in it; all zero if no bin
 // does (need == 0 or above the total). Exactly one thread writes res[], after
 // the scan's barriers (so every reader of an earlier result is done); ends
 // with a barrier.
@@ -547,13 +547,27 @@ __device__ __forceinline__ void block_pick(const uint32_t* __restrict__ hist, ui
                                            uint32_t* wsum, uint32_t* res) {
   constexpr int BPT = NB / NT;
   static_assert(BPT >= 1 && BPT * NT == NB, "whole bins per thread");
+  static_assert(BPT == 1 || BPT == 2 || BPT == 4, "one load per copy");
   const int tid = threadIdx.x;
   const int top = NB - 1 - BPT * tid;
-  uint32_t v[NSLOT][BPT];
+  uint32_t v[NSLOT][BPT];  // v[sl][b]: bin top - b
 #pragma unroll
-  for (int sl = 0; sl < NSLOT; ++sl)
-#pragma unroll
-    for (int b = 0; b < BPT; ++b) v[sl][b] = hist[(size_t)sl * NB + top - b];
+  for (int sl = 0; sl < NSLOT; ++sl) {
+    const uint32_t* src = hist + (size_t)sl * NB + (top - (BPT - 1));
+    if constexpr (BPT == 4) {
+      const uint4 q = *reinterpret_cast<const uint4*>(src);
+      v[sl][0] = q.w;
+      v[sl][1] = q.z;
+      v[sl][2] = q.y;
+      v[sl][3] = q.x;
+    } else if constexpr (BPT == 2) {
+      const uint2 q = *reinterpret_cast<const uint2*>(src);
+      v[sl][0] = q.y;
+      v[sl][1] = q.x;
+    } else {
+      v[sl][0] = src[0];
+    }
+  }
   uint32_t c[BPT], sum = 0u;
 #pragma unroll
   for (int b = 0; b < BPT; ++b) {
@@ -942,7 +956,7 @@ __global__ __launch_bounds__(NT) void k_finish(
     const uint32_t* __restrict__ rsuf, const uint2* __restrict__ rcnt,
     int32_t* __restrict__ idx_out, void* __restrict__ val_out, int val16,
     uint32_t* __restrict__ clear_next, int64_t clear_words) {
-  __shared__ uint32_t h[kH3Bins];
+  __shared__ __align__(16) uint32_t h[kH3Bins];
   __shared__ uint32_t wsum[4 * (NT / 64)];
   __shared__ uint32_t res[3];
   __shared__ uint32_t off[NT], abv[NT];
@@ -1869,8 +1883,9 @@ __global__ __launch_bounds__(kUBlock) void k_lars_rates(const int32_t* __restric
 // would run them. The first pass, over every element, takes m = 6; the later
 // ones, over the few lines that reach the bracket, take m = 12: N rounds take
 // 1 + ceil((N - 6) / 12) passes (three for N = 30).
-//   ms_stream  x = g + r into r, line summaries, per-exponent sums of the
-//              significands of |x| (exact, in integers) and the largest key
+//   ms_stream  x = g + r into r, line summaries, the exact sum of |x| (per
+//              exponent sums of significands in LDS, then ten 32-bit digits
+//              per workgroup added into one of 16 copies) and the largest key
 //   ms_count   forms the mean (the exact sum rounded once to double, divided
 //              by d) and u, then counts every element against the 63 keys of
 //              rounds 1..6
@@ -1903,79 +1918,73 @@ __device__ __forceinline__ uint32_t ms_key_ceil(double t) {
   return b;
 }
 
-// The exact sum of binary32 magnitudes, rounded once to double (nearest,
-// ties to even). es[E] = the sum of the significands (hidden bit included)
-// of the magnitudes with exponent field E, so the sum is
-// sum_E es[E] * 2^(max(E, 1) - 150). Called by a whole workgroup of at least
-// 256 threads (thread E adds its term as three 32-bit digits into dig[], 10
-// words of LDS, zeroed here; es < 2^55 and a shift < 254 fit in 10 digits).
-// Returns the double in every thread.
-__device__ double ms_exact_sum(const unsigned long long* es, unsigned long long* dig,
-                               double* out) {
-  const int tid = threadIdx.x;
-  if (tid < 10) dig[tid] = 0ull;
-  __syncthreads();
-  if (tid < 255) {
-    const unsigned long long m = es[tid];
-    if (m) {
-      const int sft = (tid ? tid : 1) - 1;  // units of 2^-149
-      const int q = sft >> 5, o = sft & 31;
-      // m << o spans 87 bits at most: three digits from q
-      const unsigned long long lo = m << o;                      // bits 0..63 of m << o
-      const unsigned long long hi = o ? (m >> (64 - o)) : 0ull;  // bits 64..
-      atomicAdd(&dig[q], lo & 0xFFFFFFFFull);
-      atomicAdd(&dig[q + 1], lo >> 32);
-      if (hi) atomicAdd(&dig[q + 2], hi);
-    }
+// The exact sum of binary32 magnitudes is kept as kMsDigits 32-bit digits
+// (units of 2^-149, each digit accumulated in 64 bits so that carries can
+// wait): es[E] = the sum of the significands (hidden bit included) of the
+// magnitudes with exponent field E contributes es[E] * 2^(max(E, 1) - 1).
+// ms_digits_add adds one such term as three digits (es < 2^55 and a shift
+// < 254 fit in the 320 bits).
+constexpr int kMsDigits = 10;
+static_assert(kMsDigits <= kMsDigitStride, "digits per copy");
+__device__ __forceinline__ void ms_digits_add(int E, unsigned long long m,
+                                              unsigned long long* dig) {
+  if (!m) return;
+  const int sft = (E ? E : 1) - 1;
+  const int q = sft >> 5, o = sft & 31;
+  // m << o spans 87 bits at most: three digits from q
+  const unsigned long long lo = m << o;                      // bits 0..63 of m << o
+  const unsigned long long hi = o ? (m >> (64 - o)) : 0ull;  // bits 64..
+  atomicAdd(&dig[q], lo & 0xFFFFFFFFull);
+  atomicAdd(&dig[q + 1], lo >> 32);
+  if (hi) atomicAdd(&dig[q + 2], hi);
+}
+
+// The digits' value rounded once to double (nearest, ties to even). Called
+// by one thread; every dig[i] < 2^63.
+__device__ double ms_digits_round(const unsigned long long* dig) {
+  // carries: every digit becomes < 2^32; then five 64-bit limbs
+  uint64_t L[5];
+  unsigned long long c = 0ull;
+  uint32_t d32[kMsDigits];
+  for (int i = 0; i < kMsDigits; ++i) {
+    const unsigned long long t = dig[i] + c;
+    d32[i] = (uint32_t)t;
+    c = t >> 32;
   }
-  __syncthreads();
-  if (tid == 0) {
-    // carries: every digit becomes < 2^32; then five 64-bit limbs
-    uint64_t L[5];
-    unsigned long long c = 0ull;
-    uint32_t d32[10];
-    for (int i = 0; i < 10; ++i) {
-      const unsigned long long t = dig[i] + c;
-      d32[i] = (uint32_t)t;
-      c = t >> 32;
+  for (int i = 0; i < 5; ++i) L[i] = (uint64_t)d32[2 * i] | ((uint64_t)d32[2 * i + 1] << 32);
+  int top = -1;
+  for (int i = 4; i >= 0 && top < 0; --i)
+    if (L[i]) top = 64 * i + 63 - __clzll((long long)L[i]);
+  double v = 0.0;
+  if (top >= 0 && top < 53) {
+    v = ldexp((double)L[0], -149);
+  } else if (top >= 53) {
+    const int lo = top - 52, rb = lo - 1;
+    auto bits64 = [&](int b) -> uint64_t {  // 64 bits of L from bit b
+      const int q = b >> 6, o = b & 63;
+      uint64_t x = L[q] >> o;
+      if (o && q + 1 < 5) x |= L[q + 1] << (64 - o);
+      return x;
+    };
+    uint64_t m = bits64(lo) & ((1ull << 53) - 1ull);
+    const bool rnd = (bits64(rb) & 1ull) != 0ull;
+    bool sticky = false;
+    for (int i = 0; i < 5; ++i) {
+      const int b0 = 64 * i;
+      if (b0 + 64 <= rb) sticky |= L[i] != 0ull;
+      else if (b0 < rb) sticky |= (L[i] & ((1ull << (rb - b0)) - 1ull)) != 0ull;
     }
-    for (int i = 0; i < 5; ++i) L[i] = (uint64_t)d32[2 * i] | ((uint64_t)d32[2 * i + 1] << 32);
-    int top = -1;
-    for (int i = 4; i >= 0 && top < 0; --i)
-      if (L[i]) top = 64 * i + 63 - __clzll((long long)L[i]);
-    double v = 0.0;
-    if (top >= 0 && top < 53) {
-      v = ldexp((double)L[0], -149);
-    } else if (top >= 53) {
-      const int lo = top - 52, rb = lo - 1;
-      auto bits64 = [&](int b) -> uint64_t {  // 64 bits of L from bit b
-        const int q = b >> 6, o = b & 63;
-        uint64_t x = L[q] >> o;
-        if (o && q + 1 < 5) x |= L[q + 1] << (64 - o);
-        return x;
-      };
-      uint64_t m = bits64(lo) & ((1ull << 53) - 1ull);
-      const bool rnd = (bits64(rb) & 1ull) != 0ull;
-      bool sticky = false;
-      for (int i = 0; i < 5; ++i) {
-        const int b0 = 64 * i;
-        if (b0 + 64 <= rb) sticky |= L[i] != 0ull;
-        else if (b0 < rb) sticky |= (L[i] & ((1ull << (rb - b0)) - 1ull)) != 0ull;
+    int e = lo;
+    if (rnd && (sticky || (m & 1ull))) {
+      ++m;
+      if (m == (1ull << 53)) {
+        m >>= 1;
+        ++e;
       }
-      int e = lo;
-      if (rnd && (sticky || (m & 1ull))) {
-        ++m;
-        if (m == (1ull << 53)) {
-          m >>= 1;
-          ++e;
-        }
-      }
-      v = ldexp((double)m, e - 149);
     }
-    *out = v;
+    v = ldexp((double)m, e - 149);
   }
-  __syncthreads();
-  return *out;
+  return v;
 }
 
 // Significand (hidden bit included) of |x| added into its bin of the top
@@ -2035,28 +2044,30 @@ __device__ __forceinline__ int ms_bin_big(const uint32_t* K, uint32_t key) {
   return base;
 }
 
-// The state before the first pass, from the stream's partial sums. Whole
-// workgroup (>= 256 threads). es: 256 words of LDS.
+// The state before the first pass, from the stream's partial sums: nslots
+// copies of the digits (kMsDigitStride words apart) and of the largest key.
+// Whole workgroup (>= kMsDigits threads).
 __device__ void ms_first_state(const unsigned long long* __restrict__ esum,
                                const uint32_t* __restrict__ emax, int nslots, int64_t d,
-                               MsState& s, unsigned long long* es, uint32_t* mk) {
-  __shared__ unsigned long long dig[10];
-  __shared__ double sh_sum;
+                               MsState& s, uint32_t* mk) {
+  __shared__ unsigned long long dig[kMsDigits];
   const int tid = threadIdx.x;
   if (tid == 0) *mk = 0u;
-  if (tid < 256) {
+  if (tid < kMsDigits) {
     unsigned long long v[kMsSlots];
 #pragma unroll
-    for (int sl = 0; sl < kMsSlots; ++sl) v[sl] = sl < nslots ? esum[(size_t)sl * 256 + tid] : 0ull;
+    for (int sl = 0; sl < kMsSlots; ++sl)
+      v[sl] = sl < nslots ? esum[(size_t)sl * kMsDigitStride + tid] : 0ull;
     unsigned long long t = 0ull;
 #pragma unroll
     for (int sl = 0; sl < kMsSlots; ++sl) t += v[sl];
-    es[tid] = t;
+    dig[tid] = t;
   }
   __syncthreads();
   if (tid < nslots) atomicMax(mk, emax[tid]);
-  const double total = ms_exact_sum(es, dig, &sh_sum);  // (its barriers publish *mk)
+  __syncthreads();
   if (tid == 0) {
+    const double total = ms_digits_round(dig);
     const uint32_t m = *mk;
     const bool bad = m >= 0x7F800000u;
     s.abar = bad ? 0.0 : total / (double)d;
@@ -2176,10 +2187,12 @@ __global__ __launch_bounds__(kBlock) void k_ms_stream(const TileDesc* __restrict
                                                       uint32_t* __restrict__ emax,
                                                       uint16_t* __restrict__ summ) {
   __shared__ unsigned long long es[kH1Bins];
+  __shared__ unsigned long long dig[kMsDigits];
   __shared__ uint32_t lmax[kQuarterLines];
   __shared__ uint32_t bmax;
   const int tid = threadIdx.x;
   for (int i = tid; i < kH1Bins; i += kBlock) es[i] = 0ull;
+  if (tid < kMsDigits) dig[tid] = 0ull;
   if (tid == 0) bmax = 0u;
   __syncthreads();
   const int slot = blockIdx.x % nslots;
@@ -2255,12 +2268,15 @@ __global__ __launch_bounds__(kBlock) void k_ms_stream(const TileDesc* __restrict
   }
   atomicMax(&bmax, tmax);
   __syncthreads();
-  // thread E: the eight bins of exponent field E, added into this copy
+  // thread E: the eight bins of exponent field E, as digits of this
+  // workgroup's exact sum, which are then added into this copy
   static_assert(kBlock == 256 && kH1Bins == 8 * kBlock, "one exponent per thread");
   unsigned long long v = 0ull;
 #pragma unroll
   for (int i = 0; i < 8; ++i) v += es[8 * tid + i];
-  if (v) atomicAdd(&esum[(size_t)slot * 256 + tid], v);
+  if (tid < 255) ms_digits_add(tid, v, dig);
+  __syncthreads();
+  if (tid < kMsDigits && dig[tid]) atomicAdd(&esum[(size_t)slot * kMsDigitStride + tid], dig[tid]);
   if (tid == 0 && bmax) atomicMax(&emax[slot], bmax);
 }
 
@@ -2277,12 +2293,11 @@ __global__ __launch_bounds__(kBlock) void k_ms_count(
     const uint16_t* __restrict__ summ, uint32_t* __restrict__ cnt,
     MsState* __restrict__ st_out, int64_t d, uint32_t* __restrict__ status) {
   __shared__ MsState s;
-  __shared__ unsigned long long es[256];
   __shared__ uint32_t K[kMsKeys];
   __shared__ uint32_t h[kMsKeys];
   __shared__ uint32_t mk;
   const int tid = threadIdx.x;
-  ms_first_state(esum, emax, nslots, d, s, es, &mk);
+  ms_first_state(esum, emax, nslots, d, s, &mk);
   if (blockIdx.x == 0 && tid == 0) {
     *st_out = s;
     if (s.bad && status) atomicOr(status, TKEF_STATUS_NONFINITE);
