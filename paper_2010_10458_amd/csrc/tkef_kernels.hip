@@ -1208,9 +1208,12 @@ __global__ __launch_bounds__(NT) void k_finish(
 //
 // gather: over the lines whose summary can hold a key of at least the
 // group's level-1 bin B1: (a) the level-2 histogram of the elements in bin
-// B1; (b) ordered compaction of all elements with key >= B1 << 20 into
-// `cand`. meta[0] = overflow (the candidates did not fit in `cap`; later
-// steps then read lines), meta[1] = candidate count.
+// B1 (counted in LDS for the group of the region's first line, which holds
+// most of a region's lines when tensors are large, and added to the global
+// histogram once; other groups' members go to it directly); (b) ordered
+// compaction of all elements with key >= B1 << 20 into `cand`. meta[0] =
+// overflow (the candidates did not fit in `cap`; later steps then read
+// lines), meta[1] = candidate count.
 __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__ tiles,
                                                     const GroupState* __restrict__ st,
                                                     const uint16_t* __restrict__ summ,
@@ -1223,9 +1226,14 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
   __shared__ uint32_t wsum[2 * kSWaves];
   __shared__ uint64_t red[kSWaves];
   __shared__ int32_t stage[kGStage * kSBlock];  // [slot][thread]
+  __shared__ uint32_t h2[kH2Bins];
   const int tid = threadIdx.x;
+  for (int i = tid; i < kH2Bins; i += kSBlock) h2[i] = 0u;
   LineSpan ls;
-  ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
+  const int64_t l0 = (int64_t)blockIdx.x * kSBlock * lpt;  // the region's first line
+  ls.load(tiles, summ, nlines, l0 + (int64_t)tid * lpt, lpt);
+  const int g0 = l0 < nlines ? tiles[l0 / kLinesPerTile].group : -1;
+  __syncthreads();  // h2 cleared
   // B1 = 0xFFFFFFFF for a group with nothing to select: shifted, it lies
   // above every key, so such a group yields no candidates
   const uint32_t b1t = st[ls.t.group].prefix;
@@ -1237,13 +1245,20 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
     if (c < (uint32_t)kGStage)
       stage[c * kSBlock + tid] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
     ++c;
-    if ((k >> kH1Shift) == b1_of(t.group))
-      atomicAdd(&hist2[(size_t)t.group * kH2Bins + ((k >> kH2Shift) & (kH2Bins - 1))], 1u);
+    if ((k >> kH1Shift) == b1_of(t.group)) {
+      const uint32_t b2 = (k >> kH2Shift) & (kH2Bins - 1);
+      if (t.group == g0) atomicAdd(&h2[b2], 1u);
+      else atomicAdd(&hist2[(size_t)t.group * kH2Bins + b2], 1u);
+    }
   });
 
   // ordered positions: scan within the workgroup, prefix across workgroups
+  // (the scan's barriers also complete the LDS histogram)
   uint32_t total;
   const uint32_t ex = sblock_scan(c, wsum, &total);
+  if (g0 >= 0)
+    for (int i = tid; i < kH2Bins; i += kSBlock)
+      if (h2[i]) atomicAdd(&hist2[(size_t)g0 * kH2Bins + i], h2[i]);
   const uint64_t pre = group_prefix(flags, total, red, status);
   const bool fits = pre + total <= cap;
   if (tid == 0) {
