@@ -122,6 +122,11 @@ constexpr size_t kMsCntWords =
 struct tkef_sparsify_plan_s {
   int32_t ntensors = 0, mode = 0, ngroups = 0, ntiles = 0, nslots = 1, stream_grid = 1;
   int32_t count_grid = 1;  // MSTopK first counting pass: eight workgroups per compute unit
+  // per-tensor path: gather runs one workgroup per line region (line_grid),
+  // hist3 and emit split the candidates over cand_grid workgroups (at least
+  // line_grid, which their line walk after an overflow needs; at most
+  // sel_grid, which sizes their flag arrays)
+  int32_t line_grid = 1, cand_grid = 1;
   int64_t d = 0, k_total = 0, nlines = 0;
   std::vector<int64_t> numels, goff, kgroup;
   std::vector<TileDesc> tiles;   // pointers filled at bind
@@ -250,6 +255,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
       p->cand_cap = (uint32_t)std::min<int64_t>(d, 4 * p->k_total + 65536);
       const int64_t g_cands = std::min<int64_t>(sg, ((int64_t)p->cand_cap + sb * 4 - 1) / (sb * 4));
       p->sel_grid = (int32_t)std::max<int64_t>(1, std::max(g_lines, g_cands));
+      p->line_grid = (int32_t)std::max<int64_t>(1, g_lines);
     }
     // level-1 histogram copies per group: many for one global selection (all
     // workgroups add into it), a few per tensor in per-tensor mode
@@ -293,7 +299,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
       p->off_rbin = o;   o = align_up(o + (size_t)kH2Bins * p->sel_grid * kPerBin * 4);
     } else {
       p->off_base = o;   o = align_up(o + (size_t)p->ngroups * 8);
-      p->off_cand = o;   o = align_up(o + (size_t)p->cand_cap * 4);
+      p->off_cand = o;   o = align_up(o + (size_t)p->cand_cap * 8);  // {code, bits of x}
     }
     p->ws_bytes = o;
   } catch (const std::bad_alloc&) {
@@ -354,6 +360,8 @@ extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* con
   const int64_t units = (int64_t)plan->ntiles * (kTile / kStreamUnit);
   plan->stream_grid = (int32_t)std::min<int64_t>((int64_t)4 * cus, units);
   plan->count_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>((int64_t)8 * cus, (units + 1) / 2));
+  // two candidate workgroups per compute unit are all resident at once
+  plan->cand_grid = std::max(plan->line_grid, std::min(plan->sel_grid, 2 * cus));
   char* base = static_cast<char*>(ws);
   hipError_t e = hipMemcpyAsync(base + plan->off_tiles, plan->tiles.data(),
                                 plan->tiles.size() * sizeof(TileDesc), hipMemcpyHostToDevice,
@@ -539,20 +547,22 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     uint64_t* flags2 = reinterpret_cast<uint64_t*>(zb + plan->off_flags2);
     uint32_t* meta = reinterpret_cast<uint32_t*>(zb + plan->off_meta);
     uint32_t* gbase = reinterpret_cast<uint32_t*>(base + plan->off_base);
-    int32_t* cand = reinterpret_cast<int32_t*>(base + plan->off_cand);
+    uint32_t* cand = reinterpret_cast<uint32_t*>(base + plan->off_cand);
     if (e == hipSuccess)
       e = launch_pick(1, groups, st, hist1, plan->nslots, ng, s, tr.at(li++));
     if (e == hipSuccess)
-      e = launch_gather(tiles, st, summ, nl, lpt, sg, hist2, flags1, cand, plan->cand_cap, meta,
-                        status, s, tr.at(li++));
+      e = launch_gather(tiles, st, summ, nl, lpt, plan->line_grid, hist2, flags1, cand,
+                        plan->cand_cap, meta, status, s, tr.at(li++));
     if (e == hipSuccess) e = launch_pick(2, groups, st, hist2, 1, ng, s, tr.at(li++));
     if (e == hipSuccess)
-      e = launch_hist3(tiles, nt, st, summ, nl, lpt, sg, cand, meta, hist3, s, tr.at(li++));
+      e = launch_hist3(tiles, nt, st, summ, nl, lpt, plan->cand_grid, cand, meta, hist3, s,
+                       tr.at(li++));
     if (e == hipSuccess) e = launch_pick(3, groups, st, hist3, 1, ng, s, tr.at(li++));
     if (e == hipSuccess) e = launch_groupscan(groups, st, ng, gbase, s, tr.at(li++));
     if (e == hipSuccess)
-      e = launch_emit(tiles, nt, groups, st, summ, nl, lpt, sg, cand, meta, gbase, flags2,
-                      idx_out, val_out, val16, status, clear_next, clear_words, s, tr.at(li++));
+      e = launch_emit(tiles, nt, groups, st, summ, nl, lpt, plan->cand_grid, cand, meta, gbase,
+                      flags2, idx_out, val_out, val16, status, clear_next, clear_words, s,
+                      tr.at(li++));
   }
   if (e != hipSuccess) {
     plan->needs_clear = true;

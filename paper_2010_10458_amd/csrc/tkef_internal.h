@@ -133,17 +133,17 @@ hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
 // several selection groups
 hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
                          int64_t nlines, int lpt, int32_t grid, uint32_t* hist2, uint64_t* flags,
-                         int32_t* cand, uint32_t cap, uint32_t* meta, uint32_t* status,
+                         uint32_t* cand, uint32_t cap, uint32_t* meta, uint32_t* status,
                          hipStream_t s, const Ev& ev);
 hipError_t launch_hist3(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
                         const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
-                        const int32_t* cand, const uint32_t* meta, uint32_t* hist3,
+                        const uint32_t* cand, const uint32_t* meta, uint32_t* hist3,
                         hipStream_t s, const Ev& ev);
 hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32_t ngroups,
                             uint32_t* base, hipStream_t s, const Ev& ev);
 hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
                        const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
-                       int32_t grid, const int32_t* cand, const uint32_t* meta,
+                       int32_t grid, const uint32_t* cand, const uint32_t* meta,
                        const uint32_t* base, uint64_t* flags, int32_t* idx_out, void* val_out,
                        int val16, uint32_t* status, uint32_t* clear_next, int64_t clear_words,
                        hipStream_t s, const Ev& ev);

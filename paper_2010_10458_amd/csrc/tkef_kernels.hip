@@ -475,7 +475,7 @@ static_assert((1 << kCandShift) == kTile, "candidate encoding");
 constexpr uint64_t kFlagValid = 1ull << 63, kFlagVal = (1ull << 63) - 1;
 constexpr uint32_t kSpinLimit = 1u << 22;
 constexpr int kStage = 8;       // candidates a thread stages in LDS
-constexpr int kGStage = 32;     // ... in gather (dense per-tensor selections; 128 KB)
+constexpr int kGStage = 24;     // ... in gather (dense per-tensor selections; 144 KB)
 
 __device__ __forceinline__ uint64_t flag_load(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -669,21 +669,30 @@ __device__ __forceinline__ void walk_mask(const LineSpan& ls, uint32_t mask, Hit
   }
 }
 
-// Calls f(tile, TileDesc, e, x, key) for candidates [cb, ce), in order.
+// Calls f(tile, TileDesc, e, x, key) for candidates [cb, ce), in order. A
+// candidate is {(tile << 13) | position-in-tile, bits of x}; four are taken
+// at a time, their entries and then their tile descriptors fetched together.
 template <typename F>
 __device__ __forceinline__ void walk_cands(const TileDesc* __restrict__ tiles, int32_t ntiles,
-                                           const int32_t* __restrict__ cand, uint32_t cb,
+                                           const uint2* __restrict__ cand, uint32_t cb,
                                            uint32_t ce, F f) {
 #pragma unroll 1
-  for (uint32_t j = cb; j < ce; ++j) {
-    const uint32_t c = (uint32_t)cand[j];
-    const int tile = (int)(c >> kCandShift);
-    const int e = (int)(c & (kTile - 1));
-    if (tile >= ntiles) continue;  // never produced; keeps accesses in bounds
-    const TileDesc t = tiles[tile];
-    if (e >= t.len) continue;
-    const float x = gptr(t.r)[e];
-    f(tile, t, e, x, mag_key(x));
+  for (uint32_t j = cb; j < ce; j += 4) {
+    uint2 q[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) q[c] = cand[min(j + (uint32_t)c, ce - 1u)];  // clamped
+    TileDesc t[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c)  // an entry never names a tile >= ntiles; clamped anyway
+      t[c] = tiles[min((int)(q[c].x >> kCandShift), ntiles - 1)];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int tile = (int)(q[c].x >> kCandShift);
+      const int e = (int)(q[c].x & (kTile - 1));
+      if (j + (uint32_t)c >= ce || tile >= ntiles || e >= t[c].len) continue;
+      const float x = __uint_as_float(q[c].y);
+      f(tile, t[c], e, x, mag_key(x));
+    }
   }
 }
 
@@ -1220,12 +1229,14 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
                                                     int64_t nlines, int lpt,
                                                     uint32_t* __restrict__ hist2,
                                                     uint64_t* __restrict__ flags,
-                                                    int32_t* __restrict__ cand, uint32_t cap,
+                                                    uint2* __restrict__ cand, uint32_t cap,
                                                     uint32_t* __restrict__ meta,
                                                     uint32_t* __restrict__ status) {
   __shared__ uint32_t wsum[2 * kSWaves];
   __shared__ uint64_t red[kSWaves];
-  __shared__ int32_t stage[kGStage * kSBlock];  // [slot][thread]
+  // [slot][thread]: position in the tile (the thread's lines lie in one tile), x
+  __shared__ uint16_t stage_e[kGStage * kSBlock];
+  __shared__ float stage_x[kGStage * kSBlock];
   __shared__ uint32_t h2[kH2Bins];
   const int tid = threadIdx.x;
   for (int i = tid; i < kH2Bins; i += kSBlock) h2[i] = 0u;
@@ -1241,9 +1252,11 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
   const uint32_t mask = ls.flagged([&](int g) -> uint32_t { return b1_of(g) << kH1Shift; });
   auto is_cand = [&](int g, uint32_t k) -> bool { return k >= (b1_of(g) << kH1Shift); };
   uint32_t c = 0u;
-  walk_mask(ls, mask, is_cand, [&](int tile, const TileDesc& t, int e, float, uint32_t k) {
-    if (c < (uint32_t)kGStage)
-      stage[c * kSBlock + tid] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
+  walk_mask(ls, mask, is_cand, [&](int, const TileDesc& t, int e, float x, uint32_t k) {
+    if (c < (uint32_t)kGStage) {
+      stage_e[c * kSBlock + tid] = (uint16_t)e;
+      stage_x[c * kSBlock + tid] = x;
+    }
     ++c;
     if ((k >> kH1Shift) == b1_of(t.group)) {
       const uint32_t b2 = (k >> kH2Shift) & (kH2Bins - 1);
@@ -1268,13 +1281,16 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
   if (fits && c) {
     const uint64_t pos = pre + ex;
     const uint32_t ns = min(c, (uint32_t)kGStage);
+    const uint32_t tcode = (uint32_t)ls.tile << kCandShift;
 #pragma unroll 1
-    for (uint32_t q = 0; q < ns; ++q) cand[pos + q] = stage[q * kSBlock + tid];
+    for (uint32_t q = 0; q < ns; ++q)
+      cand[pos + q] = make_uint2(tcode | stage_e[q * kSBlock + tid],
+                                 __float_as_uint(stage_x[q * kSBlock + tid]));
     if (c > (uint32_t)kGStage) {  // rare: read the lines again for the rest
       uint32_t i = 0u;
-      walk_mask(ls, mask, is_cand, [&](int tile, const TileDesc&, int e, float, uint32_t) {
+      walk_mask(ls, mask, is_cand, [&](int tile, const TileDesc&, int e, float x, uint32_t) {
         if (i >= (uint32_t)kGStage)
-          cand[pos + i] = (int32_t)(((uint32_t)tile << kCandShift) | (uint32_t)e);
+          cand[pos + i] = make_uint2(((uint32_t)tile << kCandShift) | (uint32_t)e, __float_as_uint(x));
         ++i;
       });
     }
@@ -1289,7 +1305,7 @@ __global__ __launch_bounds__(kSBlock) void k_hist3(const TileDesc* __restrict__ 
                                                    const GroupState* __restrict__ st,
                                                    const uint16_t* __restrict__ summ,
                                                    int64_t nlines, int lpt,
-                                                   const int32_t* __restrict__ cand,
+                                                   const uint2* __restrict__ cand,
                                                    const uint32_t* __restrict__ meta,
                                                    uint32_t* __restrict__ hist3) {
   const int tid = threadIdx.x;
@@ -1311,7 +1327,8 @@ __global__ __launch_bounds__(kSBlock) void k_hist3(const TileDesc* __restrict__ 
     const uint32_t per_wg = (C + gridDim.x - 1) / gridDim.x;
     const uint32_t wb = min(C, blockIdx.x * per_wg), we = min(C, wb + per_wg);
 #pragma unroll 1
-    for (uint32_t j = wb + tid; j < we; j += kSBlock) walk_cands(tiles, ntiles, cand, j, j + 1, body);
+    for (uint32_t j = wb + 4 * tid; j < we; j += 4 * kSBlock)
+      walk_cands(tiles, ntiles, cand, j, min(j + 4u, we), body);
   }
 }
 
@@ -1355,7 +1372,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
                                                   const GroupState* __restrict__ st,
                                                   const uint16_t* __restrict__ summ,
                                                   int64_t nlines, int lpt,
-                                                  const int32_t* __restrict__ cand,
+                                                  const uint2* __restrict__ cand,
                                                   const uint32_t* __restrict__ meta,
                                                   const uint32_t* __restrict__ base,
                                                   uint64_t* __restrict__ flags,
@@ -2585,18 +2602,18 @@ hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
 
 hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
                          int64_t nlines, int lpt, int32_t grid, uint32_t* hist2, uint64_t* flags,
-                         int32_t* cand, uint32_t cap, uint32_t* meta, uint32_t* status,
+                         uint32_t* cand, uint32_t cap, uint32_t* meta, uint32_t* status,
                          hipStream_t s, const Ev& ev) {
   return launch(k_gather, dim3(grid), dim3(kSBlock), s, ev, tiles, st, summ, nlines, lpt, hist2,
-                flags, cand, cap, meta, status);
+                flags, reinterpret_cast<uint2*>(cand), cap, meta, status);
 }
 
 hipError_t launch_hist3(const TileDesc* tiles, int32_t ntiles, const GroupState* st,
                         const uint16_t* summ, int64_t nlines, int lpt, int32_t grid,
-                        const int32_t* cand, const uint32_t* meta, uint32_t* hist3,
+                        const uint32_t* cand, const uint32_t* meta, uint32_t* hist3,
                         hipStream_t s, const Ev& ev) {
   return launch(k_hist3, dim3(grid), dim3(kSBlock), s, ev, tiles, ntiles, st, summ, nlines, lpt,
-                cand, meta, hist3);
+                reinterpret_cast<const uint2*>(cand), meta, hist3);
 }
 
 hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32_t ngroups,
@@ -2606,12 +2623,13 @@ hipError_t launch_groupscan(const GroupDesc* groups, const GroupState* st, int32
 
 hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* groups,
                        const GroupState* st, const uint16_t* summ, int64_t nlines, int lpt,
-                       int32_t grid, const int32_t* cand, const uint32_t* meta,
+                       int32_t grid, const uint32_t* cand, const uint32_t* meta,
                        const uint32_t* base, uint64_t* flags, int32_t* idx_out, void* val_out,
                        int val16, uint32_t* status, uint32_t* clear_next, int64_t clear_words,
                        hipStream_t s, const Ev& ev) {
   return launch(k_emit, dim3(grid), dim3(kSBlock), s, ev, tiles, ntiles, groups, st, summ, nlines,
-                lpt, cand, meta, base, flags, idx_out, val_out, val16, status, clear_next,
+                lpt, reinterpret_cast<const uint2*>(cand), meta, base, flags, idx_out, val_out,
+                val16, status, clear_next,
                 clear_words);
 }
 
