@@ -119,6 +119,24 @@ def test_multi_tensor_global_and_per_tensor():
     compare_with_oracle(grads, res, rho=0.3, mode=tk.PER_TENSOR, label="multi per-tensor 0.3")
 
 
+def test_per_tensor_candidate_overflow_and_dense_threads():
+    """Per tensor: a 300 K tensor of one magnitude (every element a candidate
+    of its group: more than the candidate list holds, 4 k_total + 65,536, so
+    hist3 and emit walk the lines instead) next to ordinary tensors; and a
+    dense selection where threads hold more candidates than gather stages."""
+    rng = np.random.default_rng(310)
+    n0 = 300_000
+    flat = np.where(np.arange(n0) % 5 == 0, np.float32(-0.75), np.float32(0.75))
+    grads = [flat, (rng.standard_normal(50_000)).astype(np.float32),
+             (rng.standard_normal(8_193) * 3).astype(np.float32)]
+    res = [np.zeros(a.size, np.float32) for a in grads]
+    compare_with_oracle(grads, res, rho=0.001, mode=tk.PER_TENSOR, label="per-tensor overflow")
+    dense = [(rng.standard_normal(n) * (1 + t)).astype(np.float32)
+             for t, n in enumerate([200_000, 70_001, 5])]
+    res = [(rng.standard_normal(a.size) * 0.1).astype(np.float32) for a in dense]
+    compare_with_oracle(dense, res, rho=0.4, mode=tk.PER_TENSOR, label="per-tensor rho 0.4")
+
+
 def test_unaligned_views():
     """Tensors that start off a 16-byte boundary take the scalar path."""
     import torch
