@@ -435,7 +435,7 @@ def main() -> int:
     if args.probe_copy:
         return probe_copy(args.probe_copy)
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (this build has no multi-GPU path); "
+        print(f"bench.py measures one GPU only (the library has no multi-GPU path); "
               f"got --gpus {args.gpus}", file=sys.stderr)
         return 2
     if args.workload != "resnet50":
