@@ -2430,6 +2430,9 @@ __global__ __launch_bounds__(kSBlock) void k_ms_refine(
   __shared__ uint32_t h[kMsRefineKeys];
   __shared__ uint32_t wsum[kSWaves];
   const int tid = threadIdx.x;
+  // this thread's summaries first: their latency overlaps the state
+  LineSpan ls;
+  ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
   const MsState prev = *st_prev;
   ms_next_state(prev, cnt_prev, prev_slots, prev_nb, rounds_prev, n_search, k, d, window_word, s,
                 h, wsum);
@@ -2437,8 +2440,6 @@ __global__ __launch_bounds__(kSBlock) void k_ms_refine(
   for (int i = tid; i < kMsRefineKeys; i += kSBlock) h[i] = 0u;
   ms_keys(s, K, kMsRefineKeys);
   const uint32_t kmin = K[1];
-  LineSpan ls;
-  ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
   const uint32_t mask = ls.flagged([&](int) -> uint32_t { return kmin; });
   walk_mask(ls, mask, [&](int, uint32_t key) -> bool { return key >= kmin; },
             [&](int, const TileDesc&, int, float, uint32_t key) {
@@ -2468,6 +2469,9 @@ __global__ __launch_bounds__(kSBlock) void k_ms_emit(
   __shared__ int32_t stage_code[kStage * kSBlock];
   __shared__ float stage_x[kStage * kSBlock];
   const int tid = threadIdx.x;
+  // this thread's summaries first: their latency overlaps the state
+  LineSpan ls;
+  ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
   const MsState prev = *st_prev;
   ms_next_state(prev, cnt_prev, prev_slots, prev_nb, rounds_prev, n_search, k, d, window_word, s,
                 h, wsum);
@@ -2477,8 +2481,6 @@ __global__ __launch_bounds__(kSBlock) void k_ms_emit(
        i += (int64_t)gridDim.x * kSBlock)
     clear_next[i] = 0u;
   const uint32_t K1 = s.K1, K2 = s.K2, rand = s.rand, take = s.take;
-  LineSpan ls;
-  ls.load(tiles, summ, nlines, ((int64_t)blockIdx.x * kSBlock + tid) * lpt, lpt);
   const uint32_t mask = ls.flagged([&](int) -> uint32_t { return K2; });
   auto hit = [&](int, uint32_t key) -> bool { return key >= K2; };
   uint32_t c1 = 0u, c2 = 0u, nst = 0u;
