@@ -445,10 +445,11 @@ __global__ __launch_bounds__(kBlock) void k_pick(int level, const GroupDesc* __r
 // ---------------------------------------------------------------------------
 // Selection kernels after the stream.
 //
-// They run as at most kSMaxGroups workgroups of kSBlock threads, each thread
-// owning `lpt` consecutive summary lines (or, in the per-tensor emit and
-// hist3, a run of the compacted candidate list). A candidate is encoded as
-// (tile << 13) | position-in-tile.
+// They run as at most kSMaxGroups workgroups of kSBlock threads (collect and
+// finish: NT threads, see below), each thread owning `lpt` consecutive
+// summary lines (or, in the per-tensor emit and hist3, a run of the compacted
+// candidate list). A candidate is encoded as (tile << 13) | position-in-tile,
+// in the per-tensor list together with the bits of x.
 //
 // The per-tensor path places its ordered output with a prefix of
 // per-workgroup counts: each workgroup publishes its count in a flag word
@@ -699,9 +700,8 @@ __device__ __forceinline__ void walk_cands(const TileDesc* __restrict__ tiles, i
 // ---------------------------------------------------------------------------
 // One selection group (top-k over all tensors together): collect, finish.
 //
-// Workgroup w of either kernel owns the region of summary lines
-// [w * kSBlock * lpt, (w + 1) * kSBlock * lpt), lpt consecutive lines per
-// thread. No workgroup waits on another: the ordered output is placed from
+// Workgroup w of either kernel (NT threads) owns the region of summary lines
+// [w * NT * lpt, (w + 1) * NT * lpt), lpt consecutive lines per thread. No workgroup waits on another: the ordered output is placed from
 // small per-region counts that collect leaves behind.
 //
 // collect makes the level-1 pick (bin B1 of the k-th largest key) itself from
