@@ -101,7 +101,10 @@ static const char* const kSparsifyLaunchesOne[] = {"stream", "collect", "finish"
 static const char* const kSparsifyLaunchesMany[] = {"stream", "pick1", "gather",
                                                     "pick2",  "hist3", "pick3",
                                                     "groupscan", "emit"};
-constexpr int32_t kSparsifyNLaunchOne = 3, kSparsifyNLaunchMany = 8;
+// up to emit_lds_groups() groups, emit forms the group bases itself
+static const char* const kSparsifyLaunchesFold[] = {"stream", "pick1", "gather", "pick2",
+                                                    "hist3",  "pick3", "emit"};
+constexpr int32_t kSparsifyNLaunchOne = 3, kSparsifyNLaunchMany = 8, kSparsifyNLaunchFold = 7;
 // MSTopK: stream, count, refine x (passes - 1), emit
 static const char* const kApproxRefine[] = {"ms_refine1", "ms_refine2", "ms_refine3",
                                             "ms_refine4", "ms_refine5", "ms_refine6",
@@ -154,7 +157,8 @@ struct tkef_sparsify_plan_s {
   int32_t ms_passes() const { return ms_passes_for(ms_rounds); }
   int32_t nlaunch() const {
     if (mode == TKEF_APPROX) return 2 + ms_passes();
-    return ngroups == 1 ? kSparsifyNLaunchOne : kSparsifyNLaunchMany;
+    if (ngroups == 1) return kSparsifyNLaunchOne;
+    return ngroups <= emit_lds_groups() ? kSparsifyNLaunchFold : kSparsifyNLaunchMany;
   }
   void* bound_ws = nullptr;
   hipEvent_t* events = nullptr;
@@ -406,7 +410,8 @@ extern "C" const char* tkef_sparsify_plan_launch_name(tkef_sparsify_plan plan, i
     if (i == plan->nlaunch() - 1) return "ms_emit";
     return kApproxRefine[i - 2];
   }
-  return plan->ngroups == 1 ? kSparsifyLaunchesOne[i] : kSparsifyLaunchesMany[i];
+  if (plan->ngroups == 1) return kSparsifyLaunchesOne[i];
+  return plan->ngroups <= emit_lds_groups() ? kSparsifyLaunchesFold[i] : kSparsifyLaunchesMany[i];
 }
 
 extern "C" int tkef_sparsify_plan_set_approx(tkef_sparsify_plan plan, int32_t n_search,
@@ -558,11 +563,12 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
       e = launch_hist3(tiles, nt, st, summ, nl, lpt, plan->cand_grid, cand, meta, hist3, s,
                        tr.at(li++));
     if (e == hipSuccess) e = launch_pick(3, groups, st, hist3, 1, ng, s, tr.at(li++));
-    if (e == hipSuccess) e = launch_groupscan(groups, st, ng, gbase, s, tr.at(li++));
+    const bool fold = ng <= emit_lds_groups();
+    if (e == hipSuccess && !fold) e = launch_groupscan(groups, st, ng, gbase, s, tr.at(li++));
     if (e == hipSuccess)
       e = launch_emit(tiles, nt, groups, st, summ, nl, lpt, plan->cand_grid, cand, meta, gbase,
-                      flags2, idx_out, val_out, val16, status, clear_next, clear_words, s,
-                      tr.at(li++));
+                      flags2, idx_out, val_out, val16, status, clear_next, clear_words,
+                      fold ? ng : 0, s, tr.at(li++));
   }
   if (e != hipSuccess) {
     plan->needs_clear = true;

@@ -146,7 +146,7 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
                        int32_t grid, const uint32_t* cand, const uint32_t* meta,
                        const uint32_t* base, uint64_t* flags, int32_t* idx_out, void* val_out,
                        int val16, uint32_t* status, uint32_t* clear_next, int64_t clear_words,
-                       hipStream_t s, const Ev& ev);
+                       int32_t fold_ngroups, hipStream_t s, const Ev& ev);
 // MSTopK (one group, TKEF_APPROX). st[b] = state before pass b (written by
 // pass b's kernel), st[passes] = the final state (written by emit).
 hipError_t launch_ms_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,
@@ -176,6 +176,7 @@ int32_t select_max_groups();
 int32_t select_block();
 int32_t collect_block(int64_t nlines);  // collect and finish (one exact selection group)
 int32_t select_max_lpt();
+int32_t emit_lds_groups();  // groups whose bases k_emit can form itself
 
 hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, int32_t P,
                       int32_t d, int32_t ntiles_u, int32_t* seg, uint32_t* status,

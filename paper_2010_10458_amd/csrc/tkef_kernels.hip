@@ -476,6 +476,7 @@ static_assert((1 << kCandShift) == kTile, "candidate encoding");
 constexpr uint64_t kFlagValid = 1ull << 63, kFlagVal = (1ull << 63) - 1;
 constexpr uint32_t kSpinLimit = 1u << 22;
 constexpr int kStage = 8;       // candidates a thread stages in LDS
+constexpr int kEmitLdsGroups = kSBlock;  // group bases k_emit forms itself (8 KB of LDS)
 constexpr int kGStage = 24;     // ... in gather (dense per-tensor selections; 144 KB)
 
 __device__ __forceinline__ uint64_t flag_load(const uint64_t* p) {
@@ -1380,12 +1381,23 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
                                                   void* __restrict__ val_out, int val16,
                                                   uint32_t* __restrict__ status,
                                                   uint32_t* __restrict__ clear_next,
-                                                  int64_t clear_words) {
+                                                  int64_t clear_words, int32_t fold_ngroups) {
   __shared__ uint32_t wsum[2 * kSWaves];
   __shared__ uint64_t red[kSWaves];
   __shared__ int32_t stage_code[kStage * kSBlock];  // [slot][thread]: (tile << 13) | e
   __shared__ float stage_x[kStage * kSBlock];
+  __shared__ uint2 lbase[kEmitLdsGroups];
   const int tid = threadIdx.x;
+  // With fold_ngroups > 0 (at most kEmitLdsGroups groups) every workgroup
+  // forms the groups' bases itself (what k_groupscan writes into base[]):
+  // the groups' results are fetched now and scanned after pass 1.
+  uint32_t fgt = 0u, feq = 0u;
+  if (tid < fold_ngroups) {
+    const GroupState sg = st[tid];
+    const uint32_t kg = groups[tid].k;
+    fgt = (kg > sg.need) ? kg - sg.need : 0u;
+    feq = sg.need ? sg.n_eq : 0u;
+  }
   // clear the other copy of the zero-initialised scratch for the next run
 #pragma unroll 1
   for (int64_t i = (int64_t)blockIdx.x * kSBlock + tid; i < clear_words;
@@ -1424,6 +1436,11 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
   auto at_least_T = [&](int g, uint32_t k) -> bool { return k >= T_of(g); };
   if (ov) walk_mask(ls, mask, at_least_T, count);
   else walk_cands(tiles, ntiles, cand, cb, ce, count);
+  if (fold_ngroups > 0) {  // (uniform; its barriers also order lbase for the writes)
+    uint2 gtot;
+    const uint2 gx = block_scan2<kSBlock>(fgt, feq, wsum, &gtot);
+    if (tid < fold_ngroups) lbase[tid] = gx;
+  }
   uint2 tot;
   const uint2 x2 = block_scan2<kSBlock>(gt, eq, wsum, &tot);
   const uint64_t pre = group_prefix(flags, (uint64_t)tot.x | ((uint64_t)tot.y << 31), red, status);
@@ -1437,7 +1454,8 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
     if (k < T) return;
     const GroupDesc gd = groups[g];
     const uint32_t need = st[g].need;
-    const uint32_t bg = base[2 * g], be = base[2 * g + 1];
+    const uint32_t bg = fold_ngroups > 0 ? lbase[g].x : base[2 * g];
+    const uint32_t be = fold_ngroups > 0 ? lbase[g].y : base[2 * g + 1];
     uint32_t pos = 0xFFFFFFFFu;
     if (k > T) {
       pos = (gtr - bg) + min(eqr - be, need);
@@ -2628,11 +2646,11 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
                        int32_t grid, const uint32_t* cand, const uint32_t* meta,
                        const uint32_t* base, uint64_t* flags, int32_t* idx_out, void* val_out,
                        int val16, uint32_t* status, uint32_t* clear_next, int64_t clear_words,
-                       hipStream_t s, const Ev& ev) {
+                       int32_t fold_ngroups, hipStream_t s, const Ev& ev) {
+  if (fold_ngroups > kEmitLdsGroups) return hipErrorInvalidValue;
   return launch(k_emit, dim3(grid), dim3(kSBlock), s, ev, tiles, ntiles, groups, st, summ, nlines,
                 lpt, reinterpret_cast<const uint2*>(cand), meta, base, flags, idx_out, val_out,
-                val16, status, clear_next,
-                clear_words);
+                val16, status, clear_next, clear_words, fold_ngroups);
 }
 
 hipError_t launch_ms_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,
@@ -2681,6 +2699,7 @@ int32_t collect_block(int64_t nlines) {
   return nlines <= kCSmallLines ? kCBlockSmall : kSBlock;
 }
 int32_t select_max_lpt() { return kSMaxLpt; }
+int32_t emit_lds_groups() { return kEmitLdsGroups; }
 
 hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, int32_t P,
                       int32_t d, int32_t ntiles_u, int32_t* seg, uint32_t* status,

@@ -149,6 +149,18 @@ def test_no_cpu_fallback_when_library_missing(tmp_path, monkeypatch):
         tk.lib()
 
 
+def test_per_tensor_launch_names():
+    """Per tensor: up to 1,024 groups the emit kernel forms the group bases
+    itself (seven kernels); beyond that a scan kernel does (eight)."""
+    p = tk.SparsifyPlan([10] * 5 + [40_000], mode=tk.PER_TENSOR, rho=0.1)
+    assert p.nlaunch == 7
+    assert p.launch_names() == ["stream", "pick1", "gather", "pick2", "hist3", "pick3", "emit"]
+    q = tk.SparsifyPlan([3] * 1100, mode=tk.PER_TENSOR, rho=0.5)
+    assert q.nlaunch == 8 and q.launch_names()[6:] == ["groupscan", "emit"]
+    g = tk.SparsifyPlan([3] * 1100, mode=tk.GLOBAL, rho=0.5)
+    assert g.launch_names() == ["stream", "collect", "finish"]
+
+
 def test_approx_plan_host_side():
     """MSTopK plans: parameters, kernel count and names, and the errors the
     host can see (no GPU needed)."""

@@ -137,6 +137,18 @@ def test_per_tensor_candidate_overflow_and_dense_threads():
     compare_with_oracle(dense, res, rho=0.4, mode=tk.PER_TENSOR, label="per-tensor rho 0.4")
 
 
+def test_per_tensor_many_groups():
+    """1,100 small tensors per tensor (more groups than emit forms bases for
+    itself: the group-scan kernel runs) and 1,000 (emit forms them)."""
+    rng = np.random.default_rng(311)
+    for T in (1100, 1000):
+        sizes = [int(n) for n in rng.integers(0, 300, T)]
+        grads = [(rng.standard_normal(n) * (1 + (t % 7))).astype(np.float32)
+                 for t, n in enumerate(sizes)]
+        res = [(rng.standard_normal(n) * 0.1).astype(np.float32) for n in sizes]
+        compare_with_oracle(grads, res, rho=0.05, mode=tk.PER_TENSOR, label=f"{T} groups")
+
+
 def test_unaligned_views():
     """Tensors that start off a 16-byte boundary take the scalar path."""
     import torch
