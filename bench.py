@@ -573,7 +573,11 @@ def main() -> int:
         "sparsify_us": round(sp_s * 1e6, 2),
         "sparsify_GBps": round(sp_bytes / sp_s / 1e9, 1),
         "sparsify_frac_hbm_peak": round(sp_bytes / sp_s / 1e9 / HBM_PEAK_GBPS, 4),
+        "sparsify_us_p10_p50_p90": [round(float(v) * 1e3, 2)
+                                    for v in np.percentile(sp_ms, [10, 50, 90])],
         "update_us": round(up_s * 1e6, 2),
+        "update_us_p10_p50_p90": [round(float(v) * 1e3, 2)
+                                  for v in np.percentile(up_ms, [10, 50, 90])],
         "update_GBps": round(up_bytes / up_s / 1e9, 1),
         "update_frac_hbm_peak": round(up_bytes / up_s / 1e9 / HBM_PEAK_GBPS, 4),
         "kernels_us": {k: round(v * 1e3, 2) for k, v in kern.items()},
