@@ -96,7 +96,9 @@ typedef struct tkef_sparsify_plan_s *tkef_sparsify_plan;
 
 /* Host only. numels: host array of T sizes (each >= 0, total in [1, 2^31-1]).
  * k > 0 gives an explicit k (TKEF_GLOBAL only, k <= total); k == 0 takes k
- * from rho. */
+ * from rho. The list takes ceil(numel_t / 8192) tiles per tensor, at most
+ * 2^18 in all (TKEF_ERANGE otherwise); one tensor of 2^31 - 1 elements takes
+ * exactly 2^18. */
 int tkef_sparsify_plan_create(const int64_t *numels, int32_t ntensors, int32_t mode,
                               double rho, int64_t k, tkef_sparsify_plan *plan_out);
 int tkef_sparsify_plan_destroy(tkef_sparsify_plan plan);

@@ -180,6 +180,9 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
   } else if (!(rho > 0.0 && rho <= 1.0) || !std::isfinite(rho)) {
     return TKEF_ERANGE;
   }
+  int64_t ntiles = 0;
+  for (int32_t t = 0; t < ntensors; ++t) ntiles += (numels[t] + kTile - 1) / kTile;
+  if (ntiles > kMaxTiles) return TKEF_ERANGE;
   tkef_sparsify_plan p = new (std::nothrow) tkef_sparsify_plan_s();
   if (!p) return TKEF_ENOMEM;
   try {
@@ -242,7 +245,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     const int64_t want = (p->nlines + sb * 256 - 1) / (sb * 256);
     int64_t lpt = 4;  // a power of two from 4 to select_max_lpt()
     while (lpt < want && lpt < select_max_lpt()) lpt *= 2;
-    if ((p->nlines + sb * lpt - 1) / (sb * lpt) > sg) throw std::bad_alloc();  // d < 2^31
+    if ((p->nlines + sb * lpt - 1) / (sb * lpt) > sg) throw std::bad_alloc();  // kMaxTiles
     p->sel_lpt = (int32_t)lpt;
     const int64_t g_lines = (p->nlines + sb * lpt - 1) / (sb * lpt);
     // Candidates are the positions at or above the level-1 threshold bin:

@@ -17,6 +17,13 @@ constexpr int kBlock = 256;
 constexpr int kTile = 8192;
 constexpr int kLine = 32;
 constexpr int kLinesPerTile = kTile / kLine;  // == kBlock: one line per thread
+// A sparsify tensor list may take at most kMaxTiles tiles (tensor t takes
+// ceil(numel_t / kTile)): the selection grids cover at most that many tiles'
+// summary lines, and the per-tensor and MSTopK selections carry a candidate as
+// (tile << 13) | position-in-tile in 32 bits. One tensor of 2^31 - 1
+// elements takes exactly kMaxTiles.
+constexpr int64_t kMaxTiles = (int64_t)1 << 18;
+static_assert(kMaxTiles * kTile <= (int64_t)1 << 32, "candidate code width");
 static_assert(kLinesPerTile == kBlock, "one summary line per thread");
 // The stream walks the tiles in units of kStreamUnit elements (a persistent
 // grid takes units round-robin).

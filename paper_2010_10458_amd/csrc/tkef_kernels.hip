@@ -473,6 +473,9 @@ constexpr int kSMaxLpt = 16;     // lines per thread at most
 static_assert(kLinesPerTile % kSMaxLpt == 0, "a thread's lines lie in one tile");
 constexpr int kCandShift = 13;   // log2(kTile)
 static_assert((1 << kCandShift) == kTile, "candidate encoding");
+static_assert((int64_t)kSMaxGroups * kSBlock * kSMaxLpt >= kMaxTiles * kLinesPerTile &&
+              (int64_t)kSMaxGroups * kCBlockSmall * kSMaxLpt >= kCSmallLines,
+              "the selection grids cover every tile of a list");
 constexpr uint64_t kFlagValid = 1ull << 63, kFlagVal = (1ull << 63) - 1;
 constexpr uint32_t kSpinLimit = 1u << 22;
 constexpr int kStage = 8;       // candidates a thread stages in LDS

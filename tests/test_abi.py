@@ -73,6 +73,13 @@ def test_sparsify_plan_validation():
     assert _create([10], k=11, rho=0.0) == tk.ERANGE
     assert _create([10], k=10, rho=0.0) == tk.OK
     assert _create([10], k=-1) == tk.ERANGE
+    # at most 2^18 tiles of 8,192 elements in a list, whatever the mode
+    mixed = [4096] * 2**17 + [1] * 2**17  # exactly 2^18 tiles
+    for mode in (tk.GLOBAL, tk.APPROX):
+        assert _create(mixed, mode=mode) == tk.OK
+    for mode in (tk.GLOBAL, tk.PER_TENSOR, tk.APPROX):
+        assert _create(mixed + [1], mode=mode) == tk.ERANGE
+    assert _create([2**31 - 8192, 8191], mode=tk.PER_TENSOR) == tk.OK
     assert _create([10, 5], mode=tk.PER_TENSOR, k=3) == tk.EINVAL
     L = tk.lib()
     assert L.tkef_sparsify_plan_create(None, 1, 0, 0.1, 0, None) == tk.EINVAL
