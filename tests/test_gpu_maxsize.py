@@ -32,23 +32,22 @@ def _i32(t):
     return t.view(torch.int32)
 
 
-def test_max_size_sparsify_and_plain_update():
+def _planted_input(dev):
+    """g ~ N(0, 1) and r ~ N(0, 1e-3) over 2^31 - 1 positions (torch's seeded
+    device generator), with N_TIES positions, the last eight among them, set
+    to x = +-q exactly. q is the magnitude whose expected count above it among
+    d standard normals is k - 10,000 (seven standard deviations below k), so
+    the planted tie class straddles the k-th place and the index rule splits
+    it."""
     from scipy.special import erfcinv
 
-    dev = need_gpu()
     d = D_MAX
     k = int(tk.k_from_rho(d, RHO))
-    assert k == 2_147_484
-    # A magnitude q whose expected count above it among d standard normals is
-    # k - 10,000 (seven standard deviations below k); N_TIES planted copies of
-    # +-q then straddle the k-th place, so the index rule splits them.
     q = float(np.float32(np.sqrt(2.0) * erfcinv((k - 10_000) / d)))
     rng = np.random.default_rng(2_010_104_580)
     planted = rng.choice(d - 8, size=N_TIES - 8, replace=False)
-    planted = np.concatenate([planted, np.arange(d - 8, d)])  # the last positions too
+    planted = np.concatenate([planted, np.arange(d - 8, d)])
     signs = np.where(rng.integers(0, 2, size=N_TIES) == 1, 1.0, -1.0).astype(np.float32)
-
-    announce(f"max size d={d}: generate")
     tg = torch.Generator(device=dev)
     tg.manual_seed(2_010_104_581)
     g = torch.randn(d, generator=tg, device=dev)
@@ -62,9 +61,19 @@ def test_max_size_sparsify_and_plain_update():
     ties = int((xa == q).sum())
     del xa
     assert above < k < above + ties, (above, ties, k)
+    return g, r, x, k, q, above, ties
 
-    announce(f"max size d={d}: sparsify k={k}")
-    plan = tk.SparsifyPlan([d], rho=RHO)
+
+@pytest.mark.parametrize("mode", [tk.GLOBAL, tk.PER_TENSOR])
+def test_max_size_sparsify(mode):
+    dev = need_gpu()
+    d = D_MAX
+    announce(f"max size d={d} mode={mode}: generate")
+    g, r, x, k, q, above, ties = _planted_input(dev)
+    assert k == 2_147_484
+
+    announce(f"max size d={d} mode={mode}: sparsify k={k}")
+    plan = tk.SparsifyPlan([d], mode=mode, rho=RHO)
     plan.bind([g], [r])
     idx, val = plan.execute()
     torch.cuda.synchronize()
@@ -91,24 +100,31 @@ def test_max_size_sparsify_and_plain_update():
     assert int(unsel_tie.sum()) == ties - (k - above)
     first_unsel_tie = int(torch.argmax(unsel_tie.to(torch.uint8)))
     assert last_sel_tie < first_unsel_tie, "ties not broken toward lower positions"
-    del x, r, unsel_tie, sel_tie, va
+    del x, r, unsel_tie, sel_tie, va, li, idx, val
     torch.cuda.empty_cache()
 
-    # plain update (mu = wd = 0) of 2^31 - 1 parameters with two lists: the
-    # selection above and a seeded list that includes the first and last
-    # positions
-    announce(f"max size d={d}: plain update P=2")
-    idx1 = np.unique(np.concatenate([rng.integers(0, d, size=5000), [0, d - 2, d - 1]]))
-    n1 = idx1.size
-    val1 = (rng.standard_normal(n1) * 0.01).astype(np.float32)
-    stride = max(k, n1)
+
+def test_max_size_plain_update():
+    """Plain update (mu = wd = 0) of 2^31 - 1 parameters with two seeded
+    ascending lists (2.1 M and 5 K entries) that both include the first and
+    the last positions."""
+    dev = need_gpu()
+    d = D_MAX
+    rng = np.random.default_rng(2_010_104_582)
+    ends = [0, d - 2, d - 1]
+    lists = [np.unique(np.concatenate([rng.integers(0, d, size=n), ends])).astype(np.int32)
+             for n in (2_150_000, 5_000)]
+    vals = [(rng.standard_normal(a.size) * 0.01).astype(np.float32) for a in lists]
+    stride = max(a.size for a in lists)
     idx_all = torch.zeros((2, stride), dtype=torch.int32, device=dev)
     val_all = torch.zeros((2, stride), dtype=torch.float32, device=dev)
-    idx_all[0, :k] = idx
-    val_all[0, :k] = val
-    idx_all[1, :n1] = torch.from_numpy(idx1.astype(np.int32)).to(dev)
-    val_all[1, :n1] = torch.from_numpy(val1).to(dev)
-    nnz = torch.tensor([k, n1], dtype=torch.int32, device=dev)
+    for p, (a, v) in enumerate(zip(lists, vals)):
+        idx_all[p, :a.size] = torch.from_numpy(a).to(dev)
+        val_all[p, :a.size] = torch.from_numpy(v).to(dev)
+    nnz = torch.tensor([a.size for a in lists], dtype=torch.int32, device=dev)
+    announce(f"max size d={d}: plain update P=2")
+    tg = torch.Generator(device=dev)
+    tg.manual_seed(2_010_104_583)
     w = torch.randn(d, generator=tg, device=dev).mul_(0.1)
     w0 = w.clone()
     up = tk.UpdatePlan([d], P=2, stride=stride)
@@ -119,8 +135,8 @@ def test_max_size_sparsify_and_plain_update():
     del up
 
     G = torch.zeros(d, device=dev)
-    G.index_add_(0, li, val)
-    G.index_add_(0, idx_all[1, :n1].long(), val_all[1, :n1])
+    for p, a in enumerate(lists):
+        G.index_add_(0, idx_all[p, :a.size].long(), val_all[p, :a.size])
     step = G.mul_(lr)                # fl32(lr * G)
     w_ref = w0.sub_(step)            # fl32(w - fl32(lr * G)); untouched: w - 0 = w
     assert torch.equal(_i32(w), _i32(w_ref)), "plain update differs from its definition"
