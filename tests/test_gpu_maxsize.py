@@ -142,3 +142,48 @@ def test_max_size_plain_update():
     assert torch.equal(_i32(w), _i32(w_ref)), "plain update differs from its definition"
     del w, w0, G, idx_all, val_all
     torch.cuda.empty_cache()
+
+
+def test_max_size_mstopk():
+    """MSTopK (Alg. 1, N = 30) over 2^31 - 1 positions, through its
+    invariants: the k1 positions at or above thres1 are all selected, the
+    band {thres2 <= |x| < thres1} holds k2 - k1 positions, and the selection
+    takes k - k1 consecutive band members (in position order) from the drawn
+    offset; idx, val and the residual obey the sparsify contract."""
+    dev = need_gpu()
+    d = D_MAX
+    announce(f"max size d={d}: MSTopK generate")
+    g, r, x, k, q, above, ties = _planted_input(dev)
+    del q, above, ties
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    announce(f"max size d={d}: MSTopK k={k}")
+    plan = tk.SparsifyPlan([d], mode=tk.APPROX, rho=RHO, n_search=30)
+    plan.bind([g], [r])
+    idx, val = plan.execute(status=status, window_word=0x9E3779B97F4A7C15)
+    torch.cuda.synchronize()
+    res = plan.approx_result()
+    del plan, g
+    torch.cuda.empty_cache()
+    assert int(status.item()) == 0
+
+    k1, k2, off, take = res["k1"], res["k2"], res["offset"], res["take"]
+    assert 0 <= k1 <= k <= k2 and take == k - k1 and 0 <= off <= k2 - k1 - take, res
+    li = idx.long()
+    assert idx.numel() == k
+    assert bool((li[1:] > li[:-1]).all()), "indices not strictly ascending"
+    assert torch.equal(_i32(val), _i32(x[li])), "val != x[idx]"
+    assert bool((_i32(r[li]) == 0).all()), "selected residual entries must be +0.0"
+    keys = _i32(x) & 0x7FFFFFFF
+    ks = keys[li]
+    assert int((ks >= res["key1"]).sum()) == k1
+    assert int((keys >= res["key1"]).sum()) == k1, "a position above thres1 left out"
+    in_band = (keys >= res["key2"]) & (keys < res["key1"])
+    assert int(in_band.sum()) == k2 - k1
+    band = torch.nonzero(in_band).squeeze(1)
+    del in_band, keys
+    sel_band = li[(ks >= res["key2"]) & (ks < res["key1"])]
+    assert torch.equal(sel_band, band[off:off + take]), "band window is not consecutive"
+    x[li] = 0.0
+    assert torch.equal(_i32(r), _i32(x)), "unselected residual != x"
+    del x, r, band, sel_band, li, idx, val
+    torch.cuda.empty_cache()
