@@ -139,9 +139,11 @@ def test_per_tensor_candidate_overflow_and_dense_threads():
 
 def test_per_tensor_many_groups():
     """1,100 small tensors per tensor (more groups than emit forms bases for
-    itself: the group-scan kernel runs) and 1,000 (emit forms them)."""
+    itself: the group-scan kernel runs), 5,000 (more groups than the
+    selection grids have workgroups, and several rounds of the group scan) and
+    1,000 (emit forms them)."""
     rng = np.random.default_rng(311)
-    for T in (1100, 1000):
+    for T in (1100, 5000, 1000):
         sizes = [int(n) for n in rng.integers(0, 300, T)]
         grads = [(rng.standard_normal(n) * (1 + (t % 7))).astype(np.float32)
                  for t, n in enumerate(sizes)]
