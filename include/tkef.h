@@ -280,9 +280,13 @@ int tkef_sparse_aggregate(float *const *outs, const int64_t *numels, int32_t nte
  *
  * A layer is one tensor of the update plan's list. Norms are Euclidean, summed
  * in double (in a fixed order: the same inputs give the same rates on every
- * run); when ||w_l|| or ||g_l|| is zero the rate is gamma * eta (gamma, eta
- * and eps enter the rate in double). The step, in binary32 with the rate and
- * eps each rounded to binary32 once, for every position:
+ * run); gamma, eta and eps enter the rate in double, and eps (the weight
+ * decay) must be >= 0. The rate is the equation's value wherever its
+ * denominator is positive: 0 for ||w_l|| = 0 < ||g_l||, gamma * eta / eps for
+ * ||g_l|| = 0 < ||w_l||. A zero denominator (g_l = 0 and eps * w_l = 0, where
+ * the equation is undefined) gives rate 0; D below is then zero, so the step
+ * does not depend on it. The step, in binary32 with the rate and eps each
+ * rounded to binary32 once, for every position:
  *   D = g + eps * w;  U = rate * D;
  *   with momentum (mu != 0, momentum bound):  b = mu * b + U;  w = w - b
  *   without:                                  w = w - U
@@ -294,7 +298,7 @@ int tkef_sparse_aggregate(float *const *outs, const int64_t *numels, int32_t nte
  * (names from tkef_lars_launch_name(0, i); the timing hook of
  * tkef_update_plan_set_events takes 5 events). rate_out: optional device
  * array of ntensors doubles receiving the rates. mu != 0 needs momentum
- * buffers bound. TKEF_ERANGE for non-finite gamma, eta, eps or mu. */
+ * buffers bound. TKEF_ERANGE for non-finite gamma, eta, eps or mu, or eps < 0. */
 int tkef_lars_update_execute(tkef_update_plan plan, const int32_t *idx, const void *val,
                              const int32_t *nnz, double gamma, double eta, double eps,
                              float mu, double *rate_out, void *ws, size_t ws_bytes,

@@ -14,10 +14,13 @@ Readings (each also listed with the design notes):
   * norms are Euclidean, in double: the squares of the binary32 values are
     exact in double, their sum is rounded once (math.fsum), then the square
     root; the rate is (gamma * eta * ||w||) / (||g|| + eps * ||w||) in double;
-  * when ||w|| or ||g|| is zero the trust ratio ||w|| / (||g|| + eps ||w||)
-    is taken as 1 (the rate is gamma * eta), as LARS implementations do: a
-    zero weight norm would freeze the layer and a zero gradient norm would
-    give 1 / eps;
+  * the equation is taken as printed wherever its denominator is positive:
+    ||w|| = 0 < ||g|| gives rate 0, ||g|| = 0 < ||w|| gives gamma * eta / eps;
+  * eps >= 0 (a weight decay). The denominator ||g|| + eps ||w|| is then zero
+    only when g = 0 and eps w = 0 on the whole layer (0/0, or ||w|| / 0 with
+    eps = 0), where the equation is undefined; the rate is read as 0 there.
+    D = g + eps w is then zero at every position, so any finite rate gives
+    the same step;
   * the step is binary32, one rounding per operation, with lambda rounded to
     binary32 once: D = g + eps * w, U = lambda * D, b = mu * b + U, w = w - U
     (or w = w - b with momentum), b starting at 0;
@@ -39,9 +42,12 @@ def layer_norm(v) -> float:
 
 
 def lars_rate(nw: float, ng: float, gamma: float, eta: float, eps: float) -> float:
-    if nw > 0.0 and ng > 0.0:
-        return (gamma * eta * nw) / (ng + eps * nw)
-    return gamma * eta
+    if eps < 0.0:
+        raise ValueError("eps (the weight decay) must be >= 0")
+    den = ng + eps * nw
+    if den > 0.0:
+        return (gamma * eta * nw) / den
+    return 0.0
 
 
 def lars_rates(ws: Sequence[np.ndarray], gs: Sequence[np.ndarray], gamma: float, eta: float,

@@ -841,7 +841,7 @@ extern "C" int tkef_lars_update_execute(tkef_update_plan plan, const int32_t* id
                                         void* ws, size_t ws_bytes, uint32_t* status,
                                         hipStream_t s) {
   if (!plan) return TKEF_EINVAL;
-  if (!finite_all(gamma, eta, eps) || !std::isfinite(mu)) return TKEF_ERANGE;
+  if (!finite_all(gamma, eta, eps) || !(eps >= 0.0) || !std::isfinite(mu)) return TKEF_ERANGE;
   if (mu != 0.0f && !plan->has_mom) return TKEF_EINVAL;
   if (!ws || ws_bytes < plan->ws_bytes || !aligned_ws(ws)) return TKEF_EWORKSPACE;
   if (plan->bound_ws != ws) return TKEF_ESTATE;
@@ -877,7 +877,7 @@ extern "C" int tkef_lars_rates_execute(tkef_update_plan plan, double gamma, doub
                                        double eps, double* rate_out, void* ws, size_t ws_bytes,
                                        hipStream_t s) {
   if (!plan) return TKEF_EINVAL;
-  if (!finite_all(gamma, eta, eps)) return TKEF_ERANGE;
+  if (!finite_all(gamma, eta, eps) || !(eps >= 0.0)) return TKEF_ERANGE;
   if (!ws || ws_bytes < plan->ws_bytes || !aligned_ws(ws)) return TKEF_EWORKSPACE;
   if (plan->bound_ws != ws || !plan->has_grads) return TKEF_ESTATE;
   char* base = static_cast<char*>(ws);

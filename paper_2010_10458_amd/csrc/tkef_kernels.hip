@@ -1900,8 +1900,11 @@ __global__ __launch_bounds__(kUBlock) void k_lars_norm_dense(
 }
 
 // One workgroup per tensor: its pairs summed in a fixed order, the norms,
-// and the rate gamma eta ||w|| / (||g|| + eps ||w||) (gamma eta when either
-// norm is zero).
+// and the rate gamma eta ||w|| / (||g|| + eps ||w||) of Eq. lars wherever the
+// denominator is positive (0 for a zero weight norm, gamma eta / eps for a
+// zero gradient norm). With eps >= 0 the denominator is zero only when g = 0
+// and eps w = 0 on the whole layer; the rate is 0 there (every finite rate
+// gives the same step, since D = g + eps w = 0).
 __global__ __launch_bounds__(kUBlock) void k_lars_rates(const int32_t* __restrict__ tpair,
                                                         const double2* __restrict__ part,
                                                         double gamma, double eta, double eps,
@@ -1919,8 +1922,8 @@ __global__ __launch_bounds__(kUBlock) void k_lars_rates(const int32_t* __restric
   const double2 r = ublock_sum2(sw, sg, lred);
   if (tid == 0) {
     const double nw = sqrt(r.x), ng = sqrt(r.y);
-    const double lam = (nw > 0.0 && ng > 0.0) ? (gamma * eta * nw) / (ng + eps * nw)
-                                               : gamma * eta;
+    const double den = ng + eps * nw;
+    const double lam = den > 0.0 ? (gamma * eta * nw) / den : 0.0;
     rate[t] = lam;
     if (rate_out) rate_out[t] = lam;
   }

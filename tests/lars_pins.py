@@ -12,7 +12,10 @@ Sources of truth:
     w = 2, g = 1/2, eps = 1/4, gamma = eta = 1), with and without momentum;
   * layer independence: a layer's rate does not depend on the other layers in
     the list;
-  * the zero-norm convention (rate gamma eta);
+  * Eq. (lars) at zero norms: ||w|| = 0 < ||g|| gives 0 and ||g|| = 0 < ||w||
+    gives gamma eta / eps (the equation's value, checked against exact
+    rationals), and a hand-worked dyadic step for the zero-gradient layer;
+    a zero denominator (0/0, or eps = 0 with g = 0) gives the reading's 0;
   * the step over several layers against the same step layer by layer;
   * a hand-worked case where binary32 rounding of the rate and of D decides
     the result (exactly 0 in binary32, about 2^-25 with wider arithmetic).
@@ -49,10 +52,31 @@ def pin_lars_norm_decimal(lars):
 
 
 def pin_lars_zero_norms(lars):
-    z = np.zeros(8, np.float32)
-    o = np.ones(8, np.float32)
-    for w, g in ((z, o), (o, z), (z, z)):
-        assert lars.lars_rates([w], [g], 0.5, 0.1, 0.01)[0] == 0.5 * 0.1
+    # n = 16 positions of 0 or 1: the norms are 0 or exactly 4
+    z = np.zeros(16, np.float32)
+    o = np.ones(16, np.float32)
+    # ||w|| = 0 < ||g||: gamma eta 0 / (4 + eps 0) = 0
+    for eps in (0.0, 0.25, 1e-4):
+        assert lars.lars_rates([z], [o], 0.5, 0.25, eps)[0] == 0.0
+    # ||g|| = 0 < ||w||: gamma eta 4 / (eps 4) = gamma eta / eps
+    for gamma, eta, eps in ((0.5, 0.25, 0.25), (0.001, 0.1, 5e-5), (2.0, 3.0, 1e-4)):
+        r = lars.lars_rates([o], [z], gamma, eta, eps)[0]
+        exact = Fraction(gamma) * Fraction(eta) / Fraction(eps)
+        assert abs(Fraction(r) - exact) <= exact * Fraction(1, 2 ** 50), (gamma, eta, eps, r)
+    assert lars.lars_rates([o], [z], 0.5, 0.25, 0.25)[0] == 0.5
+    # a zero denominator: 0/0, and ||w|| / 0 with eps = 0 (the reading: 0)
+    assert lars.lars_rates([z], [z], 0.5, 0.25, 0.25)[0] == 0.0
+    assert lars.lars_rates([o], [z], 0.5, 0.25, 0.0)[0] == 0.0
+    # the zero-gradient layer's step: rate 1/2, D = w / 4 = 1/4, U = 1/8,
+    # w' = 7/8 (every value dyadic, so exact); momentum 1/2 on b = 1:
+    # b' = 1/2 + 1/8 = 5/8, w' = 1 - 5/8 = 3/8
+    w2, _, rates = lars.lars_update([o], None, [z], 0.5, 0.25, 0.25, 0.0)
+    assert rates[0] == 0.5 and np.all(w2[0] == np.float32(0.875))
+    w3, b3, _ = lars.lars_update([o], [np.ones(16, np.float32)], [z], 0.5, 0.25, 0.25, 0.5)
+    assert np.all(b3[0] == np.float32(0.625)) and np.all(w3[0] == np.float32(0.375))
+    # the zero-weight layer does not move (rate 0, D = g, U = 0)
+    w4, _, _ = lars.lars_update([z], None, [o], 0.5, 0.25, 0.25, 0.0)
+    assert np.all(w4[0] == 0.0)
 
 
 def pin_lars_worked_steps(lars):
