@@ -33,7 +33,7 @@
 extern "C" {
 #endif
 
-#define TKEF_VERSION 10000 /* major * 10000 + minor * 100 + patch */
+#define TKEF_VERSION 10100 /* major * 10000 + minor * 100 + patch */
 
 /* return codes */
 #define TKEF_OK 0
@@ -59,7 +59,8 @@ extern "C" {
 #define TKEF_STATUS_NAN 1u         /* sparsify saw a NaN in g + r */
 #define TKEF_STATUS_UNSORTED 2u    /* an update index list is not ascending */
 #define TKEF_STATUS_INDEX_RANGE 4u /* an update index lies outside [0, d) */
-#define TKEF_STATUS_TIMEOUT 8u     /* a bounded wait between workgroups gave up (results invalid) */
+#define TKEF_STATUS_TIMEOUT 8u     /* a bounded wait between workgroups gave up: results invalid
+                                       (the workgroups that gave up wrote no output) */
 #define TKEF_STATUS_NONFINITE 16u  /* MSTopK saw an infinity or NaN in g + r (it then takes
                                        the first k positions) */
 
@@ -179,15 +180,36 @@ int tkef_sparsify_plan_set_events(tkef_sparsify_plan plan, hipEvent_t *events,
                                   int32_t n_events);
 const char *tkef_sparsify_plan_launch_name(tkef_sparsify_plan plan, int32_t i);
 
-/* One-shot convenience: create + bind + execute + destroy. Synchronizes
- * `stream` once (during bind). */
+/* One-shot calls (the call shape sparsify(grad, residual, rho) -> idx, val):
+ * create + bind + execute + destroy; each synchronizes `stream` once (during
+ * bind). tkef_sparsify_workspace reports the workspace of a call with the
+ * same numels, mode, rho and k, and its number of pairs (k_total). */
 int tkef_sparsify_workspace(const int64_t *numels, int32_t ntensors, int32_t mode,
                             double rho, int64_t k, size_t *workspace_bytes,
                             int64_t *k_total);
+
+/* Sparsify of a tensor list (the operation above; mode TKEF_GLOBAL,
+ * TKEF_PER_TENSOR or TKEF_APPROX with N = 30 and window word 0). k > 0:
+ * explicit k (not TKEF_PER_TENSOR); k == 0: k from rho. val_format: TKEF_VAL_F32
+ * or TKEF_VAL_F16. idx_out / val_out (device) receive k_total pairs, grouped
+ * by selection group in tensor order. counts_out: optional host array that
+ * receives the k of each selection group (1 entry, or T for
+ * TKEF_PER_TENSOR), written before any GPU work. */
 int tkef_sparsify(const float *const *grads, float *const *residuals,
                   const int64_t *numels, int32_t ntensors, int32_t mode, double rho,
-                  int64_t k, int32_t *idx_out, void *val_out, void *ws,
-                  size_t ws_bytes, uint32_t *status, hipStream_t stream);
+                  int64_t k, int32_t val_format, int32_t *idx_out, void *val_out,
+                  int64_t *counts_out, void *ws, size_t ws_bytes, uint32_t *status,
+                  hipStream_t stream);
+
+/* One flat tensor with an explicit k: Alg. 1's interface (x, k) -> (values,
+ * indices), Sec. 3.1, with the exact selection and error feedback above. g, r:
+ * device, d elements each (1 <= d <= 2^31 - 1, not overlapping); 1 <= k <= d
+ * (TKEF_ERANGE otherwise). idx_out (int32) and val_out (binary32): device, k
+ * entries. ws: at least what tkef_sparsify_workspace(&d, 1, TKEF_GLOBAL, 0.0,
+ * k, ...) reports. status: optional device word. Synchronizes `stream` once. */
+int tkef_sparsify1(const float *g, float *r, int64_t d, int64_t k, int32_t *idx_out,
+                   float *val_out, void *ws, size_t ws_bytes, uint32_t *status,
+                   hipStream_t stream);
 
 /* ========================================================================
  * Sparse aggregate + merged multi-tensor SGD update
@@ -272,6 +294,25 @@ int tkef_sparse_aggregate(float *const *outs, const int64_t *numels, int32_t nte
                           const int32_t *idx, const void *val, int32_t val_format, int32_t P,
                           int64_t stride, const int32_t *nnz, void *ws, size_t ws_bytes,
                           uint32_t *status, hipStream_t stream);
+
+/* Aggregate + update over P separate worker lists (the lists that Alg. 2
+ * gathers from the nodes, each added at its indices, Sec. 3.2; then the
+ * update of Eq. (1) above): the call shape sparse_aggregate_update(params,
+ * {idx, val} x P, lr). idx[p], val[p]: host array of P device pointers, worker
+ * p's nnz[p] global positions (int32, ascending, repeats summed) and binary32
+ * values; nnz: host array of P counts (>= 0; a list with nnz[p] == 0 may have
+ * null pointers). params / momentum / numels / lr / mu / wd as in
+ * tkef_sparse_aggregate_update (momentum may be NULL iff mu == 0; mu == wd
+ * == 0 takes the sparse plain step). ws: at least tkef_aggregate_workspace();
+ * the host arrays are staged into it (a table of 32 bytes per worker).
+ * Synchronizes `stream` once; the library allocates nothing. */
+int tkef_aggregate_workspace(const int64_t *numels, int32_t ntensors, int32_t P,
+                             size_t *workspace_bytes);
+int tkef_aggregate_update(float *const *params, float *const *momentum,
+                          const int64_t *numels, int32_t ntensors,
+                          const int32_t *const *idx, const float *const *val,
+                          const int64_t *nnz, int32_t P, float lr, float mu, float wd,
+                          void *ws, size_t ws_bytes, uint32_t *status, hipStream_t stream);
 
 /* ========================================================================
  * LARS (Eq. lars: the layer-wise rate rate_l = gamma * eta * ||w_l|| /

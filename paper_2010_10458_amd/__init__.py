@@ -45,6 +45,21 @@ class TkefError(RuntimeError):
         self.code = code
 
 
+class TkefStatusError(RuntimeError):
+    """A call finished with bits set in its device status word."""
+
+    NAMES = {STATUS_NAN: "NaN in g + r (selection unspecified)",
+             STATUS_UNSORTED: "an index list is not ascending",
+             STATUS_INDEX_RANGE: "an index lies outside [0, d)",
+             STATUS_TIMEOUT: "a wait between workgroups gave up (results invalid)",
+             STATUS_NONFINITE: "MSTopK saw a non-finite value (it took the first k positions)"}
+
+    def __init__(self, fn: str, bits: int):
+        what = "; ".join(m for b, m in self.NAMES.items() if bits & b) or "unknown bits"
+        super().__init__(f"{fn}: device status {bits:#x}: {what}")
+        self.bits = bits
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -68,8 +83,12 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
         "tkef_sparsify_plan_set_approx": ([vp, i32, ctypes.c_uint64], ctypes.c_int),
         "tkef_sparsify_approx_result": ([vp, vp, P(f64), P(i64), vp], ctypes.c_int),
         "tkef_sparsify_workspace": ([P(i64), i32, i32, f64, i64, P(sz), P(i64)], ctypes.c_int),
-        "tkef_sparsify": ([P(vp), P(vp), P(i64), i32, i32, f64, i64, vp, vp, vp, sz, vp, vp],
-                          ctypes.c_int),
+        "tkef_sparsify": ([P(vp), P(vp), P(i64), i32, i32, f64, i64, i32, vp, vp, P(i64), vp,
+                           sz, vp, vp], ctypes.c_int),
+        "tkef_sparsify1": ([vp, vp, i64, i64, vp, vp, vp, sz, vp, vp], ctypes.c_int),
+        "tkef_aggregate_workspace": ([P(i64), i32, i32, P(sz)], ctypes.c_int),
+        "tkef_aggregate_update": ([P(vp), P(vp), P(i64), i32, P(vp), P(vp), P(i64), i32, f32,
+                                   f32, f32, vp, sz, vp, vp], ctypes.c_int),
         "tkef_update_plan_create": ([P(i64), i32, i32, i64, P(vp)], ctypes.c_int),
         "tkef_update_plan_destroy": ([vp], ctypes.c_int),
         "tkef_update_plan_info": ([vp, P(sz), P(i64), P(i32)], ctypes.c_int),
@@ -111,6 +130,19 @@ def lib() -> ctypes.CDLL:
 def _check(fn: str, rc: int) -> None:
     if rc != OK:
         raise TkefError(fn, rc, lib().tkef_strerror(rc).decode())
+
+
+def _new_status(dev) -> torch.Tensor:
+    return torch.zeros(1, dtype=torch.int32, device=dev)
+
+
+def _raise_on_status(fn: str, status: torch.Tensor, stream=None) -> None:
+    """Synchronizes the stream and raises TkefStatusError if any status bit is
+    set."""
+    (stream or torch.cuda.current_stream()).synchronize()
+    bits = int(status.item()) & 0xFFFFFFFF
+    if bits:
+        raise TkefStatusError(fn, bits)
 
 
 def strerror(code: int) -> str:
@@ -165,7 +197,11 @@ class SparsifyPlan:
     """Plan for sparsifying a fixed list of tensor sizes (see tkef.h)."""
 
     def __init__(self, numels: Sequence[int], mode: int = GLOBAL, rho: Optional[float] = None,
-                 k: Optional[int] = None, val_dtype=torch.float32, n_search: int = 30):
+                 k: Optional[int] = None, val_dtype=torch.float32, n_search: int = 30,
+                 check: bool = False):
+        """check=True: every execute without a caller status word uses its
+        own, synchronizes and raises TkefStatusError on any status bit."""
+        self.check = bool(check)
         self._numels = [int(n) for n in numels]
         self._h = ctypes.c_void_p()
         L = lib()
@@ -251,10 +287,15 @@ class SparsifyPlan:
             raise ValueError("output buffers too small")
         if idx_out.dtype != torch.int32 or val_out.dtype != self.val_dtype:
             raise ValueError("idx_out must be int32 and val_out of the plan's value dtype")
+        own = self.check and status is None
+        if own:
+            status = _new_status(dev)
         _check("tkef_sparsify_execute", lib().tkef_sparsify_execute(
             self._h, self.ws.data_ptr(), self.ws.numel(), idx_out.data_ptr(),
             val_out.data_ptr(), status.data_ptr() if status is not None else None,
             _stream_handle(stream)))
+        if own:
+            _raise_on_status("tkef_sparsify_execute", status, stream)
         return idx_out[: self.k_total], val_out[: self.k_total]
 
 
@@ -277,7 +318,12 @@ LARS_DENSE_LAUNCHES = ["lars_norm_dense", "lars_rates"]
 class UpdatePlan:
     """Plan for the sparse aggregate + SGD update of a fixed parameter list."""
 
-    def __init__(self, numels: Sequence[int], P: int, stride: int, val_dtype=torch.float32):
+    def __init__(self, numels: Sequence[int], P: int, stride: int, val_dtype=torch.float32,
+                 check: bool = False):
+        """check=True: every execute / aggregate / lars_execute without a
+        caller status word uses its own, synchronizes and raises
+        TkefStatusError on any status bit."""
+        self.check = bool(check)
         self._numels = [int(n) for n in numels]
         self.P, self.stride = int(P), int(stride)
         self._h = ctypes.c_void_p()
@@ -341,15 +387,22 @@ class UpdatePlan:
         if nnz is not None and (nnz.dtype != torch.int32 or nnz.numel() < self.P or not nnz.is_cuda):
             raise ValueError("nnz must be a CUDA int32 tensor of P counts")
 
+    def _status(self, status):
+        own = self.check and status is None
+        return (_new_status(self.ws.device) if own else status), own
+
     def execute(self, idx: torch.Tensor, val: torch.Tensor, lr: float, mu: float = 0.0,
                 wd: float = 0.0, nnz: Optional[torch.Tensor] = None,
                 status: Optional[torch.Tensor] = None, stream=None) -> None:
         self._check_lists(idx, val, nnz)
+        status, own = self._status(status)
         _check("tkef_update_execute", lib().tkef_update_execute(
             self._h, idx.data_ptr(), val.data_ptr(),
             nnz.data_ptr() if nnz is not None else None, float(lr), float(mu), float(wd),
             self.ws.data_ptr(), self.ws.numel(),
             status.data_ptr() if status is not None else None, _stream_handle(stream)))
+        if own:
+            _raise_on_status("tkef_update_execute", status, stream)
 
     def lars_execute(self, idx: torch.Tensor, val: torch.Tensor, gamma: float, eta: float,
                      eps: float, mu: float = 0.0, nnz: Optional[torch.Tensor] = None,
@@ -360,11 +413,14 @@ class UpdatePlan:
         self._check_lists(idx, val, nnz)
         if rates is None:
             rates = torch.empty(len(self._numels), dtype=torch.float64, device=self.ws.device)
+        status, own = self._status(status)
         _check("tkef_lars_update_execute", lib().tkef_lars_update_execute(
             self._h, idx.data_ptr(), val.data_ptr(),
             nnz.data_ptr() if nnz is not None else None, float(gamma), float(eta), float(eps),
             float(mu), rates.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
             status.data_ptr() if status is not None else None, _stream_handle(stream)))
+        if own:
+            _raise_on_status("tkef_lars_update_execute", status, stream)
         return rates
 
     def bind_grads(self, grads: Sequence[torch.Tensor], stream=None) -> "UpdatePlan":
@@ -399,25 +455,133 @@ class UpdatePlan:
         """Writes the sum of the P lists into the bound tensors (every
         position; zero where no list names it)."""
         self._check_lists(idx, val, nnz)
+        status, own = self._status(status)
         _check("tkef_aggregate_execute", lib().tkef_aggregate_execute(
             self._h, idx.data_ptr(), val.data_ptr(),
             nnz.data_ptr() if nnz is not None else None, self.ws.data_ptr(), self.ws.numel(),
             status.data_ptr() if status is not None else None, _stream_handle(stream)))
+        if own:
+            _raise_on_status("tkef_aggregate_execute", status, stream)
 
 
 # ----------------------------------------------------------------------------
-# one-shot conveniences (the north-star call shapes)
+# one-shot calls: each calls the C one-shot of the same name. Without a caller
+# status word they use their own, synchronize and raise TkefStatusError when
+# the device reports a problem; with one, checking it is the caller's.
+
+def _ws(nbytes: int, dev) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=dev)
+
+
+def _finish(fn: str, status: Optional[torch.Tensor], own: bool) -> None:
+    if own:
+        _raise_on_status(fn, status)
+
 
 def sparsify(grads: Sequence[torch.Tensor], residuals: Sequence[torch.Tensor],
              rho: Optional[float] = None, mode: int = GLOBAL, k: Optional[int] = None,
-             status: Optional[torch.Tensor] = None, val_dtype=torch.float32
-             ) -> Tuple[torch.Tensor, torch.Tensor]:
+             status: Optional[torch.Tensor] = None, val_dtype=torch.float32,
+             return_counts: bool = False):
     """x = g + r; top-k of |x| (ties to the lower position); r <- x with the
     selected entries zeroed. Returns (idx int32, val of val_dtype: float32,
-    or float16 rounded to nearest even)."""
-    plan = SparsifyPlan([t.numel() for t in grads], mode=mode, rho=rho, k=k, val_dtype=val_dtype)
-    plan.bind(grads, residuals)
-    return plan.execute(status=status)
+    or float16 rounded to nearest even), and with return_counts the k of each
+    selection group."""
+    if len(grads) != len(residuals) or not grads:
+        raise ValueError("grads and residuals: equal, non-empty lists")
+    _check_f32_tensors(list(grads) + list(residuals), "sparsify")
+    numels = [t.numel() for t in grads]
+    if [t.numel() for t in residuals] != numels:
+        raise ValueError("residual sizes differ from the gradients'")
+    L = lib()
+    arr = _i64_array(numels)
+    rho_v, k_v = float(rho) if rho is not None else 0.0, int(k) if k else 0
+    nbytes, kt = ctypes.c_size_t(), ctypes.c_int64()
+    _check("tkef_sparsify_workspace", L.tkef_sparsify_workspace(
+        arr, len(numels), int(mode), rho_v, k_v, ctypes.byref(nbytes), ctypes.byref(kt)))
+    dev = grads[0].device
+    ngroups = len(numels) if mode == PER_TENSOR else 1
+    counts = (ctypes.c_int64 * ngroups)()
+    idx = torch.empty(max(kt.value, 1), dtype=torch.int32, device=dev)
+    val = torch.empty(max(kt.value, 1), dtype=val_dtype, device=dev)
+    own = status is None
+    if own:
+        status = _new_status(dev)
+    _check("tkef_sparsify", L.tkef_sparsify(
+        _ptr_array(grads), _ptr_array(residuals), arr, len(numels), int(mode), rho_v, k_v,
+        _val_format(val_dtype), idx.data_ptr(), val.data_ptr(), counts,
+        _ws(nbytes.value, dev).data_ptr(), max(nbytes.value, 256), status.data_ptr(),
+        _stream_handle(None)))
+    _finish("tkef_sparsify", status, own)
+    out = (idx[: kt.value], val[: kt.value])
+    return (*out, list(counts)) if return_counts else out
+
+
+def sparsify1(g: torch.Tensor, r: torch.Tensor, k: int,
+              status: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """One flat tensor, explicit k (tkef_sparsify1). Returns (idx, val)."""
+    _check_f32_tensors([g, r], "sparsify1")
+    d = g.numel()
+    if r.numel() != d:
+        raise ValueError("g and r differ in size")
+    L = lib()
+    nbytes = ctypes.c_size_t()
+    _check("tkef_sparsify_workspace", L.tkef_sparsify_workspace(
+        _i64_array([d]), 1, GLOBAL, 0.0, int(k), ctypes.byref(nbytes), None))
+    idx = torch.empty(max(int(k), 1), dtype=torch.int32, device=g.device)
+    val = torch.empty(max(int(k), 1), dtype=torch.float32, device=g.device)
+    own = status is None
+    if own:
+        status = _new_status(g.device)
+    _check("tkef_sparsify1", L.tkef_sparsify1(
+        g.data_ptr(), r.data_ptr(), d, int(k), idx.data_ptr(), val.data_ptr(),
+        _ws(nbytes.value, g.device).data_ptr(), max(nbytes.value, 256), status.data_ptr(),
+        _stream_handle(None)))
+    _finish("tkef_sparsify1", status, own)
+    return idx[: int(k)], val[: int(k)]
+
+
+def aggregate_update(params: Sequence[torch.Tensor],
+                     lists: Sequence[Tuple[torch.Tensor, torch.Tensor]], lr: float,
+                     momentum: Optional[Sequence[torch.Tensor]] = None, mu: float = 0.0,
+                     wd: float = 0.0, status: Optional[torch.Tensor] = None) -> None:
+    """Sum P separate worker lists [(idx_p int32, val_p float32), ...] (each
+    ascending) and apply w -= lr * (sum [+ wd * w], through momentum if
+    mu != 0): tkef_aggregate_update."""
+    _check_f32_tensors(list(params) + list(momentum or []), "aggregate_update")
+    numels = [t.numel() for t in params]
+    P = len(lists)
+    if P < 1:
+        raise ValueError("at least one worker list")
+    for i, v in lists:
+        if i.dtype != torch.int32 or v.dtype != torch.float32 or i.numel() != v.numel():
+            raise ValueError("each list: int32 idx and float32 val of one length")
+        if i.numel() and not (i.is_cuda and v.is_cuda and i.is_contiguous() and v.is_contiguous()):
+            raise ValueError("lists must be contiguous CUDA tensors")
+    L = lib()
+    arr = _i64_array(numels)
+    nbytes = ctypes.c_size_t()
+    _check("tkef_aggregate_workspace", L.tkef_aggregate_workspace(
+        arr, len(numels), P, ctypes.byref(nbytes)))
+    dev = params[0].device
+    own = status is None
+    if own:
+        status = _new_status(dev)
+    ip = (ctypes.c_void_p * P)(*[(i.data_ptr() if i.numel() else None) for i, _ in lists])
+    vp = (ctypes.c_void_p * P)(*[(v.data_ptr() if v.numel() else None) for _, v in lists])
+    _check("tkef_aggregate_update", L.tkef_aggregate_update(
+        _ptr_array(params), _ptr_array(momentum) if momentum is not None else None, arr,
+        len(numels), ip, vp, _i64_array([i.numel() for i, _ in lists]), P, float(lr),
+        float(mu), float(wd), _ws(nbytes.value, dev).data_ptr(), max(nbytes.value, 256),
+        status.data_ptr(), _stream_handle(None)))
+    _finish("tkef_aggregate_update", status, own)
+
+
+def _gathered(idx: torch.Tensor, val: torch.Tensor):
+    if idx.dim() == 1:
+        idx, val = idx.view(1, -1), val.view(1, -1)
+    if idx.shape != val.shape or idx.dtype != torch.int32:
+        raise ValueError("idx (int32) and val: (P, stride) of one shape")
+    return idx.contiguous(), val.contiguous(), idx.shape[0], idx.shape[1]
 
 
 def sparse_aggregate_update(params: Sequence[torch.Tensor], idx: torch.Tensor,
@@ -427,23 +591,52 @@ def sparse_aggregate_update(params: Sequence[torch.Tensor], idx: torch.Tensor,
                             nnz: Optional[torch.Tensor] = None,
                             status: Optional[torch.Tensor] = None) -> None:
     """Sum P workers' sparse gradients (idx, val: (P, stride) gathered layout)
-    and apply w -= lr * (sum [+ wd * w], through momentum if mu != 0)."""
-    if idx.dim() == 1:
-        idx, val = idx.view(1, -1), val.view(1, -1)
-    P, stride = idx.shape
-    plan = UpdatePlan([t.numel() for t in params], P=P, stride=stride, val_dtype=val.dtype)
-    plan.bind(params, momentum)
-    plan.execute(idx.contiguous(), val.contiguous(), lr=lr, mu=mu, wd=wd, nnz=nnz, status=status)
+    and apply w -= lr * (sum [+ wd * w], through momentum if mu != 0):
+    tkef_sparse_aggregate_update."""
+    _check_f32_tensors(list(params) + list(momentum or []), "sparse_aggregate_update")
+    idx, val, P, stride = _gathered(idx, val)
+    if val.dtype != torch.float32:
+        raise ValueError("values are float32 (binary16 lists: UpdatePlan)")
+    numels = [t.numel() for t in params]
+    L = lib()
+    arr = _i64_array(numels)
+    nbytes = ctypes.c_size_t()
+    _check("tkef_update_workspace", L.tkef_update_workspace(
+        arr, len(numels), P, stride, ctypes.byref(nbytes)))
+    dev = params[0].device
+    own = status is None
+    if own:
+        status = _new_status(dev)
+    _check("tkef_sparse_aggregate_update", L.tkef_sparse_aggregate_update(
+        _ptr_array(params), _ptr_array(momentum) if momentum is not None else None, arr,
+        len(numels), idx.data_ptr(), val.data_ptr(), P, stride,
+        nnz.data_ptr() if nnz is not None else None, float(lr), float(mu), float(wd),
+        _ws(nbytes.value, dev).data_ptr(), max(nbytes.value, 256), status.data_ptr(),
+        _stream_handle(None)))
+    _finish("tkef_sparse_aggregate_update", status, own)
 
 
 def sparse_aggregate(outs: Sequence[torch.Tensor], idx: torch.Tensor, val: torch.Tensor,
                      nnz: Optional[torch.Tensor] = None,
                      status: Optional[torch.Tensor] = None) -> None:
     """outs <- sum of P workers' sparse lists (idx, val: (P, stride) gathered
-    layout), densely: every position written, zero where no list names it."""
-    if idx.dim() == 1:
-        idx, val = idx.view(1, -1), val.view(1, -1)
-    P, stride = idx.shape
-    plan = UpdatePlan([t.numel() for t in outs], P=P, stride=stride, val_dtype=val.dtype)
-    plan.bind(outs)
-    plan.aggregate(idx.contiguous(), val.contiguous(), nnz=nnz, status=status)
+    layout), densely: every position written, zero where no list names it
+    (tkef_sparse_aggregate; float32 or float16 values)."""
+    _check_f32_tensors(list(outs), "sparse_aggregate")
+    idx, val, P, stride = _gathered(idx, val)
+    numels = [t.numel() for t in outs]
+    L = lib()
+    arr = _i64_array(numels)
+    nbytes = ctypes.c_size_t()
+    _check("tkef_update_workspace", L.tkef_update_workspace(
+        arr, len(numels), P, stride, ctypes.byref(nbytes)))
+    dev = outs[0].device
+    own = status is None
+    if own:
+        status = _new_status(dev)
+    _check("tkef_sparse_aggregate", L.tkef_sparse_aggregate(
+        _ptr_array(outs), arr, len(numels), idx.data_ptr(), val.data_ptr(),
+        _val_format(val.dtype), P, stride, nnz.data_ptr() if nnz is not None else None,
+        _ws(nbytes.value, dev).data_ptr(), max(nbytes.value, 256), status.data_ptr(),
+        _stream_handle(None)))
+    _finish("tkef_sparse_aggregate", status, own)

@@ -165,6 +165,92 @@ struct tkef_sparsify_plan_s {
   int32_t n_events = 0;
 };
 
+// Launch shapes and workspace layout of a sparsify plan from its sizes (mode,
+// d, ngroups, k_total, ntiles, nlines); allocates nothing. False when the
+// selection grids cannot cover the tiles.
+bool sparsify_layout(tkef_sparsify_plan_s* p) {
+  // selection kernels: `lpt` consecutive summary lines per thread, at most
+  // select_max_groups() workgroups of sb threads (collect_block() for the
+  // exact one-group kernels, select_block() for the others). Aim for about
+  // 256 workgroups (one per compute unit); lpt is a power of two from 4 up
+  // (the kernels fetch four 16-bit summaries per load, and a thread's lines
+  // must lie in one tile).
+  const bool one = p->ngroups == 1;
+  const bool approx = p->mode == TKEF_APPROX;
+  const bool coll = one && !approx;
+  const int64_t sb = coll ? collect_block(p->nlines) : select_block();
+  p->sel_block = (int32_t)sb;
+  const int64_t sg = select_max_groups();
+  const int64_t want = (p->nlines + sb * 256 - 1) / (sb * 256);
+  int64_t lpt = 4;  // a power of two from 4 to select_max_lpt()
+  while (lpt < want && lpt < select_max_lpt()) lpt *= 2;
+  if ((p->nlines + sb * lpt - 1) / (sb * lpt) > sg) return false;  // (kMaxTiles)
+  p->sel_lpt = (int32_t)lpt;
+  const int64_t g_lines = (p->nlines + sb * lpt - 1) / (sb * lpt);
+  // Candidates are the positions at or above the level-1 threshold bin:
+  // about k plus one bin's worth. One group: each region (the lines of one
+  // workgroup) stores up to rcap of them, several times the even share of
+  // 8k + 65536; per tensor: one compacted list of 4k + 65536. Heavier inputs
+  // fall back to re-reading lines.
+  if (one) {
+    p->sel_grid = (int32_t)std::max<int64_t>(1, g_lines);
+    const int64_t region = lpt * sb * kLine;
+    const int64_t share = (8 * p->k_total + 65536 + p->sel_grid - 1) / p->sel_grid;
+    p->rcap = (uint32_t)std::min<int64_t>(region, std::max<int64_t>(4096, (share + 63) / 64 * 64));
+  } else {
+    p->cand_cap = (uint32_t)std::min<int64_t>(p->d, 4 * p->k_total + 65536);
+    const int64_t g_cands = std::min<int64_t>(sg, ((int64_t)p->cand_cap + sb * 4 - 1) / (sb * 4));
+    p->sel_grid = (int32_t)std::max<int64_t>(1, std::max(g_lines, g_cands));
+    p->line_grid = (int32_t)std::max<int64_t>(1, g_lines);
+  }
+  // level-1 histogram copies per group: many for one global selection (all
+  // workgroups add into it), a few per tensor in per-tensor mode
+  p->nslots = one ? kSlotsOne : kSlotsMany;
+
+  // workspace layout (every region 256-B aligned)
+  size_t o = 0;
+  p->off_tiles = o;   o = align_up(o + (size_t)p->ntiles * sizeof(TileDesc));
+  p->off_groups = o;  o = align_up(o + (size_t)p->ngroups * sizeof(GroupDesc));
+  p->off_state = o;   o = align_up(o + (size_t)p->ngroups * sizeof(GroupState));
+  size_t z = 0;
+  if (approx) {
+    p->off_ms_state = o;  o = align_up(o + (size_t)(kMsMaxPasses + 1) * sizeof(MsState));
+    p->off_ms_esum = z;   z = align_up(z + (size_t)kMsSlots * kMsDigitStride * 8);
+    p->off_ms_emax = z;   z = align_up(z + (size_t)kMsSlots * 4);
+    p->off_ms_cnt = z;    z = align_up(z + kMsCntWords * 4);
+    p->off_ms_flags = z;  z = align_up(z + (size_t)p->sel_grid * 8);
+  } else {
+    p->off_hist1 = z;   z = align_up(z + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
+    p->off_hist2 = z;   z = align_up(z + (size_t)p->ngroups * kH2Bins * 4);
+  }
+  if (!one) {
+    p->off_hist3 = z;   z = align_up(z + (size_t)p->ngroups * kH3Bins * 4);
+    p->off_flags1 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
+    p->off_flags2 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
+    p->off_meta = z;    z = align_up(z + 8);
+  }
+  p->zero_bytes = z;
+  p->off_zero[0] = o; o = align_up(o + z);
+  p->off_zero[1] = o; o = align_up(o + z);
+  p->off_summ = o;    o = align_up(o + (size_t)p->nlines * sizeof(uint16_t));
+  if (approx) {
+    // no candidate tables: the passes read the lines again
+  } else if (one) {
+    const size_t slots = (size_t)p->sel_grid * p->rcap;
+    p->off_rcand = o;  o = align_up(o + slots * 16);
+    p->off_rband = o;  o = align_up(o + slots * 4);
+    p->off_rbtmp = o;  o = align_up(o + slots * 4);
+    p->off_rsuf = o;   o = align_up(o + (size_t)p->sel_grid * kH2Bins * 4);
+    p->off_rcnt = o;   o = align_up(o + (size_t)p->sel_grid * 8);
+    p->off_rbin = o;   o = align_up(o + (size_t)kH2Bins * p->sel_grid * kPerBin * 4);
+  } else {
+    p->off_base = o;   o = align_up(o + (size_t)p->ngroups * 8);
+    p->off_cand = o;   o = align_up(o + (size_t)p->cand_cap * 8);  // {code, bits of x}
+  }
+  p->ws_bytes = o;
+  return true;
+}
+
 extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors, int32_t mode,
                                          double rho, int64_t k, tkef_sparsify_plan* plan_out) {
   if (!plan_out) return TKEF_EINVAL;
@@ -230,85 +316,7 @@ extern "C" int tkef_sparsify_plan_create(const int64_t* numels, int32_t ntensors
     }
     p->ntiles = static_cast<int32_t>(p->tiles.size());
     p->nlines = (int64_t)p->ntiles * kLinesPerTile;
-    // selection kernels: `lpt` consecutive summary lines per thread, at most
-    // select_max_groups() workgroups of sb threads (collect_block() for the
-    // exact one-group kernels, select_block() for the others). Aim for about
-    // 256 workgroups (one per compute unit); lpt is a power of two from 4 up
-    // (the kernels fetch four 16-bit summaries per load, and a thread's lines
-    // must lie in one tile).
-    const bool one = p->ngroups == 1;
-    const bool approx = mode == TKEF_APPROX;
-    const bool coll = one && !approx;
-    const int64_t sb = coll ? collect_block(p->nlines) : select_block();
-    p->sel_block = (int32_t)sb;
-    const int64_t sg = select_max_groups();
-    const int64_t want = (p->nlines + sb * 256 - 1) / (sb * 256);
-    int64_t lpt = 4;  // a power of two from 4 to select_max_lpt()
-    while (lpt < want && lpt < select_max_lpt()) lpt *= 2;
-    if ((p->nlines + sb * lpt - 1) / (sb * lpt) > sg) throw std::bad_alloc();  // kMaxTiles
-    p->sel_lpt = (int32_t)lpt;
-    const int64_t g_lines = (p->nlines + sb * lpt - 1) / (sb * lpt);
-    // Candidates are the positions at or above the level-1 threshold bin:
-    // about k plus one bin's worth. One group: each region (the lines of one
-    // workgroup) stores up to rcap of them, several times the even share of
-    // 8k + 65536; per tensor: one compacted list of 4k + 65536. Heavier inputs
-    // fall back to re-reading lines.
-    if (one) {
-      p->sel_grid = (int32_t)std::max<int64_t>(1, g_lines);
-      const int64_t region = lpt * sb * kLine;
-      const int64_t share = (8 * p->k_total + 65536 + p->sel_grid - 1) / p->sel_grid;
-      p->rcap = (uint32_t)std::min<int64_t>(region, std::max<int64_t>(4096, (share + 63) / 64 * 64));
-    } else {
-      p->cand_cap = (uint32_t)std::min<int64_t>(d, 4 * p->k_total + 65536);
-      const int64_t g_cands = std::min<int64_t>(sg, ((int64_t)p->cand_cap + sb * 4 - 1) / (sb * 4));
-      p->sel_grid = (int32_t)std::max<int64_t>(1, std::max(g_lines, g_cands));
-      p->line_grid = (int32_t)std::max<int64_t>(1, g_lines);
-    }
-    // level-1 histogram copies per group: many for one global selection (all
-    // workgroups add into it), a few per tensor in per-tensor mode
-    p->nslots = one ? kSlotsOne : kSlotsMany;
-
-    // workspace layout (every region 256-B aligned)
-    size_t o = 0;
-    p->off_tiles = o;   o = align_up(o + p->tiles.size() * sizeof(TileDesc));
-    p->off_groups = o;  o = align_up(o + p->groups.size() * sizeof(GroupDesc));
-    p->off_state = o;   o = align_up(o + p->groups.size() * sizeof(GroupState));
-    size_t z = 0;
-    if (approx) {
-      p->off_ms_state = o;  o = align_up(o + (size_t)(kMsMaxPasses + 1) * sizeof(MsState));
-      p->off_ms_esum = z;   z = align_up(z + (size_t)kMsSlots * kMsDigitStride * 8);
-      p->off_ms_emax = z;   z = align_up(z + (size_t)kMsSlots * 4);
-      p->off_ms_cnt = z;    z = align_up(z + kMsCntWords * 4);
-      p->off_ms_flags = z;  z = align_up(z + (size_t)p->sel_grid * 8);
-    } else {
-      p->off_hist1 = z;   z = align_up(z + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
-      p->off_hist2 = z;   z = align_up(z + (size_t)p->ngroups * kH2Bins * 4);
-    }
-    if (!one) {
-      p->off_hist3 = z;   z = align_up(z + (size_t)p->ngroups * kH3Bins * 4);
-      p->off_flags1 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
-      p->off_flags2 = z;  z = align_up(z + (size_t)p->sel_grid * 8);
-      p->off_meta = z;    z = align_up(z + 8);
-    }
-    p->zero_bytes = z;
-    p->off_zero[0] = o; o = align_up(o + z);
-    p->off_zero[1] = o; o = align_up(o + z);
-    p->off_summ = o;    o = align_up(o + (size_t)p->nlines * sizeof(uint16_t));
-    if (approx) {
-      // no candidate tables: the passes read the lines again
-    } else if (one) {
-      const size_t slots = (size_t)p->sel_grid * p->rcap;
-      p->off_rcand = o;  o = align_up(o + slots * 16);
-      p->off_rband = o;  o = align_up(o + slots * 4);
-      p->off_rbtmp = o;  o = align_up(o + slots * 4);
-      p->off_rsuf = o;   o = align_up(o + (size_t)p->sel_grid * kH2Bins * 4);
-      p->off_rcnt = o;   o = align_up(o + (size_t)p->sel_grid * 8);
-      p->off_rbin = o;   o = align_up(o + (size_t)kH2Bins * p->sel_grid * kPerBin * 4);
-    } else {
-      p->off_base = o;   o = align_up(o + (size_t)p->ngroups * 8);
-      p->off_cand = o;   o = align_up(o + (size_t)p->cand_cap * 8);  // {code, bits of x}
-    }
-    p->ws_bytes = o;
+    if (!sparsify_layout(p)) throw std::bad_alloc();  // (excluded by kMaxTiles above)
   } catch (const std::bad_alloc&) {
     delete p;
     return TKEF_ENOMEM;
@@ -594,15 +602,28 @@ extern "C" int tkef_sparsify_workspace(const int64_t* numels, int32_t ntensors, 
 
 extern "C" int tkef_sparsify(const float* const* grads, float* const* residuals,
                              const int64_t* numels, int32_t ntensors, int32_t mode, double rho,
-                             int64_t k, int32_t* idx_out, void* val_out, void* ws,
-                             size_t ws_bytes, uint32_t* status, hipStream_t stream) {
+                             int64_t k, int32_t val_format, int32_t* idx_out, void* val_out,
+                             int64_t* counts_out, void* ws, size_t ws_bytes, uint32_t* status,
+                             hipStream_t stream) {
   tkef_sparsify_plan p = nullptr;
   int rc = tkef_sparsify_plan_create(numels, ntensors, mode, rho, k, &p);
   if (rc) return rc;
-  rc = tkef_sparsify_plan_bind(p, grads, residuals, ws, ws_bytes, stream);
+  rc = tkef_sparsify_plan_set_value_format(p, val_format);
+  if (!rc && counts_out) rc = tkef_sparsify_plan_group_k(p, counts_out, p->ngroups);
+  if (!rc) rc = tkef_sparsify_plan_bind(p, grads, residuals, ws, ws_bytes, stream);
   if (!rc) rc = tkef_sparsify_execute(p, ws, ws_bytes, idx_out, val_out, status, stream);
   tkef_sparsify_plan_destroy(p);
   return rc;
+}
+
+extern "C" int tkef_sparsify1(const float* g, float* r, int64_t d, int64_t k, int32_t* idx_out,
+                              float* val_out, void* ws, size_t ws_bytes, uint32_t* status,
+                              hipStream_t stream) {
+  if (d < 1 || d > kMaxD || k < 1 || k > d) return TKEF_ERANGE;
+  const float* gs[1] = {g};
+  float* rs[1] = {r};
+  return tkef_sparsify(gs, rs, &d, 1, TKEF_GLOBAL, 0.0, k, TKEF_VAL_F32, idx_out, val_out,
+                       nullptr, ws, ws_bytes, status, stream);
 }
 
 // ============================================================================
@@ -623,7 +644,8 @@ struct tkef_update_plan_s {
   std::vector<int32_t> tile_first;
   std::vector<int32_t> tpair;  // LARS: first (tile, tensor) pair of each tensor; [T] = pairs
   size_t off_tens = 0, off_first = 0, off_seg = 0, off_tpair = 0, off_part = 0, off_rate = 0,
-         off_gptr = 0, ws_bytes = 0;
+         off_gptr = 0, off_lists = 0, ws_bytes = 0;
+  bool table = false;  // lists given as per-worker pointers (WorkerList table in ws)
   void* bound_ws = nullptr;
   bool has_mom = false;
   bool has_grads = false;  // dense gradients bound (LARS rates)
@@ -632,8 +654,10 @@ struct tkef_update_plan_s {
   int32_t n_events = 0;
 };
 
-extern "C" int tkef_update_plan_create(const int64_t* numels, int32_t ntensors, int32_t P,
-                                       int64_t stride, tkef_update_plan* plan_out) {
+namespace {
+
+int update_plan_create(const int64_t* numels, int32_t ntensors, int32_t P, int64_t stride,
+                       bool table, tkef_update_plan* plan_out) {
   if (!plan_out) return TKEF_EINVAL;
   *plan_out = nullptr;
   int64_t d = 0;
@@ -683,6 +707,10 @@ extern "C" int tkef_update_plan_create(const int64_t* numels, int32_t ntensors, 
     p->off_part = o;   o = align_up(o + (size_t)p->tpair[ntensors] * 16);
     p->off_rate = o;   o = align_up(o + (size_t)ntensors * sizeof(double));
     p->off_gptr = o;   o = align_up(o + (size_t)ntensors * sizeof(float*));
+    p->table = table;
+    if (table) {
+      p->off_lists = o;  o = align_up(o + (size_t)P * sizeof(WorkerList));
+    }
     p->ws_bytes = o;
   } catch (const std::bad_alloc&) {
     delete p;
@@ -690,6 +718,13 @@ extern "C" int tkef_update_plan_create(const int64_t* numels, int32_t ntensors, 
   }
   *plan_out = p;
   return TKEF_OK;
+}
+
+}  // namespace
+
+extern "C" int tkef_update_plan_create(const int64_t* numels, int32_t ntensors, int32_t P,
+                                       int64_t stride, tkef_update_plan* plan_out) {
+  return update_plan_create(numels, ntensors, P, stride, false, plan_out);
 }
 
 extern "C" int tkef_update_plan_destroy(tkef_update_plan plan) {
@@ -706,9 +741,11 @@ extern "C" int tkef_update_plan_info(tkef_update_plan plan, size_t* workspace_by
   return TKEF_OK;
 }
 
-extern "C" int tkef_update_plan_bind(tkef_update_plan plan, float* const* params,
-                                     float* const* momentum, void* ws, size_t ws_bytes,
-                                     hipStream_t stream) {
+namespace {
+
+// The checks of tkef_update_plan_bind (nothing is enqueued before them).
+int check_update_bind(tkef_update_plan plan, float* const* params, float* const* momentum,
+                      void* ws, size_t ws_bytes) {
   if (!plan || !params) return TKEF_EINVAL;
   if (!ws || !aligned_ws(ws) || ws_bytes < plan->ws_bytes) return TKEF_EWORKSPACE;
   for (int32_t t = 0; t < plan->ntensors; ++t) {
@@ -720,6 +757,16 @@ extern "C" int tkef_update_plan_bind(tkef_update_plan plan, float* const* params
       if (ranges_overlap(params[t], momentum[t], n)) return TKEF_EINVAL;
     }
   }
+  return TKEF_OK;
+}
+
+}  // namespace
+
+extern "C" int tkef_update_plan_bind(tkef_update_plan plan, float* const* params,
+                                     float* const* momentum, void* ws, size_t ws_bytes,
+                                     hipStream_t stream) {
+  const int rc = check_update_bind(plan, params, momentum, ws, ws_bytes);
+  if (rc) return rc;
   for (int32_t t = 0; t < plan->ntensors; ++t) {
     plan->tens[t].w = params[t];
     plan->tens[t].b = momentum ? momentum[t] : nullptr;
@@ -936,6 +983,73 @@ extern "C" int tkef_sparse_aggregate(float* const* outs, const int64_t* numels, 
   rc = tkef_update_plan_set_value_format(p, val_format);
   if (!rc) rc = tkef_update_plan_bind(p, outs, nullptr, ws, ws_bytes, stream);
   if (!rc) rc = tkef_aggregate_execute(p, idx, val, nnz, ws, ws_bytes, status, stream);
+  tkef_update_plan_destroy(p);
+  return rc;
+}
+
+extern "C" int tkef_aggregate_workspace(const int64_t* numels, int32_t ntensors, int32_t P,
+                                        size_t* workspace_bytes) {
+  tkef_update_plan p = nullptr;
+  int rc = update_plan_create(numels, ntensors, P, 0, true, &p);
+  if (rc) return rc;
+  rc = tkef_update_plan_info(p, workspace_bytes, nullptr, nullptr);
+  tkef_update_plan_destroy(p);
+  return rc;
+}
+
+extern "C" int tkef_aggregate_update(float* const* params, float* const* momentum,
+                                     const int64_t* numels, int32_t ntensors,
+                                     const int32_t* const* idx, const float* const* val,
+                                     const int64_t* nnz, int32_t P, float lr, float mu, float wd,
+                                     void* ws, size_t ws_bytes, uint32_t* status,
+                                     hipStream_t stream) {
+  if (!idx || !val || !nnz || P < 1) return TKEF_EINVAL;
+  if (!std::isfinite(lr) || !std::isfinite(mu) || !std::isfinite(wd)) return TKEF_ERANGE;
+  if (mu != 0.0f && !momentum) return TKEF_EINVAL;
+  std::vector<WorkerList> lists;
+  int64_t max_n = 0;
+  try {
+    lists.resize(P);
+  } catch (const std::bad_alloc&) {
+    return TKEF_ENOMEM;
+  }
+  for (int32_t q = 0; q < P; ++q) {
+    if (nnz[q] < 0) return TKEF_EINVAL;
+    if (nnz[q] > kMaxD) return TKEF_ERANGE;
+    if (nnz[q] > 0 && (!idx[q] || !val[q])) return TKEF_EINVAL;
+    lists[q] = WorkerList{idx[q], val[q], nnz[q], 0};
+    max_n = std::max(max_n, nnz[q]);
+  }
+  tkef_update_plan p = nullptr;
+  int rc = update_plan_create(numels, ntensors, P, 0, true, &p);
+  if (rc) return rc;
+  rc = check_update_bind(p, params, momentum, ws, ws_bytes);
+  if (rc) {
+    tkef_update_plan_destroy(p);
+    return rc;
+  }
+  // the worker table goes in first; bind's synchronization covers its copy
+  char* base = static_cast<char*>(ws);
+  if (hipMemcpyAsync(base + p->off_lists, lists.data(), lists.size() * sizeof(WorkerList),
+                     hipMemcpyHostToDevice, stream) != hipSuccess) {
+    tkef_update_plan_destroy(p);
+    return TKEF_EHIP;
+  }
+  rc = tkef_update_plan_bind(p, params, momentum, ws, ws_bytes, stream);
+  if (!rc) {
+    const UpdTensor* tens = reinterpret_cast<const UpdTensor*>(base + p->off_tens);
+    const int32_t* first = reinterpret_cast<const int32_t*>(base + p->off_first);
+    int32_t* seg = reinterpret_cast<int32_t*>(base + p->off_seg);
+    const WorkerList* table = reinterpret_cast<const WorkerList*>(base + p->off_lists);
+    const int op = (mu == 0.0f && wd == 0.0f) ? kOpSparseSgd : kOpSgd;
+    const int has_mom = mu != 0.0f ? 1 : 0;
+    hipError_t e = launch_seg_table(table, P, max_n, (int32_t)p->d, p->ntiles_u, seg, status,
+                                    stream, Ev{});
+    if (e == hipSuccess)
+      e = launch_update_table(tens, first, p->ntensors, (int32_t)p->d, p->ntiles_u, table, P,
+                              seg, lr, mu, wd, op, has_mom, stream, Ev{});
+    rc = hip_rc(e);
+  }
   tkef_update_plan_destroy(p);
   return rc;
 }

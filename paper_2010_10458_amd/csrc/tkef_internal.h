@@ -110,6 +110,16 @@ struct UpdTensor {       // 32 B, one per parameter tensor, written at bind
 };
 static_assert(sizeof(UpdTensor) == 32, "UpdTensor layout");
 
+// One worker's list in the per-worker pointer form of the aggregate: n
+// entries at idx[0..n) (ascending positions) and val[0..n) (binary32).
+struct WorkerList {      // 32 B, one per worker, written by the call
+  const int32_t* idx;
+  const void* val;
+  int64_t n;
+  int64_t reserved;
+};
+static_assert(sizeof(WorkerList) == 32, "WorkerList layout");
+
 // ---- kernel launchers (tkef_kernels.hip) --------------------------------------
 // Optional timing events attached to one launch (recorded by the dispatch
 // itself at the kernel's start and end).
@@ -193,6 +203,15 @@ hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32
                          int val16, int64_t stride, const int32_t* nnz, int32_t P,
                          const int32_t* seg, float lr, float mu, float wd, int op, int has_mom,
                          const LarsArgs& lars, hipStream_t s, const Ev& ev);
+// the same two steps over P per-worker lists (table in device memory; max_n:
+// the longest list)
+hipError_t launch_seg_table(const WorkerList* lists, int32_t P, int64_t max_n, int32_t d,
+                            int32_t ntiles_u, int32_t* seg, uint32_t* status, hipStream_t s,
+                            const Ev& ev);
+hipError_t launch_update_table(const UpdTensor* tens, const int32_t* tile_first, int32_t ntens,
+                               int32_t d, int32_t ntiles_u, const WorkerList* lists, int32_t P,
+                               const int32_t* seg, float lr, float mu, float wd, int op,
+                               int has_mom, hipStream_t s, const Ev& ev);
 // LARS: partial sums of w^2 and g^2 from dense gradients (g pointer per
 // tensor), and the per-tensor rates from the partial sums
 hipError_t launch_lars_norm_dense(const UpdTensor* tens, const float* const* gptrs,

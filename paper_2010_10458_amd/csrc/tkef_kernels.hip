@@ -454,10 +454,12 @@ __global__ __launch_bounds__(kBlock) void k_pick(int level, const GroupDesc* __r
 // The per-tensor path places its ordered output with a prefix of
 // per-workgroup counts: each workgroup publishes its count in a flag word
 // (bit 63 = valid) and then reads the words of all lower-numbered
-// workgroups. It waits only on workgroups dispatched before it, which publish
-// without waiting on anything, so the wait always ends; it is still bounded
-// (kSpinLimit polls per word), after which TKEF_STATUS_TIMEOUT is recorded and
-// the workgroup goes on. Flag words are cleared before every execution.
+// workgroups. It waits only on workgroups dispatched before it (workgroups
+// start in order of their number), which publish without waiting on
+// anything, so the wait ends; it is still bounded (kSpinLimit polls per
+// word), after which TKEF_STATUS_TIMEOUT is recorded and the workgroup writes
+// no output that depends on the prefix. Flag words are cleared before every
+// execution.
 constexpr int kSBlock = 1024;
 constexpr int kSWaves = kSBlock / 64;
 // collect and finish (one selection group) run kCBlockSmall threads per
@@ -516,19 +518,28 @@ __device__ __forceinline__ uint64_t sblock_sum_u64(uint64_t v, uint64_t* red) {
 }
 
 // Publishes this workgroup's count and returns the sum of the counts of the
-// workgroups numbered below it.
+// workgroups numbered below it (uniform in the workgroup).
+//
+// The wait relies on the dispatcher starting a grid's workgroups in order of
+// their number, so that every workgroup numbered below a waiting one has
+// started and will publish its count; the callers' grids are also sized so
+// that all their workgroups are resident at once. Each wait is bounded
+// (kSpinLimit sleeps): a workgroup that gives up sets TKEF_STATUS_TIMEOUT,
+// and *ok = false tells the caller that the prefix is incomplete, so that it
+// writes nothing that depends on it.
 __device__ uint64_t group_prefix(uint64_t* __restrict__ flags, uint64_t mine, uint64_t* red,
-                                 uint32_t* __restrict__ status) {
+                                 uint32_t* __restrict__ status, bool* ok) {
   const int tid = threadIdx.x;
   const int w = blockIdx.x;
   if (tid == 0) flag_store(&flags[w], kFlagValid | mine);
   uint64_t v = 0;
-  for (int j = tid; j < w; j += kSBlock) {
+  bool gave_up = false;
+  for (int j = tid; j < w && !gave_up; j += kSBlock) {
     uint64_t f = flag_load(&flags[j]);
     uint32_t spins = 0;
     while (!(f & kFlagValid)) {
       if (++spins > kSpinLimit) {
-        if (status) atomicOr(status, TKEF_STATUS_TIMEOUT);
+        gave_up = true;
         break;
       }
       __builtin_amdgcn_s_sleep(1);
@@ -536,6 +547,9 @@ __device__ uint64_t group_prefix(uint64_t* __restrict__ flags, uint64_t mine, ui
     }
     v += f & kFlagVal;
   }
+  const bool any = __syncthreads_or(gave_up ? 1 : 0) != 0;
+  if (any && tid == 0 && status) atomicOr(status, TKEF_STATUS_TIMEOUT);
+  *ok = !any;
   return sblock_sum_u64(v, red);
 }
 
@@ -1276,8 +1290,11 @@ __global__ __launch_bounds__(kSBlock) void k_gather(const TileDesc* __restrict__
   if (g0 >= 0)
     for (int i = tid; i < kH2Bins; i += kSBlock)
       if (h2[i]) atomicAdd(&hist2[(size_t)g0 * kH2Bins + i], h2[i]);
-  const uint64_t pre = group_prefix(flags, total, red, status);
-  const bool fits = pre + total <= cap;
+  bool ok;
+  const uint64_t pre = group_prefix(flags, total, red, status, &ok);
+  // (an incomplete prefix counts as an overflow: the later kernels then
+  // read the lines instead of the candidate list)
+  const bool fits = ok && pre + total <= cap;
   if (tid == 0) {
     if (!fits) atomicOr(&meta[0], 1u);
     if (blockIdx.x == gridDim.x - 1) meta[1] = (uint32_t)min(pre + total, (uint64_t)0xFFFFFFFFu);
@@ -1446,8 +1463,10 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
   }
   uint2 tot;
   const uint2 x2 = block_scan2<kSBlock>(gt, eq, wsum, &tot);
-  const uint64_t pre = group_prefix(flags, (uint64_t)tot.x | ((uint64_t)tot.y << 31), red, status);
-  if (nst == 0u) return;
+  bool ok;
+  const uint64_t pre =
+      group_prefix(flags, (uint64_t)tot.x | ((uint64_t)tot.y << 31), red, status, &ok);
+  if (nst == 0u || !ok) return;  // (no place is known without the full prefix)
   uint32_t gtr = (uint32_t)(pre & 0x7FFFFFFFu) + x2.x;
   uint32_t eqr = (uint32_t)((pre >> 31) & 0x7FFFFFFFu) + x2.y;
   // pass 2: write
@@ -1490,27 +1509,51 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
 }
 
 // ---------------------------------------------------------------------------
+// The P workers' lists, in one of two forms: the gathered layout (worker p's
+// entries at p * stride, nnz[p] of them, or stride without nnz) or a table of
+// per-worker pointers and counts (kTable).
+struct ListsArg {
+  const int32_t* idx;        // gathered form
+  const void* val;
+  int64_t stride;
+  const int32_t* nnz;
+  const WorkerList* table;   // per-worker form
+};
+typedef __attribute__((address_space(1))) const int32_t gint;
+
 // seg: seg[u * P + p] = first entry of worker p's list whose index lies in
 // update tile u or later; seg[ntiles_u * P + p] = nnz_p. Tile-major, so the
 // workgroup of tile u reads two contiguous rows. Also flags unsorted or
 // out-of-range lists in the status word.
-__global__ void k_seg(const int32_t* __restrict__ idx, int64_t stride,
-                      const int32_t* __restrict__ nnz, int32_t P, int32_t d, int32_t ntiles_u,
+template <bool kTable>
+__global__ void k_seg(ListsArg lists, int32_t P, int32_t d, int32_t ntiles_u,
                       int32_t* __restrict__ seg, uint32_t* __restrict__ status) {
   const int p = blockIdx.y;
-  const int32_t* __restrict__ L = idx + (int64_t)p * stride;
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  // this entry and the one before it, read before the count is known (every
-  // j < stride is inside the list's storage), so all three loads overlap; no
-  // storage at all for stride == 0 (a kernel-wide value)
-  const int64_t jc = j < stride ? j : stride - 1;
   int32_t i_here = 0, i_prev = 0;
-  if (stride > 0) {
-    i_here = L[jc];
-    i_prev = L[jc > 0 ? jc - 1 : 0];
+  int64_t n;
+  if constexpr (kTable) {
+    const WorkerList wl = lists.table[p];
+    n = wl.n;
+    if (j < n) {
+      const gint* L = (const gint*)wl.idx;
+      i_here = L[j];
+      i_prev = L[j > 0 ? j - 1 : 0];
+    }
+  } else {
+    // this entry and the one before it, read before the count is known
+    // (every j < stride is inside the list's storage), so all three loads
+    // overlap; no storage at all for stride == 0 (a kernel-wide value)
+    const int64_t stride = lists.stride;
+    const int32_t* __restrict__ L = lists.idx + (int64_t)p * stride;
+    const int64_t jc = j < stride ? j : stride - 1;
+    if (stride > 0) {
+      i_here = L[jc];
+      i_prev = L[jc > 0 ? jc - 1 : 0];
+    }
+    n = lists.nnz ? (int64_t)lists.nnz[p] : stride;
+    n = n < 0 ? 0 : (n > stride ? stride : n);
   }
-  int64_t n = nnz ? (int64_t)nnz[p] : stride;
-  n = n < 0 ? 0 : (n > stride ? stride : n);
   if (n == 0) {
     for (int64_t u = j; u <= ntiles_u; u += (int64_t)gridDim.x * blockDim.x)
       seg[u * P + p] = 0;
@@ -1602,13 +1645,18 @@ constexpr int kUVecPerThread = kUTile / 4 / kUBlock;  // float4 per thread per t
 
 // kLars: the LARS norm and step passes (a separate instantiation, so the SGD
 // and aggregation passes keep their register budget).
-template <bool kLars>
+// kTable: the lists come as a table of per-worker pointers (binary32 values).
+template <bool kLars, bool kTable>
 __global__ __launch_bounds__(kUBlock) void k_update(
     const UpdTensor* __restrict__ tens, const int32_t* __restrict__ tile_first, int32_t ntens,
-    int32_t d, int32_t ntiles_u, const int32_t* __restrict__ idx,
-    const void* __restrict__ val, int val16, int64_t stride, const int32_t* __restrict__ nnz,
-    int32_t P, const int32_t* __restrict__ seg, float lr, float mu, float wd, int op,
-    int has_mom, LarsArgs lars) {
+    int32_t d, int32_t ntiles_u, ListsArg lists, int val16, int32_t P,
+    const int32_t* __restrict__ seg, float lr, float mu, float wd, int op, int has_mom,
+    LarsArgs lars) {
+  static_assert(!(kLars && kTable), "LARS takes the gathered lists");
+  const int32_t* __restrict__ idx = lists.idx;
+  const void* __restrict__ val = lists.val;
+  const int64_t stride = lists.stride;
+  const int32_t* __restrict__ nnz = lists.nnz;
   const bool sparse_mode = op == kOpSparseSgd;
   const bool densify = op == kOpAggregate;
   const bool lnorm = kLars && op == kOpLarsNorm;
@@ -1618,6 +1666,9 @@ __global__ __launch_bounds__(kUBlock) void k_update(
   __shared__ uint32_t mask[kUTile / 32];
   __shared__ int32_t sbeg[kUBlock];
   __shared__ uint32_t scan[kUBlock];
+  // per-worker form: the list pointers of the current batch of workers
+  __shared__ const int32_t* s_ip[kTable ? kUBlock : 1];
+  __shared__ const float* s_vp[kTable ? kUBlock : 1];
   const int tid = threadIdx.x;
   // Workgroups go round-robin to the XCDs; give each XCD runs of kXcdRun
   // consecutive tiles, so that neighbouring tiles, which share the cache
@@ -1666,8 +1717,16 @@ __global__ __launch_bounds__(kUBlock) void k_update(
     const int p = p0 + tid;
     int32_t b = 0, e = 0;
     if (p < P) {
-      int64_t np = nnz ? (int64_t)nnz[p] : stride;
-      np = np < 0 ? 0 : (np > stride ? stride : np);
+      int64_t np;
+      if constexpr (kTable) {
+        const WorkerList wl = lists.table[p];
+        np = wl.n;
+        s_ip[tid] = wl.idx;
+        s_vp[tid] = static_cast<const float*>(wl.val);
+      } else {
+        np = nnz ? (int64_t)nnz[p] : stride;
+        np = np < 0 ? 0 : (np > stride ? stride : np);
+      }
       int64_t sb = seg[(int64_t)u * P + p], se = seg[(int64_t)(u + 1) * P + p];
       sb = sb < 0 ? 0 : (sb > np ? np : sb);
       se = se < sb ? sb : (se > np ? np : se);
@@ -1699,9 +1758,15 @@ __global__ __launch_bounds__(kUBlock) void k_update(
             if (scan[mid] > q) hi = mid; else lo = mid + 1;
           }
           const uint32_t before = lo ? scan[lo - 1] : 0u;
-          const int64_t gi = (int64_t)(p0 + lo) * stride + sbeg[lo] + (q - before);
-          li[j] = idx[gi] - base;
-          vv[j] = get_val(val, (size_t)gi, val16);
+          const int64_t jj = (int64_t)sbeg[lo] + (q - before);
+          if constexpr (kTable) {
+            li[j] = ((const gint*)s_ip[lo])[jj] - base;
+            vv[j] = ((const gfloat*)s_vp[lo])[jj];
+          } else {
+            const int64_t gi = (int64_t)(p0 + lo) * stride + jj;
+            li[j] = idx[gi] - base;
+            vv[j] = get_val(val, (size_t)gi, val16);
+          }
         }
       }
 #pragma unroll
@@ -2525,8 +2590,10 @@ __global__ __launch_bounds__(kSBlock) void k_ms_emit(
   });
   uint2 tot;
   const uint2 ex = block_scan2<kSBlock>(c1, c2, wsum, &tot);
-  const uint64_t pre = group_prefix(flags, (uint64_t)tot.x | ((uint64_t)tot.y << 31), red, status);
-  if (nst == 0u) return;
+  bool ok;
+  const uint64_t pre =
+      group_prefix(flags, (uint64_t)tot.x | ((uint64_t)tot.y << 31), red, status, &ok);
+  if (nst == 0u || !ok) return;  // (no place is known without the full prefix)
   uint32_t p1 = (uint32_t)(pre & 0x7FFFFFFFu) + ex.x;
   uint32_t p2 = (uint32_t)((pre >> 31) & 0x7FFFFFFFu) + ex.y;
   auto write = [&](int, const TileDesc& t, int e, float x, uint32_t key) {
@@ -2718,8 +2785,25 @@ hipError_t launch_seg(const int32_t* idx, int64_t stride, const int32_t* nnz, in
                       hipStream_t s, const Ev& ev) {
   int64_t bx = (stride + 255) / 256;
   if (bx < 1) bx = 1;
-  return launch(k_seg, dim3((unsigned)bx, (unsigned)P), dim3(256), s, ev, idx, stride, nnz, P, d,
+  const ListsArg lists{idx, nullptr, stride, nnz, nullptr};
+  return launch(k_seg<false>, dim3((unsigned)bx, (unsigned)P), dim3(256), s, ev, lists, P, d,
                 ntiles_u, seg, status);
+}
+
+hipError_t launch_seg_table(const WorkerList* table, int32_t P, int64_t max_n, int32_t d,
+                            int32_t ntiles_u, int32_t* seg, uint32_t* status, hipStream_t s,
+                            const Ev& ev) {
+  int64_t bx = (max_n + 255) / 256;
+  if (bx < 1) bx = 1;
+  const ListsArg lists{nullptr, nullptr, 0, nullptr, table};
+  return launch(k_seg<true>, dim3((unsigned)bx, (unsigned)P), dim3(256), s, ev, lists, P, d,
+                ntiles_u, seg, status);
+}
+
+// whole groups of kXcds runs (workgroups past the last tile return at once)
+static int32_t update_grid(int32_t ntiles_u) {
+  constexpr int32_t kGroup = kXcds * kXcdRun;
+  return (ntiles_u + kGroup - 1) / kGroup * kGroup;
 }
 
 hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32_t ntens,
@@ -2727,13 +2811,21 @@ hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32
                          int val16, int64_t stride, const int32_t* nnz, int32_t P,
                          const int32_t* seg, float lr, float mu, float wd, int op, int has_mom,
                          const LarsArgs& lars, hipStream_t s, const Ev& ev) {
-  // whole groups of kXcds runs (workgroups past the last tile return at once)
-  constexpr int32_t kGroup = kXcds * kXcdRun;
-  const int32_t grid = (ntiles_u + kGroup - 1) / kGroup * kGroup;
   const bool is_lars = op == kOpLarsNorm || op == kOpLarsApply;
-  return launch(is_lars ? k_update<true> : k_update<false>, dim3(grid), dim3(kUBlock), s, ev,
-                tens, tile_first, ntens, d, ntiles_u, idx, val, val16, stride, nnz, P, seg, lr, mu,
-                wd, op, has_mom, lars);
+  const ListsArg lists{idx, val, stride, nnz, nullptr};
+  return launch(is_lars ? k_update<true, false> : k_update<false, false>,
+                dim3(update_grid(ntiles_u)), dim3(kUBlock), s, ev, tens, tile_first, ntens, d,
+                ntiles_u, lists, val16, P, seg, lr, mu, wd, op, has_mom, lars);
+}
+
+hipError_t launch_update_table(const UpdTensor* tens, const int32_t* tile_first, int32_t ntens,
+                               int32_t d, int32_t ntiles_u, const WorkerList* table, int32_t P,
+                               const int32_t* seg, float lr, float mu, float wd, int op,
+                               int has_mom, hipStream_t s, const Ev& ev) {
+  const ListsArg lists{nullptr, nullptr, 0, nullptr, table};
+  return launch(k_update<false, true>, dim3(update_grid(ntiles_u)), dim3(kUBlock), s, ev, tens,
+                tile_first, ntens, d, ntiles_u, lists, 0, P, seg, lr, mu, wd, op, has_mom,
+                LarsArgs{nullptr, nullptr, nullptr, 0.0f});
 }
 
 hipError_t launch_lars_norm_dense(const UpdTensor* tens, const float* const* gptrs,

@@ -29,7 +29,7 @@ def test_header_symbols_exported():
 
 def test_version_and_strerror():
     L = tk.lib()
-    assert L.tkef_version() == 10000
+    assert L.tkef_version() == 10100
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert L.tkef_strerror(code)
     assert b"unknown" in L.tkef_strerror(-99)
@@ -217,6 +217,89 @@ def test_lars_host_side():
     assert L.tkef_lars_rates_execute(h, 1.0, 1.0, 0.0, P_(0x3000), ws, 10**9, None) == tk.ESTATE
     assert L.tkef_lars_rates_execute(h, 1.0, float("inf"), 0.0, P_(0x3000), ws, 10**9,
                                      None) == tk.ERANGE
+    # eps is a weight decay: negative values are refused (Eq. lars needs a
+    # denominator that vanishes only with the gradient)
+    assert L.tkef_lars_rates_execute(h, 1.0, 1.0, -1e-4, P_(0x3000), ws, 10**9,
+                                     None) == tk.ERANGE
+    assert L.tkef_lars_update_execute(h, P_(0x100), P_(0x200), None, 1.0, 1.0, -0.5, 0.0, None,
+                                      ws, 10**9, None, None) == tk.ERANGE
     names = [L.tkef_lars_launch_name(0, i).decode() for i in range(4)]
     assert names == tk.LARS_LAUNCHES and L.tkef_lars_launch_name(0, 4) is None
     assert [L.tkef_lars_launch_name(1, i).decode() for i in range(2)] == tk.LARS_DENSE_LAUNCHES
+
+
+def test_one_shot_sparsify_host_side():
+    """tkef_sparsify writes counts_out (the k of each selection group) before
+    any GPU work; tkef_sparsify1 checks d and k; both refuse a missing
+    workspace without touching the GPU."""
+    L = tk.lib()
+    P_ = ctypes.c_void_p
+    numels = [100, 8192 * 3 + 1, 0, 7]
+    arr = (ctypes.c_int64 * 4)(*numels)
+    g = (P_ * 4)(P_(0x1000), P_(0x100000), None, P_(0x300000))
+    r = (P_ * 4)(P_(0x400000), P_(0x500000), None, P_(0x600000))
+    counts = (ctypes.c_int64 * 4)(-1, -1, -1, -1)
+    assert L.tkef_sparsify(g, r, arr, 4, tk.PER_TENSOR, 0.01, 0, tk.VAL_F32, P_(0x10), P_(0x20),
+                           counts, None, 10**9, None, None) == tk.EWORKSPACE
+    assert list(counts) == [1, 246, 0, 1]
+    counts[0] = -1
+    assert L.tkef_sparsify(g, r, arr, 4, tk.GLOBAL, 0.01, 0, tk.VAL_F16, P_(0x10), P_(0x20),
+                           counts, None, 10**9, None, None) == tk.EWORKSPACE
+    assert counts[0] == tk.k_from_rho(sum(numels), 0.01)
+    assert L.tkef_sparsify(g, r, arr, 4, tk.GLOBAL, 0.01, 0, 7, P_(0x10), P_(0x20),
+                           None, None, 10**9, None, None) == tk.EINVAL
+    nb, kt = ctypes.c_size_t(), ctypes.c_int64()
+    assert L.tkef_sparsify_workspace(arr, 4, tk.GLOBAL, 0.0, 5, ctypes.byref(nb),
+                                     ctypes.byref(kt)) == tk.OK
+    assert kt.value == 5 and nb.value % 256 == 0
+    for d, k in ((0, 1), (10, 0), (10, 11), (2**31, 1), (-5, 1)):
+        assert L.tkef_sparsify1(P_(0x1000), P_(0x100000), d, k, P_(0x10), P_(0x20), P_(0x10000),
+                                10**9, None, None) == tk.ERANGE, (d, k)
+    assert L.tkef_sparsify1(P_(0x1000), P_(0x100000), 10, 3, P_(0x10), P_(0x20), None, 10**9,
+                            None, None) == tk.EWORKSPACE
+    # g and r overlap
+    assert L.tkef_sparsify1(P_(0x1000), P_(0x1000 + 8), 10, 3, P_(0x10), P_(0x20),
+                            P_(0x10000), 10**9, None, None) == tk.EINVAL
+
+
+def test_aggregate_update_host_side():
+    """tkef_aggregate_update / tkef_aggregate_workspace: argument checks on
+    the host, before any GPU work."""
+    L = tk.lib()
+    P_ = ctypes.c_void_p
+    numels = (ctypes.c_int64 * 2)(100, 5000)
+    nb, nb_g = ctypes.c_size_t(), ctypes.c_size_t()
+    assert L.tkef_aggregate_workspace(numels, 2, 300, ctypes.byref(nb)) == tk.OK
+    assert L.tkef_update_workspace(numels, 2, 300, 0, ctypes.byref(nb_g)) == tk.OK
+    assert nb.value >= nb_g.value + 300 * 32 and nb.value % 256 == 0
+    assert L.tkef_aggregate_workspace(numels, 2, 0, ctypes.byref(nb)) == tk.EINVAL
+    w = (P_ * 2)(P_(0x1000), P_(0x2000))
+    b = (P_ * 2)(P_(0x100000), P_(0x200000))
+    ip = (P_ * 3)(P_(0x300000), None, P_(0x310000))
+    vp = (P_ * 3)(P_(0x400000), None, P_(0x410000))
+    nnz = (ctypes.c_int64 * 3)(10, 0, 5)
+    ws = P_(0x10000)
+
+    def call(params=w, mom=None, i=ip, v=vp, n=nnz, P=3, lr=0.1, mu=0.0, wd=0.0, ws=ws,
+             wsb=10**9):
+        return L.tkef_aggregate_update(params, mom, numels, 2, i, v, n, P, lr, mu, wd, ws, wsb,
+                                       None, None)
+
+    assert call(i=None) == tk.EINVAL
+    assert call(v=None) == tk.EINVAL
+    assert call(n=None) == tk.EINVAL
+    assert call(P=0) == tk.EINVAL
+    assert call(lr=float("nan")) == tk.ERANGE
+    assert call(mu=0.9) == tk.EINVAL                     # momentum buffers needed
+    bad_n = (ctypes.c_int64 * 3)(10, -1, 5)
+    assert call(n=bad_n) == tk.EINVAL
+    big_n = (ctypes.c_int64 * 3)(10, 2**31, 5)
+    assert call(n=big_n) == tk.ERANGE
+    null_list = (ctypes.c_int64 * 3)(10, 4, 5)            # list 1 has entries, no pointers
+    assert call(n=null_list) == tk.EINVAL
+    assert call(ws=None) == tk.EWORKSPACE
+    assert call(ws=P_(0x10010)) == tk.EWORKSPACE
+    assert call(wsb=16) == tk.EWORKSPACE
+    assert call(params=(P_ * 2)(None, P_(0x2000))) == tk.EINVAL
+    overlap = (P_ * 2)(P_(0x1000 + 4), P_(0x200000))
+    assert call(mom=overlap, mu=0.9) == tk.EINVAL

@@ -48,9 +48,12 @@ def gpu_update(sizes, w_host, b_host, idx, val, lr, mu, wd, nnz=None, views=None
     return (to_host(w), to_host(b) if b is not None else None, int(status.item()))
 
 
-def compare(sizes, w0, b0, idx, val, lr, mu, wd, nnz=None, exact=False, label=""):
+def compare(sizes, w0, b0, idx, val, lr, mu, wd, nnz=None, exact=False, label="", runner=None):
+    """runner(sizes, w0, b0, idx, val, lr, mu, wd, nnz) -> (w, b, status):
+    the GPU call under test (default: an UpdatePlan over the gathered
+    lists)."""
     announce(f"update {label} P={idx.shape[0]} stride={idx.shape[1]} mu={mu} wd={wd}")
-    w_gpu, b_gpu, status = gpu_update(sizes, w0, b0, idx, val, lr, mu, wd, nnz)
+    w_gpu, b_gpu, status = (runner or gpu_update)(sizes, w0, b0, idx, val, lr, mu, wd, nnz)
     assert status == 0
     w_ref, b_ref = orc().update(gen.concat(w0), None if b0 is None else gen.concat(b0), idx, val,
                                 nnz=None if nnz is None else np.asarray(nnz, np.int64),
@@ -225,10 +228,11 @@ def test_c5_resnet50_p128_momentum_3_steps():
         A = np.zeros(d)
         np.add.at(A, idx.ravel(), np.abs(val.ravel().astype(np.float64)))
         S = 0.1 * (A + 5e-5 * np.abs(w_prev) + 0.9 * np.abs(b_prev))
+        # every step starts from the GPU's own state, so positions with at
+        # most two contributions in this step match bit for bit on each step
         le2 = cnt <= 2
-        if step == 0:
-            assert_bitwise(wg[le2], w_ref[le2], "w (<= 2 contributions)")
-            assert_bitwise(bg[le2], b_ref[le2], "b (<= 2 contributions)")
+        assert_bitwise(wg[le2], w_ref[le2], f"w (<= 2 contributions, step {step})")
+        assert_bitwise(bg[le2], b_ref[le2], f"b (<= 2 contributions, step {step})")
         assert np.all(np.abs(wg.astype(np.float64) - w_ref) <= 1e-6 * (np.abs(w_ref) + S))
         assert np.all(np.abs(bg.astype(np.float64) - b_ref) <= 1e-6 * (np.abs(b_ref) + S / 0.1))
         # carry the GPU state forward so later steps test one step at a time
