@@ -211,6 +211,25 @@ int tkef_sparsify1(const float *g, float *r, int64_t d, int64_t k, int32_t *idx_
                    float *val_out, void *ws, size_t ws_bytes, uint32_t *status,
                    hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * tkef_sparsify1 without a workspace argument. Its scratch is a fixed array of
+ * TKEF_STATIC_SCRATCH_BYTES in the library's device memory, one per GPU, held
+ * until the process ends; the first call on a device looks up that device's
+ * copy. Limits: 1 <= d <= TKEF_STATIC_MAX_D and 1 <= k <= min(d,
+ * TKEF_STATIC_MAX_K) (TKEF_ERANGE otherwise). The call allocates nothing and
+ * does not synchronize: four kernels on `stream` (a set-up kernel, then the
+ * three of the exact selection). Results are those of tkef_sparsify1. All
+ * calls on one GPU use that GPU's one array, which keeps the last call's
+ * contents (each call clears what must start at zero): calls that overlap in
+ * time on one GPU (other streams, other host threads) race and give wrong
+ * results. */
+#define TKEF_STATIC_MAX_D (1LL << 26)
+#define TKEF_STATIC_MAX_K (1LL << 17)
+#define TKEF_STATIC_SCRATCH_BYTES ((size_t)36 << 20)
+int tkef_sparsify1_static(const float *g, float *r, int64_t d, int64_t k, int32_t *idx_out,
+                          float *val_out, uint32_t *status, hipStream_t stream);
+
 /* ========================================================================
  * Sparse aggregate + merged multi-tensor SGD update
  * (Alg. 2, accumulation of the gathered lists; Eq. (1) update)

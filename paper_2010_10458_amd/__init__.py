@@ -86,6 +86,7 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
         "tkef_sparsify": ([P(vp), P(vp), P(i64), i32, i32, f64, i64, i32, vp, vp, P(i64), vp,
                            sz, vp, vp], ctypes.c_int),
         "tkef_sparsify1": ([vp, vp, i64, i64, vp, vp, vp, sz, vp, vp], ctypes.c_int),
+        "tkef_sparsify1_static": ([vp, vp, i64, i64, vp, vp, vp, vp], ctypes.c_int),
         "tkef_aggregate_workspace": ([P(i64), i32, i32, P(sz)], ctypes.c_int),
         "tkef_aggregate_update": ([P(vp), P(vp), P(i64), i32, P(vp), P(vp), P(i64), i32, f32,
                                    f32, f32, vp, sz, vp, vp], ctypes.c_int),
@@ -538,6 +539,36 @@ def sparsify1(g: torch.Tensor, r: torch.Tensor, k: int,
         _stream_handle(None)))
     _finish("tkef_sparsify1", status, own)
     return idx[: int(k)], val[: int(k)]
+
+
+STATIC_MAX_D = 1 << 26
+STATIC_MAX_K = 1 << 17
+
+
+def sparsify1_static(g: torch.Tensor, r: torch.Tensor, k: int,
+                     idx_out: Optional[torch.Tensor] = None,
+                     val_out: Optional[torch.Tensor] = None,
+                     status: Optional[torch.Tensor] = None, stream=None
+                     ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """tkef_sparsify1 with the library's fixed scratch (tkef_sparsify1_static,
+    for callers that cannot allocate): no workspace, no synchronization.
+    With idx_out / val_out / status given, this function allocates nothing
+    either; the status word, when given, is the caller's to check."""
+    _check_f32_tensors([g, r], "sparsify1_static")
+    d = g.numel()
+    if r.numel() != d:
+        raise ValueError("g and r differ in size")
+    if idx_out is None:
+        idx_out = torch.empty(max(int(k), 1), dtype=torch.int32, device=g.device)
+    if val_out is None:
+        val_out = torch.empty(max(int(k), 1), dtype=torch.float32, device=g.device)
+    if idx_out.numel() < k or val_out.numel() < k or idx_out.dtype != torch.int32 or \
+            val_out.dtype != torch.float32:
+        raise ValueError("idx_out (int32) and val_out (float32) must hold k entries")
+    _check("tkef_sparsify1_static", lib().tkef_sparsify1_static(
+        g.data_ptr(), r.data_ptr(), d, int(k), idx_out.data_ptr(), val_out.data_ptr(),
+        status.data_ptr() if status is not None else None, _stream_handle(stream)))
+    return idx_out[: int(k)], val_out[: int(k)]
 
 
 def aggregate_update(params: Sequence[torch.Tensor],

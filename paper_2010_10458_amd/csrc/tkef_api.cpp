@@ -348,6 +348,57 @@ extern "C" int tkef_sparsify_plan_group_k(tkef_sparsify_plan plan, int64_t* k_ou
   return TKEF_OK;
 }
 
+namespace {
+
+// The exact selection of one group: stream, collect, finish. The workspace at
+// base is laid out by sparsify_layout, its tables are written and the zeroed
+// scratch copy starts at zb; finish clears clear_words words at clear_next
+// for the next execution.
+hipError_t run_one_group(const tkef_sparsify_plan_s* p, char* base, char* zb,
+                         uint32_t* clear_next, int64_t clear_words, int32_t* idx_out,
+                         void* val_out, int val16, uint32_t* status, hipStream_t s,
+                         const Tracer& tr) {
+  const TileDesc* tiles = reinterpret_cast<const TileDesc*>(base + p->off_tiles);
+  const GroupDesc* groups = reinterpret_cast<const GroupDesc*>(base + p->off_groups);
+  GroupState* st = reinterpret_cast<GroupState*>(base + p->off_state);
+  uint32_t* hist1 = reinterpret_cast<uint32_t*>(zb + p->off_hist1);
+  uint32_t* hist2 = reinterpret_cast<uint32_t*>(zb + p->off_hist2);
+  uint16_t* summ = reinterpret_cast<uint16_t*>(base + p->off_summ);
+  uint32_t* rcand = reinterpret_cast<uint32_t*>(base + p->off_rcand);
+  uint32_t* rband = reinterpret_cast<uint32_t*>(base + p->off_rband);
+  uint32_t* rbtmp = reinterpret_cast<uint32_t*>(base + p->off_rbtmp);
+  uint32_t* rsuf = reinterpret_cast<uint32_t*>(base + p->off_rsuf);
+  uint32_t* rcnt = reinterpret_cast<uint32_t*>(base + p->off_rcnt);
+  uint32_t* rbin = reinterpret_cast<uint32_t*>(base + p->off_rbin);
+  const int64_t nl = p->nlines;
+  const int lpt = p->sel_lpt, sg = p->sel_grid;
+  hipError_t e = launch_stream(tiles, p->ntiles, p->stream_grid, hist1, p->nslots, summ, status,
+                               s, tr.at(0));
+  if (e == hipSuccess)
+    e = launch_collect(tiles, groups, st, hist1, p->nslots, summ, nl, lpt, sg, p->sel_block,
+                       p->rcap, hist2, rbin, rcand, rband, rbtmp, rsuf, rcnt, s, tr.at(1));
+  if (e == hipSuccess)
+    e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, p->sel_block, p->rcap, hist2, rbin,
+                      rcand, rband, rsuf, rcnt, idx_out, val_out, val16, clear_next, clear_words,
+                      s, tr.at(2));
+  return e;
+}
+
+// Persistent stream grid: four workgroups per compute unit.
+int stream_grid_for(int64_t ntiles, int32_t* grid, int32_t* cus_out) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return TKEF_EHIP;
+  const int64_t units = ntiles * (kTile / kStreamUnit);
+  *grid = (int32_t)std::min<int64_t>((int64_t)4 * cus, units);
+  if (cus_out) *cus_out = cus;
+  return TKEF_OK;
+}
+
+}  // namespace
+
 extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* const* grads,
                                        float* const* residuals, void* ws, size_t ws_bytes,
                                        hipStream_t stream) {
@@ -366,14 +417,9 @@ extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* con
       plan->tiles[i].r = residuals[t] + s;
     }
   }
-  // persistent stream grid: four workgroups per compute unit
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      cus <= 0)
-    return TKEF_EHIP;
+  int32_t cus = 0;
+  if (stream_grid_for(plan->ntiles, &plan->stream_grid, &cus)) return TKEF_EHIP;
   const int64_t units = (int64_t)plan->ntiles * (kTile / kStreamUnit);
-  plan->stream_grid = (int32_t)std::min<int64_t>((int64_t)4 * cus, units);
   plan->count_grid = (int32_t)std::max<int64_t>(1, std::min<int64_t>((int64_t)8 * cus, (units + 1) / 2));
   // two candidate workgroups per compute unit are all resident at once
   plan->cand_grid = std::max(plan->line_grid, std::min(plan->sel_grid, 2 * cus));
@@ -466,6 +512,7 @@ extern "C" int tkef_sparsify_approx_result(tkef_sparsify_plan plan, void* ws, do
   return TKEF_OK;
 }
 
+
 extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t ws_bytes,
                                      int32_t* idx_out, void* val_out, uint32_t* status,
                                      hipStream_t s) {
@@ -540,24 +587,12 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     plan->executions++;
     return TKEF_OK;
   }
-  e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s,
-                    tr.at(li++));
   if (ng == 1) {
-    uint32_t* rcand = reinterpret_cast<uint32_t*>(base + plan->off_rcand);
-    uint32_t* rband = reinterpret_cast<uint32_t*>(base + plan->off_rband);
-    uint32_t* rbtmp = reinterpret_cast<uint32_t*>(base + plan->off_rbtmp);
-    uint32_t* rsuf = reinterpret_cast<uint32_t*>(base + plan->off_rsuf);
-    uint32_t* rcnt = reinterpret_cast<uint32_t*>(base + plan->off_rcnt);
-    uint32_t* rbin = reinterpret_cast<uint32_t*>(base + plan->off_rbin);
-    if (e == hipSuccess)
-      e = launch_collect(tiles, groups, st, hist1, plan->nslots, summ, nl, lpt, sg,
-                         plan->sel_block, plan->rcap, hist2, rbin, rcand, rband, rbtmp, rsuf,
-                         rcnt, s, tr.at(li++));
-    if (e == hipSuccess)
-      e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, plan->sel_block, plan->rcap, hist2,
-                        rbin, rcand, rband, rsuf, rcnt, idx_out, val_out, val16, clear_next,
-                        clear_words, s, tr.at(li++));
+    e = run_one_group(plan, base, zb, clear_next, clear_words, idx_out, val_out, val16, status,
+                      s, tr);
   } else {
+    e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s,
+                      tr.at(li++));
     uint32_t* hist3 = reinterpret_cast<uint32_t*>(zb + plan->off_hist3);
     uint64_t* flags1 = reinterpret_cast<uint64_t*>(zb + plan->off_flags1);
     uint64_t* flags2 = reinterpret_cast<uint64_t*>(zb + plan->off_flags2);
@@ -624,6 +659,47 @@ extern "C" int tkef_sparsify1(const float* g, float* r, int64_t d, int64_t k, in
   float* rs[1] = {r};
   return tkef_sparsify(gs, rs, &d, 1, TKEF_GLOBAL, 0.0, k, TKEF_VAL_F32, idx_out, val_out,
                        nullptr, ws, ws_bytes, status, stream);
+}
+
+extern "C" int tkef_sparsify1_static(const float* g, float* r, int64_t d, int64_t k,
+                                     int32_t* idx_out, float* val_out, uint32_t* status,
+                                     hipStream_t stream) {
+  static_assert(TKEF_STATIC_MAX_D == kStaticMaxD && TKEF_STATIC_MAX_K == kStaticMaxK &&
+                    TKEF_STATIC_SCRATCH_BYTES == kStaticScratchBytes,
+                "header and library agree on the fixed scratch");
+  if (!g || !r || !idx_out || !val_out) return TKEF_EINVAL;
+  if (d < 1 || d > kStaticMaxD || k < 1 || k > d || k > kStaticMaxK) return TKEF_ERANGE;
+  if (ranges_overlap(g, r, d)) return TKEF_EINVAL;
+  // the layout of a one-tensor global plan, computed without allocating
+  // (the plan's vectors stay empty)
+  tkef_sparsify_plan_s p;
+  p.ntensors = 1;
+  p.mode = TKEF_GLOBAL;
+  p.ngroups = 1;
+  p.d = d;
+  p.k_total = k;
+  p.ntiles = (int32_t)((d + kTile - 1) / kTile);
+  p.nlines = (int64_t)p.ntiles * kLinesPerTile;
+  if (!sparsify_layout(&p)) return TKEF_ERANGE;
+  if (p.ws_bytes > kStaticScratchBytes) return TKEF_EWORKSPACE;  // (not within the limits)
+  if (stream_grid_for(p.ntiles, &p.stream_grid, nullptr)) return TKEF_EHIP;
+  hipError_t e = hipSuccess;
+  char* base = static_cast<char*>(static_scratch(&e));
+  if (!base) return TKEF_EHIP;
+  // the array keeps the previous call's contents: the set-up kernel writes
+  // the tables, clears the histograms and the last tile's line summaries
+  // (the stream rewrites the summaries of every line that holds elements)
+  char* zb = base + p.off_zero[0];
+  uint16_t* summ = reinterpret_cast<uint16_t*>(base + p.off_summ);
+  e = launch_setup_one(reinterpret_cast<TileDesc*>(base + p.off_tiles),
+                       reinterpret_cast<GroupDesc*>(base + p.off_groups), g, r, d, k, p.ntiles,
+                       reinterpret_cast<uint32_t*>(zb), (int64_t)(p.zero_bytes / 4),
+                       reinterpret_cast<uint32_t*>(summ + (int64_t)(p.ntiles - 1) * kLinesPerTile),
+                       kLinesPerTile / 2, stream);
+  if (e == hipSuccess)
+    e = run_one_group(&p, base, zb, nullptr, 0, idx_out, val_out, 0, status, stream,
+                      Tracer{nullptr, 0});
+  return hip_rc(e);
 }
 
 // ============================================================================

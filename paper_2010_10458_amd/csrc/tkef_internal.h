@@ -120,6 +120,24 @@ struct WorkerList {      // 32 B, one per worker, written by the call
 };
 static_assert(sizeof(WorkerList) == 32, "WorkerList layout");
 
+// ---- fixed scratch for callers that cannot allocate --------------------------
+// One single-tensor exact selection of d <= kStaticMaxD elements with
+// k <= kStaticMaxK needs at most 35.1 MiB of workspace (checked over every
+// tile count by the host tests); the array holds 36 MiB.
+constexpr int64_t kStaticMaxD = (int64_t)1 << 26;
+constexpr int64_t kStaticMaxK = (int64_t)1 << 17;
+constexpr size_t kStaticScratchBytes = (size_t)36 << 20;
+// Device address of the current device's copy of the fixed scratch array
+// (looked up once per device with hipGetSymbolAddress); null on failure, with
+// the HIP error in *err.
+void* static_scratch(hipError_t* err);
+// Writes the tile table and group descriptor of one tensor of d elements
+// (k pairs) into the workspace, and zeroes n_zero words at zero and
+// n_tail words at tail.
+hipError_t launch_setup_one(TileDesc* tiles, GroupDesc* groups, const float* g, float* r,
+                            int64_t d, int64_t k, int32_t ntiles, uint32_t* zero, int64_t n_zero,
+                            uint32_t* tail, int64_t n_tail, hipStream_t s);
+
 // ---- kernel launchers (tkef_kernels.hip) --------------------------------------
 // Optional timing events attached to one launch (recorded by the dispatch
 // itself at the kernel's start and end).

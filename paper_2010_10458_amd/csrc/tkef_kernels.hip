@@ -21,6 +21,8 @@
 //            are ascending, so tile boundaries are where idx >> shift grows)
 //   update   per tile: LDS accumulation of all workers' entries of the tile,
 //            then one pass applying the SGD step to that parameter range
+#include <mutex>
+
 #include <hip/hip_ext.h>
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -2626,6 +2628,63 @@ __global__ __launch_bounds__(kSBlock) void k_ms_emit(
 }
 
 // ---------------------------------------------------------------------------
+// Fixed scratch for the entry point that allocates nothing: one array per
+// GPU, in the library's device memory until the process ends. Host code
+// never passes the array's name to a kernel (on the host it only names a
+// stand-in); it uses the address hipGetSymbolAddress returns for the current
+// device, kept per device.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+void* static_scratch(hipError_t* err) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess && (dev < 0 || dev >= kMaxDevices)) e = hipErrorInvalidDevice;
+  if (e != hipSuccess) {
+    *err = e;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      *err = e != hipSuccess ? e : hipErrorInvalidSymbol;
+      return nullptr;
+    }
+    addr[dev] = ptr;
+  }
+  *err = hipSuccess;
+  return addr[dev];
+}
+
+// The descriptors of one tensor (what bind copies from the host for a plan)
+// and the words that must start at zero.
+__global__ void k_setup_one(TileDesc* __restrict__ tiles, GroupDesc* __restrict__ groups,
+                            const float* g, float* r, int64_t d, int64_t k, int32_t ntiles,
+                            uint32_t* __restrict__ zero, int64_t n_zero,
+                            uint32_t* __restrict__ tail, int64_t n_tail) {
+  const int64_t step = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < ntiles; i += step) {
+    TileDesc t;
+    t.g = g + i * kTile;
+    t.r = r + i * kTile;
+    t.gstart = (int32_t)(i * kTile);
+    t.len = (int32_t)min((int64_t)kTile, d - i * kTile);
+    t.group = 0;
+    t.reserved = 0;
+    tiles[i] = t;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) groups[0] = GroupDesc{(uint32_t)k, 0u, 0u, 0u};
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_zero; i += step)
+    zero[i] = 0u;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_tail; i += step)
+    tail[i] = 0u;
+}
+
+// ---------------------------------------------------------------------------
 // launchers (the timing events, when given, are recorded by the dispatch)
 
 template <typename K, typename... Args>
@@ -2639,6 +2698,19 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s) {
   int64_t blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   return launch(k_fill_u32, dim3((unsigned)blocks), dim3(256), s, Ev{}, p, v, n);
+}
+
+hipError_t launch_setup_one(TileDesc* tiles, GroupDesc* groups, const float* g, float* r,
+                            int64_t d, int64_t k, int32_t ntiles, uint32_t* zero, int64_t n_zero,
+                            uint32_t* tail, int64_t n_tail, hipStream_t s) {
+  int64_t n = ntiles;
+  if (n_zero > n) n = n_zero;
+  if (n_tail > n) n = n_tail;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 1024) blocks = 1024;
+  return launch(k_setup_one, dim3((unsigned)blocks), dim3(256), s, Ev{}, tiles, groups, g, r, d,
+                k, ntiles, zero, n_zero, tail, n_tail);
 }
 
 hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, uint32_t* hist1,

@@ -303,3 +303,28 @@ def test_aggregate_update_host_side():
     assert call(params=(P_ * 2)(None, P_(0x2000))) == tk.EINVAL
     overlap = (P_ * 2)(P_(0x1000 + 4), P_(0x200000))
     assert call(mom=overlap, mu=0.9) == tk.EINVAL
+
+
+def test_static_entry_point_host_side():
+    """tkef_sparsify1_static (no workspace): its limits are refused on the
+    host, and every single-tensor layout within them (each tile count up to
+    2^26 elements, with the largest k allowed) fits the fixed scratch."""
+    L = tk.lib()
+    P_ = ctypes.c_void_p
+    g, r, i, v = P_(0x1000), P_(0x40000000), P_(0x10), P_(0x20)
+    for d, k in ((0, 1), (10, 0), (10, 11), (tk.STATIC_MAX_D + 1, 5),
+                 (tk.STATIC_MAX_D, tk.STATIC_MAX_K + 1), (2**31, 1)):
+        assert L.tkef_sparsify1_static(g, r, d, k, i, v, None, None) == tk.ERANGE, (d, k)
+    assert L.tkef_sparsify1_static(None, r, 10, 1, i, v, None, None) == tk.EINVAL
+    assert L.tkef_sparsify1_static(g, r, 10, 1, None, v, None, None) == tk.EINVAL
+    assert L.tkef_sparsify1_static(g, P_(0x1000 + 4), 10, 1, i, v, None, None) == tk.EINVAL
+    limit = 36 << 20
+    worst = 0
+    nb = ctypes.c_size_t()
+    for ntiles in range(1, tk.STATIC_MAX_D // 8192 + 1):
+        d = ntiles * 8192
+        k = min(tk.STATIC_MAX_K, d)
+        assert L.tkef_sparsify_workspace((ctypes.c_int64 * 1)(d), 1, tk.GLOBAL, 0.0, k,
+                                         ctypes.byref(nb), None) == tk.OK
+        worst = max(worst, nb.value)
+    assert worst <= limit, worst
