@@ -145,7 +145,8 @@ struct tkef_sparsify_plan_s {
   size_t off_tiles = 0, off_groups = 0, off_state = 0, off_zero[2] = {0, 0}, zero_bytes = 0,
          off_hist1 = 0, off_hist2 = 0, off_hist3 = 0, off_flags1 = 0, off_flags2 = 0,
          off_meta = 0, off_summ = 0, off_base = 0, off_cand = 0, off_rcand = 0, off_rband = 0,
-         off_rsuf = 0, off_rcnt = 0, off_rbin = 0, off_rbtmp = 0, ws_bytes = 0;
+         off_rsuf = 0, off_rcnt = 0, off_rbin = 0, off_rbtmp = 0, off_ticket = 0, off_rzr = 0,
+         ws_bytes = 0;
   int32_t val_format = TKEF_VAL_F32;  // value array written by execute
   // MSTopK (TKEF_APPROX): rounds, offset word, scratch
   int32_t ms_rounds = 30;
@@ -190,13 +191,16 @@ bool sparsify_layout(tkef_sparsify_plan_s* p) {
   // Candidates are the positions at or above the level-1 threshold bin:
   // about k plus one bin's worth. One group: each region (the lines of one
   // workgroup) stores up to rcap of them, several times the even share of
-  // 8k + 65536; per tensor: one compacted list of 4k + 65536. Heavier inputs
-  // fall back to re-reading lines.
+  // 8k + 65536, and at least 1/64 of the region (a level-1 bin, 1/8 of an
+  // octave, can hold a percent of the data when the residual has piled mass
+  // just below the threshold); per tensor: one compacted list of
+  // 4k + 65536. Heavier inputs fall back to re-reading lines.
   if (one) {
     p->sel_grid = (int32_t)std::max<int64_t>(1, g_lines);
     const int64_t region = lpt * sb * kLine;
     const int64_t share = (8 * p->k_total + 65536 + p->sel_grid - 1) / p->sel_grid;
-    p->rcap = (uint32_t)std::min<int64_t>(region, std::max<int64_t>(4096, (share + 63) / 64 * 64));
+    p->rcap = (uint32_t)std::min<int64_t>(
+        region, std::max<int64_t>(std::max<int64_t>(4096, (share + 63) / 64 * 64), region / 64));
   } else {
     p->cand_cap = (uint32_t)std::min<int64_t>(p->d, 4 * p->k_total + 65536);
     const int64_t g_cands = std::min<int64_t>(sg, ((int64_t)p->cand_cap + sb * 4 - 1) / (sb * 4));
@@ -222,6 +226,9 @@ bool sparsify_layout(tkef_sparsify_plan_s* p) {
   } else {
     p->off_hist1 = z;   z = align_up(z + (size_t)p->ngroups * p->nslots * kH1Bins * 4);
     p->off_hist2 = z;   z = align_up(z + (size_t)p->ngroups * kH2Bins * 4);
+    if (one) {
+      p->off_ticket = z;  z = align_up(z + 4);  // finish's last-workgroup ticket
+    }
   }
   if (!one) {
     p->off_hist3 = z;   z = align_up(z + (size_t)p->ngroups * kH3Bins * 4);
@@ -243,6 +250,7 @@ bool sparsify_layout(tkef_sparsify_plan_s* p) {
     p->off_rsuf = o;   o = align_up(o + (size_t)p->sel_grid * kH2Bins * 4);
     p->off_rcnt = o;   o = align_up(o + (size_t)p->sel_grid * 8);
     p->off_rbin = o;   o = align_up(o + (size_t)kH2Bins * p->sel_grid * kPerBin * 4);
+    p->off_rzr = o;    o = align_up(o + (size_t)p->sel_grid * 8);  // deferred residual slots
   } else {
     p->off_base = o;   o = align_up(o + (size_t)p->ngroups * 8);
     p->off_cand = o;   o = align_up(o + (size_t)p->cand_cap * 8);  // {code, bits of x}
@@ -380,7 +388,8 @@ hipError_t run_one_group(const tkef_sparsify_plan_s* p, char* base, char* zb,
   if (e == hipSuccess)
     e = launch_finish(tiles, groups, st, summ, nl, lpt, sg, p->sel_block, p->rcap, hist2, rbin,
                       rcand, rband, rsuf, rcnt, idx_out, val_out, val16, clear_next, clear_words,
-                      s, tr.at(2));
+                      reinterpret_cast<uint32_t*>(zb + p->off_ticket),
+                      reinterpret_cast<uint32_t*>(base + p->off_rzr), s, tr.at(2));
   return e;
 }
 

@@ -164,7 +164,8 @@ hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          const uint32_t* rbin, const uint32_t* rcand, const uint32_t* rband,
                          const uint32_t* rsuf,
                          const uint32_t* rcnt, int32_t* idx_out, void* val_out, int val16,
-                         uint32_t* clear_next, int64_t clear_words, hipStream_t s, const Ev& ev);
+                         uint32_t* clear_next, int64_t clear_words, uint32_t* ticket,
+                         uint32_t* rzr, hipStream_t s, const Ev& ev);
 // several selection groups
 hipError_t launch_gather(const TileDesc* tiles, const GroupState* st, const uint16_t* summ,
                          int64_t nlines, int lpt, int32_t grid, uint32_t* hist2, uint64_t* flags,

@@ -226,7 +226,6 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v, int64_t n) {
 // histogram when the group changes and at the end; the copies spread the
 // atomics of many workgroups over many addresses.
 constexpr int kQuarter = kStreamUnit;
-constexpr int kQuarterLines = kQuarter / kLine;
 constexpr int kQV = kQuarter / (4 * kBlock);  // float4 of each array per thread per unit
 static_assert(kQV * 4 * kBlock == kQuarter && kTile % kQuarter == 0, "stream unit shape");
 
@@ -273,7 +272,6 @@ __global__ __launch_bounds__(kBlock) void k_stream(const TileDesc* __restrict__ 
                                                    int nslots, uint16_t* __restrict__ summ,
                                                    uint32_t* __restrict__ status) {
   __shared__ uint32_t h[kH1Bins];
-  __shared__ uint32_t lmax[kQuarterLines];
   __shared__ uint32_t nanflag;
   const int tid = threadIdx.x;
   for (int i = tid; i < kH1Bins; i += kBlock) h[i] = 0u;
@@ -320,34 +318,38 @@ __global__ __launch_bounds__(kBlock) void k_stream(const TileDesc* __restrict__ 
         if ((tid & 7) == 0) sq[(v * kBlock + tid) >> 3] = (uint16_t)(m >> 16);
       }
     } else {
-      // partial or misaligned quarter: element by element, every load issued
-      // before the first use so the quarter costs one memory latency
+      // partial or misaligned quarter: element by element (coalesced 4-byte
+      // accesses), every load issued before the first use so the quarter
+      // costs one memory latency. Element e = q * kBlock + tid: a wavefront's
+      // 64 lanes hold two whole lines, so a line's maximum key is a
+      // reduction over 32 lanes (lanes past the end contribute 0); the
+      // summary of a line without elements is not written.
       constexpr int kPer = kQuarter / kBlock;
-      if (tid < kQuarterLines) lmax[tid] = 0u;
-      __syncthreads();
       float gv[kPer], rv[kPer];
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int e = q * kBlock + tid;
-        gv[q] = (e < len) ? gptr(g)[e] : 0.0f;
-        rv[q] = (e < len) ? gptr(r)[e] : 0.0f;
+        gv[q] = (e < len) ? __builtin_nontemporal_load(gptr(g) + e) : 0.0f;
+        rv[q] = (e < len) ? __builtin_nontemporal_load(gptr(r) + e) : 0.0f;
       }
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int e = q * kBlock + tid;
+        uint32_t k = 0u;
         if (e < len) {
           const float x = gv[q] + rv[q];
-          gptr(r)[e] = x;
-          const uint32_t k = mag_key(x);
+          __builtin_nontemporal_store(x, gptr(r) + e);
+          k = mag_key(x);
           atomicAdd(&h[k >> kH1Shift], 1u);
-          atomicMax(&lmax[e / kLine], k);
           tmax = max(tmax, k);
         }
+        k = max(k, (uint32_t)__shfl_xor((int)k, 1));
+        k = max(k, (uint32_t)__shfl_xor((int)k, 2));
+        k = max(k, (uint32_t)__shfl_xor((int)k, 4));
+        k = max(k, (uint32_t)__shfl_xor((int)k, 8));
+        k = max(k, (uint32_t)__shfl_xor((int)k, 16));
+        if ((tid & (kLine - 1)) == 0 && e < len) sq[e / kLine] = (uint16_t)(k >> 16);
       }
-      __syncthreads();
-      const int nlines = (len + kLine - 1) / kLine;
-      if (tid < nlines) sq[tid] = (uint16_t)(lmax[tid] >> 16);
-      __syncthreads();
     }
   }
   if (cur >= 0) flush_hist(h, hist1 + ((size_t)cur * nslots + slot) * kH1Bins);
@@ -984,20 +986,29 @@ __global__ __launch_bounds__(NT) void k_finish(
     const uint32_t* __restrict__ rband,
     const uint32_t* __restrict__ rsuf, const uint2* __restrict__ rcnt,
     int32_t* __restrict__ idx_out, void* __restrict__ val_out, int val16,
-    uint32_t* __restrict__ clear_next, int64_t clear_words) {
+    uint32_t* __restrict__ clear_next, int64_t clear_words, uint32_t* __restrict__ ticket,
+    uint64_t* __restrict__ rzr) {
   __shared__ __align__(16) uint32_t h[kH3Bins];
   __shared__ uint32_t wsum[4 * (NT / 64)];
   __shared__ uint32_t res[3];
   __shared__ uint32_t off[NT], abv[NT];
   __shared__ uint32_t ovbits[kOvWords];  // regions whose band keys were not stored
+  __shared__ uint32_t c2bits[kOvWords];  // ... of them, those holding level-2 class members
   __shared__ uint32_t c2key[kC2Cap];     // level-2 class members of the stored regions
   __shared__ uint16_t c2reg[kC2Cap];     // ... and their regions
   __shared__ uint32_t n2;
+  __shared__ uint32_t any_unstored, last;
   constexpr int kRegPerThread = kSMaxGroups / NT;
   const int tid = threadIdx.x, w = blockIdx.x, G = gridDim.x;
   for (int i = tid; i < kH3Bins; i += NT) h[i] = 0u;
-  for (int i = tid; i < kOvWords; i += NT) ovbits[i] = 0u;
-  if (tid == 0) n2 = 0u;
+  for (int i = tid; i < kOvWords; i += NT) {
+    ovbits[i] = 0u;
+    c2bits[i] = 0u;
+  }
+  if (tid == 0) {
+    n2 = 0u;
+    any_unstored = 0u;
+  }
 
   // fetched together: level-1 state, this region's counts and first
   // candidate, every region's counts (and, in the pick, the level-2 histogram)
@@ -1040,7 +1051,10 @@ __global__ __launch_bounds__(NT) void k_finish(
     if (r >= G) continue;
     const uint32_t bw = cr[q].y & 0x7FFFFFFFu;
     const bool ov = (cr[q].y >> 31) != 0u;
-    if (ov) atomicOr(&ovbits[r >> 5], 1u << (r & 31));
+    if (ov) {
+      atomicOr(&ovbits[r >> 5], 1u << (r & 31));
+      any_unstored = 1u;
+    }
     if (!bw) {
       if (r < w) gtb += cr[q].x & 0x7FFFFFFFu;
       continue;
@@ -1050,7 +1064,10 @@ __global__ __launch_bounds__(NT) void k_finish(
     const uint32_t at = (B2 ? sr[B2 - 1] : bw) - above;
     const uint4 e = *reinterpret_cast<const uint4*>(rbin + ((size_t)B2 * G + r) * kPerBin);
     if (r < w) gtb += (cr[q].x & 0x7FFFFFFFu) - bw + above;
-    if (ov) continue;
+    if (ov) {
+      if (at) atomicOr(&c2bits[r >> 5], 1u << (r & 31));  // its lines are walked below
+      continue;
+    }
     if (at > (uint32_t)kPerBin) {
       slow = true;
       continue;
@@ -1110,13 +1127,14 @@ __global__ __launch_bounds__(NT) void k_finish(
       __syncthreads();
     }
   }
-  // class-2 members of the regions without stored band keys: from their lines
+  // class-2 members of the regions without stored band keys: from the lines
+  // of those that hold any (their count is known from rsuf)
   const uint32_t thr2 = cls21 << kH2Shift;
   auto in_cls2 = [&](int, uint32_t key) -> bool { return (key >> kH2Shift) == cls21; };
   auto lines_class2 = [&](int wlim, auto f) {
 #pragma unroll 1
     for (int wi = 0; wi * 32 < wlim; ++wi) {
-      uint32_t m = ovbits[wi];
+      uint32_t m = c2bits[wi];
 #pragma unroll 1
       while (m) {
         const int r = wi * 32 + __ffs(m) - 1;
@@ -1189,7 +1207,16 @@ __global__ __launch_bounds__(NT) void k_finish(
 #pragma unroll 1
   for (int64_t i = (int64_t)w * NT + tid; i < clear_words; i += (int64_t)G * NT)
     clear_next[i] = 0u;
-  if (gt + eq == 0u) return;
+  // Other workgroups read the lines of the regions whose band keys were not
+  // stored (their level-2 class members, above), so such a region does not
+  // zero its residuals here: it records its range of output slots, and the
+  // last workgroup to finish zeroes the residuals at those slots' indices.
+  const bool defer = (mine.y >> 31) != 0u;
+  if (defer && tid == 0) {
+    const uint32_t lo = tot[2] + min(tot[3], need3);
+    const uint32_t hi = tot[2] + tot[0] + min(tot[3] + tot[1], need3);
+    rzr[w] = (uint64_t)min(lo, k) | ((uint64_t)min(hi, k) << 32);
+  }
   uint32_t gtr = tot[2] + pre[0];
   uint32_t eqr = tot[3] + pre[1];
   // write
@@ -1207,10 +1234,12 @@ __global__ __launch_bounds__(NT) void k_finish(
     if (pos < k) {
       idx_out[pos] = (int32_t)gidx;
       put_val(val_out, pos, x, val16);
-      *gptr(rp) = 0.0f;
+      if (!defer) *gptr(rp) = 0.0f;
     }
   };
-  if (own_ov) {
+  if (gt + eq == 0u) {
+    // nothing to write
+  } else if (own_ov) {
     walk_mask(ls, mask, at_least_T, [&](int, const TileDesc& t, int e, float x, uint32_t) {
       write((uint32_t)(t.gstart + e), t.r + e, x);
     });
@@ -1227,6 +1256,41 @@ __global__ __launch_bounds__(NT) void k_finish(
 #pragma unroll
       for (int c = 0; c < 4; ++c)
         if (j + (uint32_t)c < ce) write_c(q[c]);
+    }
+  }
+  if (!any_unstored) return;  // (uniform) the common case ends here
+  // Every workgroup has read all it reads of the unstored regions' lines and
+  // written its outputs; the one that takes the last ticket zeroes the
+  // deferred residuals. No workgroup waits for another.
+  __syncthreads();
+  if (tid == 0) {
+    __threadfence();
+    last = (atomicAdd(ticket, 1u) == (uint32_t)G - 1u) ? 1u : 0u;
+    __threadfence();
+  }
+  __syncthreads();
+  if (!last) return;
+  const int32_t ntiles = (int32_t)(nlines / kLinesPerTile);
+#pragma unroll 1
+  for (int wi = 0; wi * 32 < G; ++wi) {
+    uint32_t m = ovbits[wi];
+#pragma unroll 1
+    while (m) {
+      const int r = wi * 32 + __ffs(m) - 1;
+      m &= m - 1u;
+      const uint64_t rg = __hip_atomic_load(&rzr[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll 1
+      for (uint32_t j = (uint32_t)rg + tid; j < (uint32_t)(rg >> 32); j += NT) {
+        const int32_t gi = __hip_atomic_load(&idx_out[j], __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+        int a = 0, b = ntiles - 1;  // the last tile starting at or before gi
+        while (a < b) {
+          const int mid = (a + b + 1) >> 1;
+          if (tiles[mid].gstart <= gi) a = mid; else b = mid - 1;
+        }
+        const TileDesc t = tiles[a];
+        gptr(t.r)[gi - t.gstart] = 0.0f;
+      }
     }
   }
 }
@@ -2317,7 +2381,6 @@ __global__ __launch_bounds__(kBlock) void k_ms_stream(const TileDesc* __restrict
                                                       uint16_t* __restrict__ summ) {
   __shared__ unsigned long long es[kH1Bins];
   __shared__ unsigned long long dig[kMsDigits];
-  __shared__ uint32_t lmax[kQuarterLines];
   __shared__ uint32_t bmax;
   const int tid = threadIdx.x;
   for (int i = tid; i < kH1Bins; i += kBlock) es[i] = 0ull;
@@ -2367,32 +2430,34 @@ __global__ __launch_bounds__(kBlock) void k_ms_stream(const TileDesc* __restrict
         if ((tid & 7) == 0) sq[(v * kBlock + tid) >> 3] = (uint16_t)(m >> 16);
       }
     } else {
+      // partial or misaligned quarter, as in k_stream: element by element,
+      // line maxima reduced over the 32 lanes that hold each line
       constexpr int kPer = kQuarter / kBlock;
-      if (tid < kQuarterLines) lmax[tid] = 0u;
-      __syncthreads();
       float gv[kPer], rv[kPer];
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int e = q * kBlock + tid;
-        gv[q] = (e < len) ? gptr(g)[e] : 0.0f;
-        rv[q] = (e < len) ? gptr(r)[e] : 0.0f;
+        gv[q] = (e < len) ? __builtin_nontemporal_load(gptr(g) + e) : 0.0f;
+        rv[q] = (e < len) ? __builtin_nontemporal_load(gptr(r) + e) : 0.0f;
       }
 #pragma unroll
       for (int q = 0; q < kPer; ++q) {
         const int e = q * kBlock + tid;
+        uint32_t k = 0u;
         if (e < len) {
           const float x = gv[q] + rv[q];
-          gptr(r)[e] = x;
-          const uint32_t k = mag_key(x);
+          __builtin_nontemporal_store(x, gptr(r) + e);
+          k = mag_key(x);
           ms_accum(k, es);
-          atomicMax(&lmax[e / kLine], k);
           tmax = max(tmax, k);
         }
+        k = max(k, (uint32_t)__shfl_xor((int)k, 1));
+        k = max(k, (uint32_t)__shfl_xor((int)k, 2));
+        k = max(k, (uint32_t)__shfl_xor((int)k, 4));
+        k = max(k, (uint32_t)__shfl_xor((int)k, 8));
+        k = max(k, (uint32_t)__shfl_xor((int)k, 16));
+        if ((tid & (kLine - 1)) == 0 && e < len) sq[e / kLine] = (uint16_t)(k >> 16);
       }
-      __syncthreads();
-      const int nl = (len + kLine - 1) / kLine;
-      if (tid < nl) sq[tid] = (uint16_t)(lmax[tid] >> 16);
-      __syncthreads();
     }
   }
   atomicMax(&bmax, tmax);
@@ -2756,18 +2821,19 @@ hipError_t launch_finish(const TileDesc* tiles, const GroupDesc* groups,
                          int32_t grid, int32_t block, uint32_t rcap, const uint32_t* hist2, const uint32_t* rbin,
                          const uint32_t* rcand, const uint32_t* rband, const uint32_t* rsuf,
                          const uint32_t* rcnt, int32_t* idx_out, void* val_out, int val16,
-                         uint32_t* clear_next, int64_t clear_words, hipStream_t s,
-                         const Ev& ev) {
+                         uint32_t* clear_next, int64_t clear_words, uint32_t* ticket,
+                         uint32_t* rzr, hipStream_t s, const Ev& ev) {
+  uint64_t* rz = reinterpret_cast<uint64_t*>(rzr);
   if (block == kCBlockSmall)
     return launch(k_finish<kCBlockSmall>, dim3(grid), dim3(block), s, ev, tiles, groups, st, summ,
                   nlines, lpt, rcap, hist2, rbin, reinterpret_cast<const uint4*>(rcand), rband,
                   rsuf, reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, val16,
-                  clear_next, clear_words);
+                  clear_next, clear_words, ticket, rz);
   if (block == kSBlock)
     return launch(k_finish<kSBlock>, dim3(grid), dim3(block), s, ev, tiles, groups, st, summ,
                   nlines, lpt, rcap, hist2, rbin, reinterpret_cast<const uint4*>(rcand), rband,
                   rsuf, reinterpret_cast<const uint2*>(rcnt), idx_out, val_out, val16,
-                  clear_next, clear_words);
+                  clear_next, clear_words, ticket, rz);
   return hipErrorInvalidValue;
 }
 

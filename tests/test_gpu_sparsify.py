@@ -375,3 +375,36 @@ def test_dense_selection_band_beyond_lds(rho):
     g = rng.standard_normal(n).astype(np.float32)
     r = (rng.standard_normal(n) * 0.01).astype(np.float32)
     compare_with_oracle([g], [r], rho=rho, label=f"dense rho={rho}")
+
+
+@pytest.mark.parametrize("case", ["one_region", "two_regions_ties", "every_region"])
+def test_band_beyond_region_capacity(case):
+    """One exact selection over 2^20 elements (16 regions of 65,536 for the
+    selection kernels, each storing at most 4,608 candidates at k = 1,000 or
+    3,500) where one or two regions hold 6,000-10,000 members of the
+    threshold's level-1 bin: those regions store neither their candidates nor
+    their band, and every later step reads their lines instead. With ties:
+    the band takes its magnitudes from 700 values, so the threshold class is
+    split by position. Every region: all sixteen hold 6,000 band members."""
+    rng = np.random.default_rng({"one_region": 4242, "two_regions_ties": 4343}.get(case, 4444))
+    n = 1 << 20
+    g = (rng.standard_normal(n) * 0.1).astype(np.float32)
+    top = rng.choice(n, 500, replace=False)
+    g[top] = (10 + rng.random(500)).astype(np.float32) * rng.choice([-1, 1], 500)
+    if case == "one_region":
+        pos = 3 * 65536 + rng.choice(65536, 10_000, replace=False)
+        g[pos] = (5 + 0.5 * rng.random(pos.size)).astype(np.float32) * rng.choice([-1, 1], pos.size)
+        k = 1000
+    elif case == "every_region":
+        pos = np.concatenate([q * 65536 + rng.choice(65536, 6000, replace=False)
+                              for q in range(16)])
+        g[pos] = (5 + 0.5 * rng.random(pos.size)).astype(np.float32) * rng.choice([-1, 1], pos.size)
+        k = 1000
+    else:
+        vals = (5 + 0.5 * rng.random(700)).astype(np.float32)
+        pos = np.concatenate([3 * 65536 + rng.choice(65536, 6000, replace=False),
+                              9 * 65536 + rng.choice(65536, 6000, replace=False)])
+        g[pos] = rng.choice(vals, pos.size) * rng.choice([-1, 1], pos.size).astype(np.float32)
+        k = 3500
+    r = np.zeros(n, np.float32)
+    compare_with_oracle([g], [r], k=k, label=f"band beyond region capacity ({case})")
