@@ -47,12 +47,13 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip timing the CPU oracle")
     ap.add_argument("--workload", default="resnet50",
-                    choices=["resnet50", "c1", "transformer", "bert"],
+                    choices=["resnet50", "c1", "transformer", "bert", "sweep"],
                     help="resnet50: the headline step (default); c1: one 1 M-element tensor, "
                          "rho 0.001, then a one-worker plain update; transformer: the 110 M "
                          "Transformer-shaped set, Laplace(0, 1e-3), rho 0.001 and 0.01, global "
                          "and per tensor; bert: one 340 M-element tie-stressed buffer, rho 0.001 "
-                         "(these three print sparsify rates only, no extras)")
+                         "(these three print sparsify rates only, no extras); sweep: flat "
+                         "N(0,1) vectors of 2^18 .. 2^27 elements, k = ceil(0.001 d)")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the variant paths timed after the step (fp16 values, dense "
                          "aggregation, shard-shaped sparsify)")
@@ -61,6 +62,17 @@ def parse_args():
     ap.add_argument("--probe-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy of MIB MiB five times (the "
                          "reference kernel for scaling HBM counter readings) and exit")
+    ap.add_argument("--probe-add", type=int, default=0, metavar="MIB",
+                    help="only run an elementwise add of two MIB MiB arrays into a third "
+                         "five times (two reads, one write: the stream's pattern) and exit")
+    ap.add_argument("--cpu-procs", type=int, default=0,
+                    help="processes of the all-core oracle leg (default: the usable cores, "
+                         "at most 16)")
+    ap.add_argument("--summarize-stats", metavar="CSV",
+                    help="print the tkef kernels of a rocprofv3 --stats kernel_stats.csv and exit")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("CSV", "COUNTER"),
+                    help="print per-dispatch averages of COUNTER per tkef kernel from a "
+                         "rocprofv3 --pmc counter_collection.csv and exit")
     return ap.parse_args()
 
 
@@ -76,6 +88,79 @@ def probe_copy(mib: int) -> int:
     print(json.dumps({"probe_copy_bytes_read": n * 4, "probe_copy_bytes_written": n * 4,
                       "launches": 5}), flush=True)
     return 0
+
+
+def probe_add(mib: int) -> int:
+    import torch
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, device="cuda:0")
+    b = torch.ones(n, device="cuda:0")
+    c = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        torch.add(a, b, out=c)
+    torch.cuda.synchronize()
+    print(json.dumps({"probe_add_bytes_read": 2 * n * 4, "probe_add_bytes_written": n * 4,
+                      "launches": 5}), flush=True)
+    return 0
+
+
+def _short_kernel(name: str) -> str:
+    n = name.split("(")[0]
+    return n[5:] if n.startswith("void ") else n
+
+
+def summarize_stats(path: str) -> int:
+    """Kernel table (calls, average / min / max duration) of the tkef kernels
+    in a rocprofv3 kernel_stats.csv."""
+    import csv
+    print(f"{'kernel':36s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} "
+          f"{'pct':>6s}")
+    for r in csv.DictReader(open(path)):
+        n = _short_kernel(r["Name"])
+        if n.startswith("tkef::"):
+            print(f"{n:36s} {int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:9.2f} "
+                  f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f} "
+                  f"{float(r['Percentage']):6.2f}")
+    return 0
+
+
+def summarize_pmc(path: str, counter: str) -> int:
+    """Per-dispatch average of one counter (summed over the dispatch's rows)
+    for every kernel in a rocprofv3 counter_collection.csv."""
+    import collections
+    import csv
+    per = collections.defaultdict(float)
+    names = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter:
+            continue
+        per[r["Dispatch_Id"]] += float(r["Counter_Value"])
+        names[r["Dispatch_Id"]] = _short_kernel(r["Kernel_Name"])
+    agg = collections.defaultdict(list)
+    for dsp, v in per.items():
+        agg[names[dsp]].append(v)
+    print(f"{'kernel':40s} {'dispatches':>10s} {counter + ' per dispatch':>28s}")
+    for n, vs in sorted(agg.items(), key=lambda kv: -max(kv[1])):
+        print(f"{n:40s} {len(vs):10d} {sum(vs) / len(vs):28.1f}")
+    return 0
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def usable_cores() -> int:
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
 
 
 def log(msg: str) -> None:
@@ -94,8 +179,10 @@ def kernel_source_digest() -> str:
 
 
 def read_traffic(kernel: str, digest: str):
-    """HBM bytes per launch measured by rocprofv3 counters, if a summary for
-    this kernel exists and was taken on the current kernel sources."""
+    """HBM traffic per launch measured by rocprofv3 counters, if a summary for
+    this kernel exists and was taken on the current kernel sources: the
+    scaled bytes, and the raw FETCH_SIZE / WRITE_SIZE readings with their
+    scale factors."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_resnet50.txt")
     if not os.path.exists(path):
         return None
@@ -107,13 +194,37 @@ def read_traffic(kernel: str, digest: str):
     if vals.get("source_digest") != digest:
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        fs, ws = (float(x) for x in vals["scale (fetch, write)"].split(","))
+        return {"bytes": float(vals["hbm_bytes_per_launch"]),
+                "fetch_kib_raw": float(vals["FETCH_SIZE per launch (raw KiB)"]),
+                "write_kib_raw": float(vals["WRITE_SIZE per launch (raw KiB)"]),
+                "fetch_scale": fs, "write_scale": ws}
     except (KeyError, ValueError):
         return None
 
 
-def cpu_baseline(sizes, d):
-    """The CPU oracle on one step of the same workload (bounded sample)."""
+def _oracle_worker(step, barrier, out):
+    """One process of the all-core leg: the oracle's sparsify of gradient
+    step `step` of the same workload, timed after every process is ready."""
+    import numpy as np
+
+    import gen
+    import oracle
+    orc = oracle.Oracle()
+    grads = gen.resnet_grads(step)
+    res = [np.zeros(a.size, np.float32) for a in grads]
+    barrier.wait()
+    t0 = time.perf_counter()
+    orc.sparsify(grads, res, rho=RHO)
+    out.put((t0, time.perf_counter()))
+
+
+def cpu_baseline(sizes, d, procs=0):
+    """The CPU oracle on bounded samples of the same workload: one sparsify
+    step (and one update) on one thread, then one sparsify step per process on
+    every usable core at once (the oracle as it is, one process per core)."""
+    import multiprocessing as mp
+
     import numpy as np
 
     import gen
@@ -124,19 +235,39 @@ def cpu_baseline(sizes, d):
     t0 = time.perf_counter()
     idx, val, _, ks = orc.sparsify(grads, res, rho=RHO)
     t_sp = time.perf_counter() - t0
+    del grads, res
     lists_i, lists_v = gen.sparse_lists(d, P_WORKERS, K_LIST, step=0)
     w = gen.concat(gen.params_like(sizes, config=5))
     b = np.zeros(d, np.float32)
     t0 = time.perf_counter()
     orc.update(w, b, lists_i, lists_v, lr=LR, mu=MU, wd=WD)
     t_up = time.perf_counter() - t0
+    del lists_i, lists_v, w, b
     upd_bytes = 16 * d + 8 * P_WORKERS * K_LIST
-    return {"value": round(d / t_sp / 1e9, 6), "unit": "Gelem/s", "cores": 1, "kind": "oracle",
-            "sample": f"one ResNet-50-shaped sparsify step (d={d}, k={ks[0]}, full comparison "
-                      f"sort) plus one P={P_WORKERS} x {K_LIST} momentum update, single thread",
-            "sparsify_s": round(t_sp, 3), "update_s": round(t_up, 3),
-            "update_GBps": round(upd_bytes / t_up / 1e9, 3),
-            "host_cpus": os.cpu_count()}
+    # all cores: spawned processes (the parent holds a GPU context, so no fork)
+    n = procs or min(16, usable_cores())
+    ctx = mp.get_context("spawn")
+    barrier, out = ctx.Barrier(n), ctx.Queue()
+    ps = [ctx.Process(target=_oracle_worker, args=(s % GRAD_STEPS, barrier, out))
+          for s in range(n)]
+    for p in ps:
+        p.start()
+    spans = [out.get() for _ in range(n)]
+    for p in ps:
+        p.join()
+    wall = max(e for _, e in spans) - min(b for b, _ in spans)
+    all_rate = n * d / wall / 1e9
+    return {"value": round(all_rate, 6), "unit": "Gelem/s", "cores": n, "kind": "oracle",
+            "sample": f"ResNet-50-shaped sparsify steps (d={d}, k={ks[0]}, full comparison "
+                      f"sort): one per process on {n} processes at once (value), and one on "
+                      f"a single thread; plus one P={P_WORKERS} x {K_LIST} momentum update "
+                      f"on a single thread",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+            "usable_cores": usable_cores(),
+            "all_cores_wall_s": round(wall, 3),
+            "single_thread": {"value": round(d / t_sp / 1e9, 6), "sparsify_s": round(t_sp, 3),
+                              "update_s": round(t_up, 3),
+                              "update_GBps": round(upd_bytes / t_up / 1e9, 3)}}
 
 
 def time_calls(plan_of, call, n_calls, warmup, make_events):
@@ -416,6 +547,45 @@ def other_workload(args) -> int:
              "0.001 and 0.01, global and per-tensor top-k", {"variants": res})
         return 0
 
+    if args.workload == "sweep":
+        # flat N(0, 1) vectors of 2^18 .. 2^27 elements (the 256 K .. 128 M
+        # operator range of Sec. 5.2), k = ceil(0.001 d). Gradients are eight
+        # slices of one 2^28-element buffer, residuals disjoint slices of
+        # another, zeroed for each size; call i takes gradient slice i % 8 and
+        # residual i % R, so consecutive calls on one residual see different
+        # gradients (as error feedback does), and there are enough residuals
+        # (at least 768 MiB of g and r together) that no call finds its
+        # inputs in the 256 MB last-level cache.
+        total, n_g = 1 << 28, 8
+        log("generating the 2^28-element sweep buffer")
+        G = torch.from_numpy(gen.flat_normal(total, config=6)).to(dev)
+        Rb = torch.zeros(total, device=dev)
+        rows = []
+        for e in range(18, 28):
+            d = 1 << e
+            R = max(2, min(total // d, -(-(768 << 20) // (8 * d))))
+            gstep = (total - d) // (n_g - 1) // 4096 * 4096
+            Rb.zero_()
+            plans = [tk.SparsifyPlan([d], rho=RHO).bind(
+                [G[(i % n_g) * gstep:(i % n_g) * gstep + d]],
+                [Rb[(i % R) * d:(i % R + 1) * d]]) for i in range(max(n_g, R))]
+            k = plans[0].k_total
+            io = torch.empty(k, dtype=torch.int32, device=dev)
+            vo = torch.empty(k, device=dev)
+            ms, kern = time_sparsify(tk, plans, K, W, make_events, io, vo)
+            rows.append({"d": d, "k": k, "replicas": R, "sparsify_us": round(ms * 1e3, 2),
+                         "Gelem_per_s": round(d / (ms / 1e3) / 1e9, 2),
+                         "frac_hbm_peak": round((12 * d + 8 * k) / (ms / 1e3) / 1e9
+                                                / HBM_PEAK_GBPS, 4),
+                         "kernels_us": kern})
+            log(f"sweep d=2^{e}: {rows[-1]['sparsify_us']} us")
+            del plans
+        top = rows[-1]
+        line(top["Gelem_per_s"], top["d"], top["sparsify_us"] / 1e3, top["kernels_us"],
+             "sweep: flat fp32 N(0,1) vectors, d = 2^18 .. 2^27, residual carried over rotating "
+             "gradients, global top-k rho=0.001", {"sweep": rows})
+        return 0
+
     # bert: one 340 M-element buffer with exact-duplicate magnitudes
     d = gen.BERT_LARGE_D
     log("generating the 340 M-element tie-stressed buffer")
@@ -434,6 +604,12 @@ def main() -> int:
     args = parse_args()
     if args.probe_copy:
         return probe_copy(args.probe_copy)
+    if args.probe_add:
+        return probe_add(args.probe_add)
+    if args.summarize_stats:
+        return summarize_stats(args.summarize_stats)
+    if args.summarize_pmc:
+        return summarize_pmc(*args.summarize_pmc)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the library has no multi-GPU path); "
               f"got --gpus {args.gpus}", file=sys.stderr)
@@ -547,10 +723,14 @@ def main() -> int:
         roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                    "traffic": read_traffic(dom, digest),
+                    "traffic": None,
                     "algorithmic_bytes_per_launch": bytes_per_launch,
                     "mean_launch_us": round(kern[dom] * 1e3, 2),
                     "source_digest": digest}
+        tr = read_traffic(dom, digest)
+        if tr is not None:
+            roofline["traffic"] = round(tr["bytes"])
+            roofline["traffic_raw"] = {k: v for k, v in tr.items() if k != "bytes"}
 
     out = {
         "metric": METRIC,
@@ -589,7 +769,7 @@ def main() -> int:
                                k_total, make_events)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on one step (bounded sample)")
-        out["cpu_baseline"] = cpu_baseline(sizes, d)
+        out["cpu_baseline"] = cpu_baseline(sizes, d, args.cpu_procs)
     print(json.dumps(out), flush=True)
     return 0
 
