@@ -203,7 +203,7 @@ def test_fp16_values_resnet_step(mode):
 
 
 def test_shard_sparsify_hitopk():
-    """The per-GPU share of the hierarchical scheme (Sec. 4.2): one node of
+    """The per-GPU share of the hierarchical scheme (Sec. 3.2, Alg. 2): one node of
     n = 8 GPUs splits the 25,557,032-element ResNet-50 gradient into eight
     contiguous shards; each GPU selects k~ = ceil(rho d / n) of its shard.
     Checks the first and the last (ragged) shard, fp32 and fp16 values."""

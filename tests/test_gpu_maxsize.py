@@ -8,7 +8,9 @@ selection is checked through the properties that fix it exactly at any size
 x[idx] bitwise, residual = x outside S and +0 inside, no unselected magnitude
 above a selected one, and the tie class at the threshold split toward lower
 positions. The checks run as torch operations on the device (8 GiB per
-array; a host copy would dominate the test). The update that follows is
+array; a host copy would dominate the test). x itself is the device's
+binary32 add of g and r, checked against the oracle's add on a sample of
+positions (the planted ties, both ends and 4 M drawn at random). The update that follows is
 checked bit-exactly against its definition: with at most two summands per
 position, the sum does not depend on the order of addition.
 """
@@ -18,8 +20,9 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 import paper_2010_10458_amd as tk
-from gpu_common import announce, need_gpu
+from gpu_common import announce, assert_bitwise, need_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -61,7 +64,19 @@ def _planted_input(dev):
     ties = int((xa == q).sum())
     del xa
     assert above < k < above + ties, (above, ties, k)
+    check_x_against_oracle(g, r, x, planted)
     return g, r, x, k, q, above, ties
+
+
+def check_x_against_oracle(g, r, x, planted):
+    """x = fl32(g + r) at sampled positions, by the oracle's add."""
+    rng = np.random.default_rng(77)
+    d = x.numel()
+    samp = np.unique(np.concatenate([planted, np.arange(1000), np.arange(d - 1000, d),
+                                     rng.integers(0, d, 4_000_000)]))
+    pos = torch.from_numpy(samp.astype(np.int64)).to(x.device)
+    gs, rs, xs = g[pos].cpu().numpy(), r[pos].cpu().numpy(), x[pos].cpu().numpy()
+    assert_bitwise(xs, oracle.Oracle().ef_add(gs, rs), "x = g + r (sampled)")
 
 
 @pytest.mark.parametrize("mode", [tk.GLOBAL, tk.PER_TENSOR])

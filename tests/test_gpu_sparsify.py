@@ -300,21 +300,25 @@ def test_transformer_110m_global_and_per_tensor():
         check_selection(x, idx, val, gen.concat(to_host(r)), plan.k_total)
         _sampled_ranks(x, idx, plan.k_total, rng)
         del g, r
-    announce("transformer 110M per-tensor rho=0.01")
-    g, r = to_dev(grads, dev), [torch.zeros(n, device=dev) for n in sizes]
-    plan = tk.SparsifyPlan(sizes, mode=tk.PER_TENSOR, rho=0.01)
-    plan.bind(g, r)
-    idx, val = plan.execute()
-    torch.cuda.synchronize()
-    idx, val = idx.cpu().numpy(), val.cpu().numpy()
-    rr = to_host(r)
-    ks = plan.group_k()
-    off, pos = 0, 0
-    for t, n in enumerate(sizes):
-        check_selection(x[off:off + n], idx[pos:pos + ks[t]], val[pos:pos + ks[t]], rr[t],
-                        ks[t], base=off)
-        off += n
-        pos += ks[t]
+    for rho in (0.001, 0.01):
+        announce(f"transformer 110M per-tensor rho={rho}")
+        g, r = to_dev(grads, dev), [torch.zeros(n, device=dev) for n in sizes]
+        plan = tk.SparsifyPlan(sizes, mode=tk.PER_TENSOR, rho=rho)
+        plan.bind(g, r)
+        idx, val = plan.execute()
+        torch.cuda.synchronize()
+        idx, val = idx.cpu().numpy(), val.cpu().numpy()
+        rr = to_host(r)
+        ks = plan.group_k()
+        assert ks == [tk.k_from_rho(n, rho) for n in sizes]
+        off, pos = 0, 0
+        for t, n in enumerate(sizes):
+            check_selection(x[off:off + n], idx[pos:pos + ks[t]], val[pos:pos + ks[t]], rr[t],
+                            ks[t], base=off)
+            off += n
+            pos += ks[t]
+        assert pos == idx.size
+        del g, r
 
 
 def test_bert_large_340m_tie_stressed():
