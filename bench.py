@@ -356,6 +356,20 @@ def extras(args, tk, gen, sizes, d, bank, resid, idx_all, val_all, nnz, k_total,
     ex["aggregate_kernels_us"] = kern
     del outs, aplans
 
+    log("extras: the momentum update with each position summed in worker order")
+    dw = [[t.clone() for t in bank[j % len(bank)]] for j in range(R)]   # parameters
+    db = [[torch.zeros_like(t) for t in bank[0]] for _ in range(R)]
+    dplans = [tk.UpdatePlan(sizes, P=P_WORKERS, stride=K_LIST, deterministic=True)
+              .bind(dw[j], db[j]) for j in range(R)]
+    ms, kern = time_calls(lambda i: dplans[i % R],
+                          lambda pl: pl.execute(idx_all[dplans.index(pl)],
+                                                val_all[dplans.index(pl)], lr=LR, mu=MU, wd=WD,
+                                                nnz=nnz),
+                          K, W, make_events)
+    ex["update_deterministic_us"] = round(ms * 1e3, 2)
+    ex["update_deterministic_kernels_us"] = kern
+    del dw, db, dplans
+
     log("extras: LARS (Eq. lars) step fused with the P = 128 aggregate; dense rates")
     lw = [[t.clone() for t in bank[j % len(bank)]] for j in range(R)]   # parameters
     lb = [[torch.zeros_like(t) for t in bank[0]] for _ in range(R)]     # momentum

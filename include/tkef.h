@@ -33,7 +33,7 @@
 extern "C" {
 #endif
 
-#define TKEF_VERSION 10100 /* major * 10000 + minor * 100 + patch */
+#define TKEF_VERSION 10200 /* major * 10000 + minor * 100 + patch */
 
 /* return codes */
 #define TKEF_OK 0
@@ -291,6 +291,19 @@ int tkef_aggregate_execute(tkef_update_plan plan, const int32_t *idx, const void
 /* Value format of the val arrays execute / aggregate read: TKEF_VAL_F32
  * (default) or TKEF_VAL_F16. Host only. */
 int tkef_update_plan_set_value_format(tkef_update_plan plan, int32_t format);
+
+/* Order of summation (Alg. 2 adds the gathered lists into g~ worker by
+ * worker, Sec. 3.2). on = 1: every position's entries are added in that
+ * order (workers p = 0..P-1, then list order within a worker), starting
+ * from +0, one binary32 add at a time, so G, and with it every execute,
+ * aggregate and LARS result of the plan, is bitwise reproducible and equals
+ * that sequential sum. on = 0 (default): the entries of a position are
+ * added in whatever order the device runs them (results within the
+ * documented tolerance of the sequential sum, exact with two or fewer
+ * entries per position). The ordered sum costs LDS and time (a counting
+ * sort of each chunk of entries per update tile). Host only;
+ * TKEF_EINVAL for other values. */
+int tkef_update_plan_set_deterministic(tkef_update_plan plan, int32_t on);
 
 /* Optional timing hook, as tkef_sparsify_plan_set_events. */
 int tkef_update_plan_set_events(tkef_update_plan plan, hipEvent_t *events,

@@ -98,6 +98,7 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
         "tkef_update_plan_set_events": ([vp, P(vp), i32], ctypes.c_int),
         "tkef_update_plan_launch_name": ([vp, i32], ctypes.c_char_p),
         "tkef_update_plan_set_value_format": ([vp, i32], ctypes.c_int),
+        "tkef_update_plan_set_deterministic": ([vp, i32], ctypes.c_int),
         "tkef_aggregate_execute": ([vp, vp, vp, vp, vp, sz, vp, vp], ctypes.c_int),
         "tkef_sparse_aggregate": ([P(vp), P(i64), i32, vp, vp, i32, i32, i64, vp, vp, sz, vp,
                                    vp], ctypes.c_int),
@@ -320,10 +321,12 @@ class UpdatePlan:
     """Plan for the sparse aggregate + SGD update of a fixed parameter list."""
 
     def __init__(self, numels: Sequence[int], P: int, stride: int, val_dtype=torch.float32,
-                 check: bool = False):
+                 check: bool = False, deterministic: bool = False):
         """check=True: every execute / aggregate / lars_execute without a
         caller status word uses its own, synchronizes and raises
-        TkefStatusError on any status bit."""
+        TkefStatusError on any status bit. deterministic=True: each
+        position's entries are summed in worker order, then list order
+        (bitwise reproducible; tkef_update_plan_set_deterministic)."""
         self.check = bool(check)
         self._numels = [int(n) for n in numels]
         self.P, self.stride = int(P), int(stride)
@@ -335,6 +338,9 @@ class UpdatePlan:
         self.val_dtype = val_dtype
         _check("tkef_update_plan_set_value_format",
                L.tkef_update_plan_set_value_format(self._h, _val_format(val_dtype)))
+        self.deterministic = bool(deterministic)
+        _check("tkef_update_plan_set_deterministic",
+               L.tkef_update_plan_set_deterministic(self._h, int(self.deterministic)))
         ws, d, nl = ctypes.c_size_t(), ctypes.c_int64(), ctypes.c_int32()
         _check("tkef_update_plan_info", L.tkef_update_plan_info(
             self._h, ctypes.byref(ws), ctypes.byref(d), ctypes.byref(nl)))

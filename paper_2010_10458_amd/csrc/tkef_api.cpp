@@ -735,6 +735,7 @@ struct tkef_update_plan_s {
   bool has_mom = false;
   bool has_grads = false;  // dense gradients bound (LARS rates)
   int32_t val_format = TKEF_VAL_F32;  // value arrays read by execute / aggregate
+  bool det = false;  // sums in worker order (tkef_update_plan_set_deterministic)
   hipEvent_t* events = nullptr;
   int32_t n_events = 0;
 };
@@ -919,6 +920,13 @@ extern "C" int tkef_update_plan_set_value_format(tkef_update_plan plan, int32_t 
   return TKEF_OK;
 }
 
+extern "C" int tkef_update_plan_set_deterministic(tkef_update_plan plan, int32_t on) {
+  if (!plan || (on != 0 && on != 1)) return TKEF_EINVAL;
+  if (plan->table) return TKEF_EINVAL;  // (the per-worker pointer form sums in any order)
+  plan->det = on != 0;
+  return TKEF_OK;
+}
+
 namespace {
 
 // seg + update with the given operation on the tile sums.
@@ -941,7 +949,7 @@ int update_run(tkef_update_plan plan, const int32_t* idx, const void* val, const
   if (e == hipSuccess)
     e = launch_update(tens, first, plan->ntensors, (int32_t)plan->d, plan->ntiles_u, idx, val,
                       val16, plan->stride, nnz, plan->P, seg, lr, mu, wd, op, has_mom,
-                      LarsArgs{nullptr, nullptr, nullptr, 0.0f}, s, tr.at(1));
+                      LarsArgs{nullptr, nullptr, nullptr, 0.0f}, plan->det, s, tr.at(1));
   return hip_rc(e);
 }
 
@@ -995,13 +1003,13 @@ extern "C" int tkef_lars_update_execute(tkef_update_plan plan, const int32_t* id
   if (e == hipSuccess)
     e = launch_update(tens, first, T, d, plan->ntiles_u, idx, val, val16, plan->stride, nnz,
                       plan->P, seg, 0.0f, 0.0f, 0.0f, kOpLarsNorm, 0,
-                      LarsArgs{part, tpair, nullptr, eps32}, s, tr.at(1));
+                      LarsArgs{part, tpair, nullptr, eps32}, plan->det, s, tr.at(1));
   if (e == hipSuccess)
     e = launch_lars_rates(tpair, part, T, gamma, eta, eps, rate, rate_out, s, tr.at(2));
   if (e == hipSuccess)
     e = launch_update(tens, first, T, d, plan->ntiles_u, idx, val, val16, plan->stride, nnz,
                       plan->P, seg, 0.0f, mu, 0.0f, kOpLarsApply, has_mom,
-                      LarsArgs{part, tpair, rate, eps32}, s, tr.at(3));
+                      LarsArgs{part, tpair, rate, eps32}, plan->det, s, tr.at(3));
   return hip_rc(e);
 }
 

@@ -221,7 +221,7 @@ hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32
                          int32_t d, int32_t ntiles_u, const int32_t* idx, const void* val,
                          int val16, int64_t stride, const int32_t* nnz, int32_t P,
                          const int32_t* seg, float lr, float mu, float wd, int op, int has_mom,
-                         const LarsArgs& lars, hipStream_t s, const Ev& ev);
+                         const LarsArgs& lars, bool det, hipStream_t s, const Ev& ev);
 // the same two steps over P per-worker lists (table in device memory; max_n:
 // the longest list)
 hipError_t launch_seg_table(const WorkerList* lists, int32_t P, int64_t max_n, int32_t d,

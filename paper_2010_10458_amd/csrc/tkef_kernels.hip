@@ -1709,10 +1709,107 @@ constexpr int kXcds = 8;                      // MI355X: 8 accelerator dies
 constexpr int kXcdRun = 16;                   // consecutive update tiles one die takes
 constexpr int kUVecPerThread = kUTile / 4 / kUBlock;  // float4 per thread per tile
 
+constexpr int kPairUnroll = 4;  // list entries per thread and chunk of the accumulation
+constexpr int kUOwn = kUTile / kUBlock;  // tile positions one thread owns in the ordered sum
+
+// The ordered accumulation of one chunk of list entries (deterministic mode).
+// Entry j * kUBlock + tid of the chunk (li[j], vv[j]; li outside [0, len)
+// for none) is the chunk's entry number j * kUBlock + tid, and the entries
+// are numbered in worker order, then list order, as Alg. 2 visits them.
+// Each position's entries are added to acc in that order, one binary32 add
+// at a time, so the sums do not depend on the order in which threads run:
+//   1. LDS counters (two 16-bit counts per word) count every position's
+//      entries; each entry keeps its arrival rank at its position;
+//   2. thread t owns positions [t * kUOwn, (t + 1) * kUOwn): an exclusive
+//      scan of the counts gives every position's first slot;
+//   3. each entry goes to slot first + rank of (dq: entry number, dv: value);
+//   4. each owner sorts its positions' slots by entry number (insertion
+//      sort; a position usually has one entry) and adds them in that order.
+// dcnt: kUTile / 2 words, zero on entry and on return; dq, dv: kUBlock *
+// kPairUnroll slots; dws: kUBlock / 64 words. Uniform in the workgroup.
+__device__ __forceinline__ void det_accumulate(const int32_t (&li)[kPairUnroll],
+                                               const float (&vv)[kPairUnroll], int32_t len,
+                                               bool sparse_mode, float* acc, uint32_t* mask,
+                                               uint32_t* dcnt, uint16_t* dq, float* dv,
+                                               uint32_t* dws) {
+  static_assert(kUBlock * kPairUnroll <= 65535, "slots and entry numbers fit 16 bits");
+  static_assert(kUOwn % 2 == 0, "two counts per word");
+  const int tid = threadIdx.x;
+  uint32_t rank[kPairUnroll];
+#pragma unroll
+  for (int j = 0; j < kPairUnroll; ++j) {
+    rank[j] = 0u;
+    if (li[j] >= 0 && li[j] < len) {
+      const uint32_t sh = 16u * (uint32_t)(li[j] & 1);
+      rank[j] = (atomicAdd(&dcnt[li[j] >> 1], 1u << sh) >> sh) & 0xFFFFu;
+    }
+  }
+  __syncthreads();
+  uint32_t cw[kUOwn / 2];  // this thread's counts, two per word
+  uint32_t mine = 0u;
+#pragma unroll
+  for (int i = 0; i < kUOwn / 2; ++i) {
+    cw[i] = dcnt[tid * (kUOwn / 2) + i];
+    mine += (cw[i] & 0xFFFFu) + (cw[i] >> 16);
+  }
+  uint32_t total;
+  const uint32_t first = block_scan<kUBlock>(mine, dws, &total);  // (ends with a barrier)
+  uint32_t o = first;
+#pragma unroll
+  for (int i = 0; i < kUOwn / 2; ++i) {
+    const uint32_t c0 = cw[i] & 0xFFFFu, c1 = cw[i] >> 16;
+    dcnt[tid * (kUOwn / 2) + i] = o | ((o + c0) << 16);  // first slots
+    o += c0 + c1;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kPairUnroll; ++j) {
+    if (li[j] >= 0 && li[j] < len) {
+      const uint32_t sh = 16u * (uint32_t)(li[j] & 1);
+      const uint32_t slot = ((dcnt[li[j] >> 1] >> sh) & 0xFFFFu) + rank[j];
+      dq[slot] = (uint16_t)(j * kUBlock + tid);
+      dv[slot] = vv[j];
+    }
+  }
+  __syncthreads();
+  o = first;
+#pragma unroll 1
+  for (int i = 0; i < kUOwn; ++i) {
+    const uint32_t c = (i & 1) ? (cw[i >> 1] >> 16) : (cw[i >> 1] & 0xFFFFu);
+    if (c == 0u) continue;
+    const uint32_t e = o + c;
+#pragma unroll 1
+    for (uint32_t a = o + 1; a < e; ++a) {
+      const uint16_t kq = dq[a];
+      const float kv = dv[a];
+      uint32_t b = a;
+      while (b > o && dq[b - 1] > kq) {
+        dq[b] = dq[b - 1];
+        dv[b] = dv[b - 1];
+        --b;
+      }
+      dq[b] = kq;
+      dv[b] = kv;
+    }
+    const int pos = tid * kUOwn + i;
+    float sum = acc[pos];
+#pragma unroll 1
+    for (uint32_t a = o; a < e; ++a) sum = sum + dv[a];
+    acc[pos] = sum;
+    if (sparse_mode) atomicOr(&mask[pos >> 5], 1u << (pos & 31));
+    o = e;
+  }
+#pragma unroll
+  for (int i = 0; i < kUOwn / 2; ++i) dcnt[tid * (kUOwn / 2) + i] = 0u;
+  __syncthreads();
+}
+
 // kLars: the LARS norm and step passes (a separate instantiation, so the SGD
 // and aggregation passes keep their register budget).
 // kTable: the lists come as a table of per-worker pointers (binary32 values).
-template <bool kLars, bool kTable>
+// kDet: each position's entries are added in worker order (det_accumulate)
+// instead of by LDS float atomics in any order.
+template <bool kLars, bool kTable, bool kDet>
 __global__ __launch_bounds__(kUBlock) void k_update(
     const UpdTensor* __restrict__ tens, const int32_t* __restrict__ tile_first, int32_t ntens,
     int32_t d, int32_t ntiles_u, ListsArg lists, int val16, int32_t P,
@@ -1735,6 +1832,11 @@ __global__ __launch_bounds__(kUBlock) void k_update(
   // per-worker form: the list pointers of the current batch of workers
   __shared__ const int32_t* s_ip[kTable ? kUBlock : 1];
   __shared__ const float* s_vp[kTable ? kUBlock : 1];
+  // deterministic mode: counters, slots and scan words of det_accumulate
+  __shared__ uint32_t dcnt[kDet ? kUTile / 2 : 1];
+  __shared__ uint16_t dq[kDet ? kUBlock * kPairUnroll : 1];
+  __shared__ float dv[kDet ? kUBlock * kPairUnroll : 1];
+  __shared__ uint32_t dws[kDet ? kUBlock / 64 : 1];
   const int tid = threadIdx.x;
   // Workgroups go round-robin to the XCDs; give each XCD runs of kXcdRun
   // consecutive tiles, so that neighbouring tiles, which share the cache
@@ -1776,6 +1878,8 @@ __global__ __launch_bounds__(kUBlock) void k_update(
   for (int i = tid; i < kUTile; i += kUBlock) acc[i] = 0.0f;
   if (sparse_mode)
     for (int i = tid; i < kUTile / 32; i += kUBlock) mask[i] = 0u;
+  if constexpr (kDet)
+    for (int i = tid; i < kUTile / 2; i += kUBlock) dcnt[i] = 0u;
   __syncthreads();
 
   // 1. accumulate every worker's entries that fall in this tile
@@ -1808,7 +1912,6 @@ __global__ __launch_bounds__(kUBlock) void k_update(
     __syncthreads();
     // entries of this batch of workers, kPairUnroll per thread with all
     // their loads in flight before the LDS adds
-    constexpr int kPairUnroll = 4;
     for (uint32_t q0 = 0; q0 < total; q0 += kUBlock * kPairUnroll) {
       int32_t li[kPairUnroll];
       float vv[kPairUnroll];
@@ -1835,11 +1938,15 @@ __global__ __launch_bounds__(kUBlock) void k_update(
           }
         }
       }
+      if constexpr (kDet) {
+        det_accumulate(li, vv, len, sparse_mode, acc, mask, dcnt, dq, dv, dws);
+      } else {
 #pragma unroll
-      for (int j = 0; j < kPairUnroll; ++j) {
-        if (li[j] >= 0 && li[j] < len) {
-          atomicAdd(&acc[li[j]], vv[j]);
-          if (sparse_mode) atomicOr(&mask[li[j] >> 5], 1u << (li[j] & 31));
+        for (int j = 0; j < kPairUnroll; ++j) {
+          if (li[j] >= 0 && li[j] < len) {
+            atomicAdd(&acc[li[j]], vv[j]);
+            if (sparse_mode) atomicOr(&mask[li[j] >> 5], 1u << (li[j] & 31));
+          }
         }
       }
     }
@@ -2948,10 +3055,12 @@ hipError_t launch_update(const UpdTensor* tens, const int32_t* tile_first, int32
                          int32_t d, int32_t ntiles_u, const int32_t* idx, const void* val,
                          int val16, int64_t stride, const int32_t* nnz, int32_t P,
                          const int32_t* seg, float lr, float mu, float wd, int op, int has_mom,
-                         const LarsArgs& lars, hipStream_t s, const Ev& ev) {
+                         const LarsArgs& lars, bool det, hipStream_t s, const Ev& ev) {
   const bool is_lars = op == kOpLarsNorm || op == kOpLarsApply;
   const ListsArg lists{idx, val, stride, nnz, nullptr};
-  return launch(is_lars ? k_update<true, false> : k_update<false, false>,
+  auto* kern = is_lars ? (det ? k_update<true, false, true> : k_update<true, false, false>)
+                       : (det ? k_update<false, false, true> : k_update<false, false, false>);
+  return launch(kern,
                 dim3(update_grid(ntiles_u)), dim3(kUBlock), s, ev, tens, tile_first, ntens, d,
                 ntiles_u, lists, val16, P, seg, lr, mu, wd, op, has_mom, lars);
 }
@@ -2961,7 +3070,7 @@ hipError_t launch_update_table(const UpdTensor* tens, const int32_t* tile_first,
                                const int32_t* seg, float lr, float mu, float wd, int op,
                                int has_mom, hipStream_t s, const Ev& ev) {
   const ListsArg lists{nullptr, nullptr, 0, nullptr, table};
-  return launch(k_update<false, true>, dim3(update_grid(ntiles_u)), dim3(kUBlock), s, ev, tens,
+  return launch(k_update<false, true, false>, dim3(update_grid(ntiles_u)), dim3(kUBlock), s, ev, tens,
                 tile_first, ntens, d, ntiles_u, lists, 0, P, seg, lr, mu, wd, op, has_mom,
                 LarsArgs{nullptr, nullptr, nullptr, 0.0f});
 }

@@ -29,7 +29,7 @@ def test_header_symbols_exported():
 
 def test_version_and_strerror():
     L = tk.lib()
-    assert L.tkef_version() == 10100
+    assert L.tkef_version() == 10200
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert L.tkef_strerror(code)
     assert b"unknown" in L.tkef_strerror(-99)
@@ -146,6 +146,11 @@ def test_update_plan_validation():
     assert L.tkef_update_plan_bind(u._h, w, None, P(0x10001), 10**9, None) == tk.EWORKSPACE
     assert L.tkef_update_execute(u._h, P(0x10), P(0x20), None, 0.1, 0.0, 0.0, P(0x10000),
                                  10**9, None, None) == tk.ESTATE
+    assert L.tkef_update_plan_set_deterministic(u._h, 1) == tk.OK
+    assert L.tkef_update_plan_set_deterministic(u._h, 0) == tk.OK
+    assert L.tkef_update_plan_set_deterministic(u._h, 2) == tk.EINVAL
+    assert L.tkef_update_plan_set_deterministic(None, 1) == tk.EINVAL
+    assert tk.UpdatePlan([10, 20], P=3, stride=4, deterministic=True).deterministic
 
 
 def test_no_cpu_fallback_when_library_missing(tmp_path, monkeypatch):
