@@ -185,9 +185,9 @@ def test_repeated_execution_is_deterministic():
     rng = np.random.default_rng(500)
     n = 300_007
     g = (np.round(rng.standard_normal(n) * 16) / 16).astype(np.float32)
-    announce("sparsify repeat x20")
+    announce("sparsify repeat x100")
     out = None
-    for it in range(20):
+    for it in range(100):
         gt = to_dev([g], dev)
         rt = to_dev([np.zeros(n, np.float32)], dev)
         plan = tk.SparsifyPlan([n], rho=0.01)
