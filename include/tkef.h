@@ -247,7 +247,9 @@ int tkef_sparsify1_static(const float *g, float *r, int64_t d, int64_t k, int32_
  *       w_i -= lr * U
  * Each step is a binary32 operation with round-to-nearest (no fused
  * multiply-add). G is accumulated in binary32; where three or more workers
- * name one position, the order of its additions is unspecified.
+ * name one position, the order of its additions is unspecified, unless the
+ * plan is set deterministic (tkef_update_plan_set_deterministic: worker
+ * order, then list order).
  * ====================================================================== */
 
 typedef struct tkef_update_plan_s *tkef_update_plan;

@@ -87,6 +87,9 @@ extern "C" int64_t tkef_k_from_rho(int64_t d, double rho) {
   if (d < 0 || !(rho > 0.0 && rho <= 1.0) || !std::isfinite(rho)) return TKEF_ERANGE;
   if (d == 0) return 0;
   const double kd = std::ceil(rho * static_cast<double>(d));
+  // clamped in double first: rho * d can round up to 2^63, which int64_t
+  // cannot hold
+  if (kd >= static_cast<double>(d)) return d;
   int64_t k = static_cast<int64_t>(kd);
   if (k < 1) k = 1;
   if (k > d) k = d;
@@ -1037,8 +1040,9 @@ extern "C" int tkef_lars_rates_execute(tkef_update_plan plan, double gamma, doub
 }
 
 extern "C" const char* tkef_lars_launch_name(int32_t dense, int32_t i) {
-  if (dense) return (i >= 0 && i < 2) ? kLarsDenseLaunches[i] : nullptr;
-  return (i >= 0 && i < 4) ? kLarsLaunches[i] : nullptr;
+  if (dense == 1) return (i >= 0 && i < 2) ? kLarsDenseLaunches[i] : nullptr;
+  if (dense == 0) return (i >= 0 && i < 4) ? kLarsLaunches[i] : nullptr;
+  return nullptr;
 }
 
 extern "C" int tkef_update_workspace(const int64_t* numels, int32_t ntensors, int32_t P,
