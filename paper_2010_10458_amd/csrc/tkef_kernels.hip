@@ -1718,10 +1718,13 @@ constexpr int kUOwn = kUTile / kUBlock;  // tile positions one thread owns in th
 // are numbered in worker order, then list order, as Alg. 2 visits them.
 // Each position's entries are added to acc in that order, one binary32 add
 // at a time, so the sums do not depend on the order in which threads run:
-//   1. LDS counters (two 16-bit counts per word) count every position's
-//      entries; each entry keeps its arrival rank at its position;
-//   2. thread t owns positions [t * kUOwn, (t + 1) * kUOwn): an exclusive
-//      scan of the counts gives every position's first slot;
+//   1. LDS counters count every position's entries (word w holds the 16-bit
+//      counts of positions w and w + kUTile / 2); each entry keeps its
+//      arrival rank at its position;
+//   2. thread t owns the words t, t + kUBlock, ... (so a wavefront's LDS
+//      accesses fall in distinct banks) and with them kUOwn positions: an
+//      exclusive scan of the counts gives every position a first slot (the
+//      positions' slot ranges are disjoint; their order does not matter);
 //   3. each entry goes to slot first + rank of (dq: entry number, dv: value);
 //   4. each owner sorts its positions' slots by entry number (insertion
 //      sort; a position usually has one entry) and adds them in that order.
@@ -1734,39 +1737,41 @@ __device__ __forceinline__ void det_accumulate(const int32_t (&li)[kPairUnroll],
                                                uint32_t* dws) {
   static_assert(kUBlock * kPairUnroll <= 65535, "slots and entry numbers fit 16 bits");
   static_assert(kUOwn % 2 == 0, "two counts per word");
+  constexpr int kHalf = kUTile / 2;  // position p: word p % kHalf, half p / kHalf
+  constexpr int kWords = kUOwn / 2;  // words per thread
   const int tid = threadIdx.x;
   uint32_t rank[kPairUnroll];
 #pragma unroll
   for (int j = 0; j < kPairUnroll; ++j) {
     rank[j] = 0u;
     if (li[j] >= 0 && li[j] < len) {
-      const uint32_t sh = 16u * (uint32_t)(li[j] & 1);
-      rank[j] = (atomicAdd(&dcnt[li[j] >> 1], 1u << sh) >> sh) & 0xFFFFu;
+      const uint32_t sh = li[j] >= kHalf ? 16u : 0u;
+      rank[j] = (atomicAdd(&dcnt[li[j] & (kHalf - 1)], 1u << sh) >> sh) & 0xFFFFu;
     }
   }
   __syncthreads();
-  uint32_t cw[kUOwn / 2];  // this thread's counts, two per word
+  uint32_t cw[kWords];  // this thread's counts, two per word
   uint32_t mine = 0u;
 #pragma unroll
-  for (int i = 0; i < kUOwn / 2; ++i) {
-    cw[i] = dcnt[tid * (kUOwn / 2) + i];
+  for (int i = 0; i < kWords; ++i) {
+    cw[i] = dcnt[tid + i * kUBlock];
     mine += (cw[i] & 0xFFFFu) + (cw[i] >> 16);
   }
   uint32_t total;
   const uint32_t first = block_scan<kUBlock>(mine, dws, &total);  // (ends with a barrier)
   uint32_t o = first;
 #pragma unroll
-  for (int i = 0; i < kUOwn / 2; ++i) {
+  for (int i = 0; i < kWords; ++i) {
     const uint32_t c0 = cw[i] & 0xFFFFu, c1 = cw[i] >> 16;
-    dcnt[tid * (kUOwn / 2) + i] = o | ((o + c0) << 16);  // first slots
+    dcnt[tid + i * kUBlock] = o | ((o + c0) << 16);  // first slots
     o += c0 + c1;
   }
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < kPairUnroll; ++j) {
     if (li[j] >= 0 && li[j] < len) {
-      const uint32_t sh = 16u * (uint32_t)(li[j] & 1);
-      const uint32_t slot = ((dcnt[li[j] >> 1] >> sh) & 0xFFFFu) + rank[j];
+      const uint32_t sh = li[j] >= kHalf ? 16u : 0u;
+      const uint32_t slot = ((dcnt[li[j] & (kHalf - 1)] >> sh) & 0xFFFFu) + rank[j];
       dq[slot] = (uint16_t)(j * kUBlock + tid);
       dv[slot] = vv[j];
     }
@@ -1791,7 +1796,7 @@ __device__ __forceinline__ void det_accumulate(const int32_t (&li)[kPairUnroll],
       dq[b] = kq;
       dv[b] = kv;
     }
-    const int pos = tid * kUOwn + i;
+    const int pos = tid + (i >> 1) * kUBlock + (i & 1) * kHalf;
     float sum = acc[pos];
 #pragma unroll 1
     for (uint32_t a = o; a < e; ++a) sum = sum + dv[a];
@@ -1800,7 +1805,7 @@ __device__ __forceinline__ void det_accumulate(const int32_t (&li)[kPairUnroll],
     o = e;
   }
 #pragma unroll
-  for (int i = 0; i < kUOwn / 2; ++i) dcnt[tid * (kUOwn / 2) + i] = 0u;
+  for (int i = 0; i < kWords; ++i) dcnt[tid + i * kUBlock] = 0u;
   __syncthreads();
 }
 
