@@ -142,10 +142,14 @@ struct tkef_sparsify_plan_s {
   int32_t sel_lpt = 1, sel_grid = 1, sel_block = 1;  // selection kernels: lines per thread,
                                                     // workgroups, threads per workgroup
   // Scratch that must start at zero (histograms, prefix flags, overflow and
-  // count words) exists twice; execution n uses copy n % 2 and its last kernel
-  // clears the other copy for execution n + 1. Offsets below are relative to
-  // the start of a copy, which lies at off_zero[0] or off_zero[1].
-  size_t off_tiles = 0, off_groups = 0, off_state = 0, off_zero[2] = {0, 0}, zero_bytes = 0,
+  // count words), at off_zero; offsets below are relative to it. It is laid
+  // out so that what the execution's last kernel uses comes last, from
+  // zero_tail on: the first kernel (the stream) clears that part, which it
+  // does not use, and the last kernel clears the part before zero_tail,
+  // which only earlier kernels use. Every execution thus launches the same
+  // kernels with the same arguments (a captured execution can be replayed).
+  size_t off_tiles = 0, off_groups = 0, off_state = 0, off_zero = 0, zero_bytes = 0,
+         zero_tail = 0,
          off_hist1 = 0, off_hist2 = 0, off_hist3 = 0, off_flags1 = 0, off_flags2 = 0,
          off_meta = 0, off_summ = 0, off_base = 0, off_cand = 0, off_rcand = 0, off_rband = 0,
          off_rsuf = 0, off_rcnt = 0, off_rbin = 0, off_rbtmp = 0, off_ticket = 0, off_rzr = 0,
@@ -156,8 +160,7 @@ struct tkef_sparsify_plan_s {
   uint64_t ms_word = 0;
   size_t off_ms_state = 0, off_ms_esum = 0, off_ms_emax = 0, off_ms_cnt = 0,
          off_ms_flags = 0;  // state: kMsMaxPasses + 1 records, zeroed scratch: the rest
-  uint64_t executions = 0;   // since the last bind
-  bool needs_clear = true;   // both copies must be cleared before the next run
+  bool needs_clear = true;   // the zeroed scratch must be cleared before the next run
   int32_t ms_passes() const { return ms_passes_for(ms_rounds); }
   int32_t nlaunch() const {
     if (mode == TKEF_APPROX) return 2 + ms_passes();
@@ -240,8 +243,11 @@ bool sparsify_layout(tkef_sparsify_plan_s* p) {
     p->off_meta = z;    z = align_up(z + 8);
   }
   p->zero_bytes = z;
-  p->off_zero[0] = o; o = align_up(o + z);
-  p->off_zero[1] = o; o = align_up(o + z);
+  // the last kernel's part: finish uses hist2 and its ticket; emit the second
+  // prefix flags and meta; MSTopK's emit the last pass's counts and its flags
+  // (that start depends on the rounds: see zero_split)
+  p->zero_tail = approx ? p->off_ms_cnt : (one ? p->off_hist2 : p->off_flags2);
+  p->off_zero = o;    o = align_up(o + z);
   p->off_summ = o;    o = align_up(o + (size_t)p->nlines * sizeof(uint16_t));
   if (approx) {
     // no candidate tables: the passes read the lines again
@@ -363,12 +369,13 @@ namespace {
 
 // The exact selection of one group: stream, collect, finish. The workspace at
 // base is laid out by sparsify_layout, its tables are written and the zeroed
-// scratch copy starts at zb; finish clears clear_words words at clear_next
-// for the next execution.
+// scratch starts at zb. The stream clears stream_words words at
+// stream_clear, finish clear_words words at clear_next (the two parts of the
+// zeroed scratch; none for a caller that clears it all beforehand).
 hipError_t run_one_group(const tkef_sparsify_plan_s* p, char* base, char* zb,
-                         uint32_t* clear_next, int64_t clear_words, int32_t* idx_out,
-                         void* val_out, int val16, uint32_t* status, hipStream_t s,
-                         const Tracer& tr) {
+                         uint32_t* stream_clear, int64_t stream_words, uint32_t* clear_next,
+                         int64_t clear_words, int32_t* idx_out, void* val_out, int val16,
+                         uint32_t* status, hipStream_t s, const Tracer& tr) {
   const TileDesc* tiles = reinterpret_cast<const TileDesc*>(base + p->off_tiles);
   const GroupDesc* groups = reinterpret_cast<const GroupDesc*>(base + p->off_groups);
   GroupState* st = reinterpret_cast<GroupState*>(base + p->off_state);
@@ -384,7 +391,7 @@ hipError_t run_one_group(const tkef_sparsify_plan_s* p, char* base, char* zb,
   const int64_t nl = p->nlines;
   const int lpt = p->sel_lpt, sg = p->sel_grid;
   hipError_t e = launch_stream(tiles, p->ntiles, p->stream_grid, hist1, p->nslots, summ, status,
-                               s, tr.at(0));
+                               stream_clear, stream_words, s, tr.at(0));
   if (e == hipSuccess)
     e = launch_collect(tiles, groups, st, hist1, p->nslots, summ, nl, lpt, sg, p->sel_block,
                        p->rcap, hist2, rbin, rcand, rband, rbtmp, rsuf, rcnt, s, tr.at(1));
@@ -442,11 +449,10 @@ extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* con
   if (e == hipSuccess)
     e = hipMemcpyAsync(base + plan->off_groups, plan->groups.data(),
                        plan->groups.size() * sizeof(GroupDesc), hipMemcpyHostToDevice, stream);
-  // both copies of the zero-initialised scratch start cleared
+  // the zero-initialised scratch starts cleared
   if (e == hipSuccess)
-    e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_zero[0]), 0u,
-                        (int64_t)((plan->off_zero[1] + plan->zero_bytes - plan->off_zero[0]) / 4),
-                        stream);
+    e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_zero), 0u,
+                        (int64_t)(plan->zero_bytes / 4), stream);
   // line summaries start at 0: the stream rewrites those of lines holding
   // elements on every run and never writes the others
   if (e == hipSuccess)
@@ -458,7 +464,6 @@ extern "C" int tkef_sparsify_plan_bind(tkef_sparsify_plan plan, const float* con
     return TKEF_EHIP;
   }
   plan->bound_ws = ws;
-  plan->executions = 0;
   plan->needs_clear = false;
   return TKEF_OK;
 }
@@ -536,9 +541,7 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   const TileDesc* tiles = reinterpret_cast<const TileDesc*>(base + plan->off_tiles);
   const GroupDesc* groups = reinterpret_cast<const GroupDesc*>(base + plan->off_groups);
   GroupState* st = reinterpret_cast<GroupState*>(base + plan->off_state);
-  const int par = (int)(plan->executions & 1u);
-  char* zb = base + plan->off_zero[par];           // this execution's cleared scratch
-  char* zn = base + plan->off_zero[par ^ 1];       // cleared for the next execution
+  char* zb = base + plan->off_zero;  // the zeroed scratch
   uint32_t* hist1 = reinterpret_cast<uint32_t*>(zb + plan->off_hist1);
   uint32_t* hist2 = reinterpret_cast<uint32_t*>(zb + plan->off_hist2);
   uint16_t* summ = reinterpret_cast<uint16_t*>(base + plan->off_summ);
@@ -548,14 +551,21 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
   const Tracer tr{plan->events, plan->n_events};
   const int val16 = plan->val_format == TKEF_VAL_F16 ? 1 : 0;
   int li = 0;  // launch index, for the timing hook
-  uint32_t* clear_next = reinterpret_cast<uint32_t*>(zn);
-  const int64_t clear_words = (int64_t)(plan->zero_bytes / 4);
+  // the last kernel clears [0, tail) of the zeroed scratch, the stream
+  // [tail, zero_bytes)
+  size_t tail = plan->zero_tail;
+  if (plan->mode == TKEF_APPROX) {
+    const int32_t last = plan->ms_passes() - 1;  // the emit kernel reads pass last's counts
+    tail += (last == 0 ? 0 : ((size_t)kMsSlots * 64 + (size_t)(last - 1) * kMsRefineBins)) * 4;
+  }
+  uint32_t* clear_next = reinterpret_cast<uint32_t*>(zb);
+  const int64_t clear_words = (int64_t)(tail / 4);
+  uint32_t* stream_clear = reinterpret_cast<uint32_t*>(zb + tail);
+  const int64_t stream_words = (int64_t)((plan->zero_bytes - tail) / 4);
 
   hipError_t e = hipSuccess;
   if (plan->needs_clear) {  // after a failed run
-    e = launch_fill_u32(reinterpret_cast<uint32_t*>(base + plan->off_zero[0]), 0u,
-                        (int64_t)((plan->off_zero[1] + plan->zero_bytes - plan->off_zero[0]) / 4),
-                        s);
+    e = launch_fill_u32(reinterpret_cast<uint32_t*>(zb), 0u, (int64_t)(plan->zero_bytes / 4), s);
     if (e != hipSuccess) return TKEF_EHIP;
     plan->needs_clear = false;
   }
@@ -577,8 +587,8 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     };
     auto slots_of = [&](int32_t b) { return b == 0 ? kMsSlots : 1; };
     auto bins_of = [&](int32_t b) { return b == 0 ? 64 : kMsRefineBins; };
-    e = launch_ms_stream(tiles, nt, plan->stream_grid, kMsSlots, esum, emax, summ, s,
-                         tr.at(li++));
+    e = launch_ms_stream(tiles, nt, plan->stream_grid, kMsSlots, esum, emax, summ, stream_clear,
+                         stream_words, s, tr.at(li++));
     if (e == hipSuccess)
       e = launch_ms_count(tiles, nt, plan->count_grid, kMsSlots, esum, emax, summ, cnt_of(0),
                           ms, plan->d, status, s, tr.at(li++));
@@ -596,15 +606,14 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
       plan->needs_clear = true;
       return TKEF_EHIP;
     }
-    plan->executions++;
     return TKEF_OK;
   }
   if (ng == 1) {
-    e = run_one_group(plan, base, zb, clear_next, clear_words, idx_out, val_out, val16, status,
-                      s, tr);
+    e = run_one_group(plan, base, zb, stream_clear, stream_words, clear_next, clear_words,
+                      idx_out, val_out, val16, status, s, tr);
   } else {
-    e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status, s,
-                      tr.at(li++));
+    e = launch_stream(tiles, nt, plan->stream_grid, hist1, plan->nslots, summ, status,
+                      stream_clear, stream_words, s, tr.at(li++));
     uint32_t* hist3 = reinterpret_cast<uint32_t*>(zb + plan->off_hist3);
     uint64_t* flags1 = reinterpret_cast<uint64_t*>(zb + plan->off_flags1);
     uint64_t* flags2 = reinterpret_cast<uint64_t*>(zb + plan->off_flags2);
@@ -632,7 +641,6 @@ extern "C" int tkef_sparsify_execute(tkef_sparsify_plan plan, void* ws, size_t w
     plan->needs_clear = true;
     return TKEF_EHIP;
   }
-  plan->executions++;
   return hip_rc(e);
 }
 
@@ -701,7 +709,7 @@ extern "C" int tkef_sparsify1_static(const float* g, float* r, int64_t d, int64_
   // the array keeps the previous call's contents: the set-up kernel writes
   // the tables, clears the histograms and the last tile's line summaries
   // (the stream rewrites the summaries of every line that holds elements)
-  char* zb = base + p.off_zero[0];
+  char* zb = base + p.off_zero;
   uint16_t* summ = reinterpret_cast<uint16_t*>(base + p.off_summ);
   e = launch_setup_one(reinterpret_cast<TileDesc*>(base + p.off_tiles),
                        reinterpret_cast<GroupDesc*>(base + p.off_groups), g, r, d, k, p.ntiles,
@@ -709,8 +717,8 @@ extern "C" int tkef_sparsify1_static(const float* g, float* r, int64_t d, int64_
                        reinterpret_cast<uint32_t*>(summ + (int64_t)(p.ntiles - 1) * kLinesPerTile),
                        kLinesPerTile / 2, stream);
   if (e == hipSuccess)
-    e = run_one_group(&p, base, zb, nullptr, 0, idx_out, val_out, 0, status, stream,
-                      Tracer{nullptr, 0});
+    e = run_one_group(&p, base, zb, nullptr, 0, nullptr, 0, idx_out, val_out, 0, status,
+                      stream, Tracer{nullptr, 0});
   return hip_rc(e);
 }
 

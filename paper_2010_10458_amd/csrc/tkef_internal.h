@@ -146,8 +146,11 @@ struct Ev {
 };
 // Each returns the hipError_t of its launch.
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
+// clear / clear_words: scratch the stream zeroes for the later kernels of the
+// execution (it does not use it itself)
 hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, uint32_t* hist1,
-                         int32_t nslots, uint16_t* summ, uint32_t* status, hipStream_t s, const Ev& ev);
+                         int32_t nslots, uint16_t* summ, uint32_t* status, uint32_t* clear,
+                         int64_t clear_words, hipStream_t s, const Ev& ev);
 hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
                        const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s, const Ev& ev);
 // one selection group
@@ -186,7 +189,8 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
 // MSTopK (one group, TKEF_APPROX). st[b] = state before pass b (written by
 // pass b's kernel), st[passes] = the final state (written by emit).
 hipError_t launch_ms_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,
-                            uint64_t* esum, uint32_t* emax, uint16_t* summ, hipStream_t s,
+                            uint64_t* esum, uint32_t* emax, uint16_t* summ, uint32_t* clear,
+                            int64_t clear_words, hipStream_t s,
                             const Ev& ev);
 hipError_t launch_ms_count(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,
                            const uint64_t* esum, const uint32_t* emax, const uint16_t* summ,

@@ -267,13 +267,20 @@ __device__ __forceinline__ void flush_hist(uint32_t* h, uint32_t* __restrict__ d
   __syncthreads();
 }
 
+// clear: clear_words words of the scratch that only later kernels of the
+// execution use (zeroed here for them; nothing in this kernel reads them).
 __global__ __launch_bounds__(kBlock) void k_stream(const TileDesc* __restrict__ tiles,
                                                    int32_t ntiles, uint32_t* __restrict__ hist1,
                                                    int nslots, uint16_t* __restrict__ summ,
-                                                   uint32_t* __restrict__ status) {
+                                                   uint32_t* __restrict__ status,
+                                                   uint32_t* __restrict__ clear,
+                                                   int64_t clear_words) {
   __shared__ uint32_t h[kH1Bins];
   __shared__ uint32_t nanflag;
   const int tid = threadIdx.x;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + tid; i < clear_words;
+       i += (int64_t)gridDim.x * kBlock)
+    clear[i] = 0u;
   for (int i = tid; i < kH1Bins; i += kBlock) h[i] = 0u;
   if (tid == 0) nanflag = 0u;
   __syncthreads();
@@ -1202,7 +1209,8 @@ __global__ __launch_bounds__(NT) void k_finish(
   const uint32_t sv[4] = {gt, eq, gtb, eqb};
   uint32_t pre[4], tot[4];
   block_scan4<NT>(sv, wsum, pre, tot);
-  // clear the other copy of the zero-initialised scratch for the next run
+  // clear the part of the zero-initialised scratch that only the earlier
+  // kernels of this execution use (not read here), for the next execution
   // (after the last barrier, which would wait for these stores)
 #pragma unroll 1
   for (int64_t i = (int64_t)w * NT + tid; i < clear_words; i += (int64_t)G * NT)
@@ -1484,7 +1492,8 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
     fgt = (kg > sg.need) ? kg - sg.need : 0u;
     feq = sg.need ? sg.n_eq : 0u;
   }
-  // clear the other copy of the zero-initialised scratch for the next run
+  // clear the part of the zero-initialised scratch that only the earlier
+  // kernels of this execution use (not read here), for the next execution
 #pragma unroll 1
   for (int64_t i = (int64_t)blockIdx.x * kSBlock + tid; i < clear_words;
        i += (int64_t)gridDim.x * kSBlock)
@@ -2490,11 +2499,16 @@ __global__ __launch_bounds__(kBlock) void k_ms_stream(const TileDesc* __restrict
                                                       int32_t ntiles, int nslots,
                                                       unsigned long long* __restrict__ esum,
                                                       uint32_t* __restrict__ emax,
-                                                      uint16_t* __restrict__ summ) {
+                                                      uint16_t* __restrict__ summ,
+                                                      uint32_t* __restrict__ clear,
+                                                      int64_t clear_words) {
   __shared__ unsigned long long es[kH1Bins];
   __shared__ unsigned long long dig[kMsDigits];
   __shared__ uint32_t bmax;
   const int tid = threadIdx.x;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + tid; i < clear_words;
+       i += (int64_t)gridDim.x * kBlock)
+    clear[i] = 0u;  // (as in k_stream)
   for (int i = tid; i < kH1Bins; i += kBlock) es[i] = 0ull;
   if (tid < kMsDigits) dig[tid] = 0ull;
   if (tid == 0) bmax = 0u;
@@ -2891,10 +2905,10 @@ hipError_t launch_setup_one(TileDesc* tiles, GroupDesc* groups, const float* g, 
 }
 
 hipError_t launch_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, uint32_t* hist1,
-                         int32_t nslots, uint16_t* summ, uint32_t* status, hipStream_t s,
-                         const Ev& ev) {
+                         int32_t nslots, uint16_t* summ, uint32_t* status, uint32_t* clear,
+                         int64_t clear_words, hipStream_t s, const Ev& ev) {
   return launch(k_stream, dim3(grid), dim3(kBlock), s, ev, tiles, ntiles, hist1, nslots, summ,
-                status);
+                status, clear, clear_words);
 }
 
 hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
@@ -2983,10 +2997,10 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
 }
 
 hipError_t launch_ms_stream(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,
-                            uint64_t* esum, uint32_t* emax, uint16_t* summ, hipStream_t s,
-                            const Ev& ev) {
+                            uint64_t* esum, uint32_t* emax, uint16_t* summ, uint32_t* clear,
+                            int64_t clear_words, hipStream_t s, const Ev& ev) {
   return launch(k_ms_stream, dim3(grid), dim3(kBlock), s, ev, tiles, ntiles, (int)nslots,
-                reinterpret_cast<unsigned long long*>(esum), emax, summ);
+                reinterpret_cast<unsigned long long*>(esum), emax, summ, clear, clear_words);
 }
 
 hipError_t launch_ms_count(const TileDesc* tiles, int32_t ntiles, int32_t grid, int32_t nslots,

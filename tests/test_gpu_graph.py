@@ -1,0 +1,97 @@
+"""The execute calls under HIP graph capture.
+
+Plan executions only launch kernels (their tables are written at bind, and
+every buffer they clear is cleared by a kernel, not by a memset), so one
+training step, sparsify then the aggregate + momentum update, can be
+captured once and replayed. The step is captured on fixed buffers; between
+replays the program copies the next gradient and the other workers' lists
+into them eagerly and synchronizes. Every replay is compared bit for bit with
+the same step run eagerly (the update in deterministic mode, so that both
+runs sum in the same order).
+"""
+import numpy as np
+import pytest
+
+import gen
+import paper_2010_10458_amd as tk
+from gpu_common import announce, assert_bitwise, need_gpu, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+STEPS, OTHERS, K_OTHER = 4, 3, 25_600
+
+
+class Step:
+    """Buffers and plans of one sparsify + update step on fixed storage."""
+
+    def __init__(self, sizes, dev):
+        import torch
+        d = sum(sizes)
+        self.sizes, self.d = sizes, d
+        self.grads = [torch.empty(n, device=dev) for n in sizes]
+        self.res = to_dev([np.zeros(n, np.float32) for n in sizes], dev)
+        self.w = to_dev(gen.params_like(sizes, config=5), dev)
+        self.b = to_dev([np.zeros(n, np.float32) for n in sizes], dev)
+        self.sp = tk.SparsifyPlan(sizes, rho=0.001).bind(self.grads, self.res)
+        self.k = self.sp.k_total
+        self.stride = max(self.k, K_OTHER)
+        self.up = tk.UpdatePlan(sizes, P=1 + OTHERS, stride=self.stride,
+                                deterministic=True).bind(self.w, self.b)
+        n = (1 + OTHERS) * self.stride
+        self.idx = torch.zeros(n, dtype=torch.int32, device=dev)
+        self.val = torch.zeros(n, dtype=torch.float32, device=dev)
+        self.nnz = torch.tensor([self.k] + [K_OTHER] * OTHERS, dtype=torch.int32, device=dev)
+
+    def load_inputs(self, s):
+        """Eager: this step's gradient and the other workers' lists."""
+        import torch
+        for t, a in zip(self.grads, gen.resnet_grads(step=s)):
+            t.copy_(torch.from_numpy(a))
+        li, lv = gen.sparse_lists(self.d, OTHERS, K_OTHER, step=2000 + s)
+        for p in range(OTHERS):
+            lo = (1 + p) * self.stride
+            self.idx[lo:lo + K_OTHER].copy_(torch.from_numpy(li[p]))
+            self.val[lo:lo + K_OTHER].copy_(torch.from_numpy(lv[p]))
+
+    def run(self):
+        """The step's GPU work: the calls that are captured."""
+        self.sp.execute(idx_out=self.idx[:self.k], val_out=self.val[:self.k])
+        self.up.execute(self.idx, self.val, lr=0.1, mu=0.9, wd=5e-5, nnz=self.nnz)
+
+    def state(self):
+        return (gen.concat(to_host(self.res)), gen.concat(to_host(self.w)),
+                gen.concat(to_host(self.b)), self.idx[:self.k].cpu().numpy().copy(),
+                self.val[:self.k].cpu().numpy().copy())
+
+
+def test_captured_step_replays_match_eager_steps():
+    import torch
+    dev = need_gpu()
+    sizes = gen.numels(gen.resnet50_shapes())
+    announce("graph: eager reference steps")
+    eager = Step(sizes, dev)
+    ref = []
+    for s in range(STEPS):
+        eager.load_inputs(s)
+        eager.run()
+        torch.cuda.synchronize()
+        ref.append(eager.state())
+    del eager
+
+    announce("graph: capture one step")
+    g = Step(sizes, dev)
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        g.run()
+    torch.cuda.synchronize()
+    # capture records the kernels without running them: the state is untouched
+    assert not torch.cat(g.res).any().item()
+    for s in range(STEPS):
+        announce(f"graph: replay {s}")
+        g.load_inputs(s)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, a, b in zip(("residual", "w", "b", "idx", "val"), g.state(), ref[s]):
+            assert_bitwise(a, b, f"{name} after replay {s}")
