@@ -24,8 +24,9 @@
  * HIP graphs: the *_execute calls of a bound plan only launch kernels, with
  * the same arguments on every call, and leave the workspace's zeroed scratch
  * as they found it, so they can be captured into a graph and replayed (the
- * buffers bound at bind must stay in place). Binds, the one-shot calls and
- * tkef_sparsify_approx_result synchronize and are not capturable.
+ * buffers bound at bind must stay in place); so can tkef_sparsify1_static.
+ * Binds, the other one-shot calls and tkef_sparsify_approx_result
+ * synchronize and are not capturable.
  */
 #ifndef TKEF_H
 #define TKEF_H
