@@ -185,7 +185,7 @@ bool sparsify_layout(tkef_sparsify_plan_s* p) {
   const bool one = p->ngroups == 1;
   const bool approx = p->mode == TKEF_APPROX;
   const bool coll = one && !approx;
-  const int64_t sb = coll ? collect_block(p->nlines) : select_block();
+  const int64_t sb = coll ? collect_block(p->nlines, p->k_total, p->d) : select_block();
   p->sel_block = (int32_t)sb;
   const int64_t sg = select_max_groups();
   const int64_t want = (p->nlines + sb * 256 - 1) / (sb * 256);

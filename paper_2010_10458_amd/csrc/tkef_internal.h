@@ -155,7 +155,7 @@ hipError_t launch_pick(int level, const GroupDesc* groups, GroupState* st,
                        const uint32_t* hist, int32_t nslots, int32_t ngroups, hipStream_t s, const Ev& ev);
 // one selection group
 constexpr int kPerBin = 4;  // band keys per (level-2 bin, region) kept in the rbin table
-// block: collect_block(nlines) threads per workgroup
+// block: collect_block(nlines, k, d) threads per workgroup
 hipError_t launch_collect(const TileDesc* tiles, const GroupDesc* groups, GroupState* st,
                           const uint32_t* hist1, int nslots, const uint16_t* summ, int64_t nlines,
                           int lpt, int32_t grid, int32_t block, uint32_t rcap, uint32_t* hist2,
@@ -214,7 +214,8 @@ hipError_t launch_ms_emit(const TileDesc* tiles, const uint16_t* summ, int64_t n
 // launch-shape limits of the selection kernels
 int32_t select_max_groups();
 int32_t select_block();
-int32_t collect_block(int64_t nlines);  // collect and finish (one exact selection group)
+// threads per workgroup of collect and finish (one exact selection group)
+int32_t collect_block(int64_t nlines, int64_t k, int64_t d);
 int32_t select_max_lpt();
 int32_t emit_lds_groups();  // groups whose bases k_emit can form itself
 
