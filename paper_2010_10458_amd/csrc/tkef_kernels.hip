@@ -483,10 +483,14 @@ constexpr int kSWaves = kSBlock / 64;
 // are walked faster by two half-size workgroups per compute unit, one
 // loading its lines while the other works through its own (110 M
 // elements: 375 against 387 us at rho = 0.01, 342 against 347 at 0.007, even
-// at 0.005, 8-10 us slower at 0.002-0.004).
+// at 0.005, 8-10 us slower at 0.002-0.004), as long as the half-size
+// regions number at most kCDenseMaxGroups: every finish workgroup's work
+// grows with the number of regions (340 M elements, 1,297 regions: 1,372
+// against 1,310 us at rho = 0.01).
 constexpr int kCBlockSmall = 512;
 constexpr int64_t kCSmallLines = (int64_t)256 * kCBlockSmall * 8;
 constexpr int64_t kCDenseDiv = 160;
+constexpr int64_t kCDenseMaxGroups = 512;
 constexpr int kSMaxGroups = 4096;
 constexpr int kSMaxLpt = 16;     // lines per thread at most
 static_assert(kLinesPerTile % kSMaxLpt == 0, "a thread's lines lie in one tile");
@@ -3045,8 +3049,7 @@ hipError_t launch_ms_emit(const TileDesc* tiles, const uint16_t* summ, int64_t n
 int32_t select_max_groups() { return kSMaxGroups; }
 int32_t select_block() { return kSBlock; }
 int32_t collect_block(int64_t nlines, int64_t k, int64_t d) {
-  // (half-size workgroups cover at most this many lines)
-  const bool fits = nlines <= (int64_t)kCBlockSmall * kSMaxLpt * kSMaxGroups;
+  const bool fits = nlines <= (int64_t)kCBlockSmall * kSMaxLpt * kCDenseMaxGroups;
   return (nlines <= kCSmallLines || (k * kCDenseDiv >= d && fits)) ? kCBlockSmall : kSBlock;
 }
 int32_t select_max_lpt() { return kSMaxLpt; }
