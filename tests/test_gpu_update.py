@@ -134,6 +134,22 @@ def test_update_dyadic_bit_exact():
     compare(sizes, w0, None, idx, val, 0.25, 0.0, 0.0, exact=True, label="dyadic plain")
 
 
+@pytest.mark.parametrize("P,stride", [(257, 150), (1000, 40), (65535, 2)])
+def test_update_many_workers(P, stride):
+    """More workers than one update workgroup takes at a time (256): several
+    worker batches per tile, up to the largest P the plan accepts."""
+    rng = np.random.default_rng(34 + P)
+    sizes = [30_011, 4096, 17]
+    d = sum(sizes)
+    w0 = [(rng.standard_normal(n) * 0.1).astype(np.float32) for n in sizes]
+    b0 = [np.zeros(n, np.float32) for n in sizes]
+    idx = np.sort(rng.integers(0, d, (P, stride)), axis=1).astype(np.int32)
+    val = (rng.standard_normal((P, stride)) * 1e-2).astype(np.float32)
+    nnz = rng.integers(0, stride + 1, P).astype(np.int32)
+    compare(sizes, w0, b0, idx, val, 0.1, 0.9, 5e-5, nnz=nnz, label=f"P={P}")
+    compare(sizes, w0, None, idx, val, 0.5, 0.0, 0.0, nnz=nnz, label=f"P={P} plain")
+
+
 def test_update_duplicates_ragged_nnz_and_empty():
     rng = np.random.default_rng(32)
     sizes = [20_000, 333]

@@ -102,6 +102,18 @@ def test_det_many_chunks_and_worker_batches():
     det_update_vs_oracle(sizes, w0, b0, idx, val, 0.1, 0.9, 5e-5, label="300 workers")
 
 
+def test_det_largest_worker_count():
+    """P = 65,535 workers of two entries each (256 worker batches per tile)."""
+    rng = np.random.default_rng(69)
+    sizes = [40_000, 123]
+    d = sum(sizes)
+    w0 = [(rng.standard_normal(n) * 0.1).astype(np.float32) for n in sizes]
+    b0 = [np.zeros(n, np.float32) for n in sizes]
+    idx = np.sort(rng.integers(0, d, (65_535, 2)), axis=1).astype(np.int32)
+    val = (rng.standard_normal((65_535, 2)) * 1e-2).astype(np.float32)
+    det_update_vs_oracle(sizes, w0, b0, idx, val, 0.1, 0.9, 5e-5, label="P=65535")
+
+
 def test_det_repeats_hot_position_ragged_nnz_empty():
     """Repeats within a worker (one worker names position 7 fifty times),
     forty workers all naming positions 7 and 8 (over a thousand entries of
