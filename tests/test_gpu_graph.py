@@ -95,3 +95,51 @@ def test_captured_step_replays_match_eager_steps():
         torch.cuda.synchronize()
         for name, a, b in zip(("residual", "w", "b", "idx", "val"), g.state(), ref[s]):
             assert_bitwise(a, b, f"{name} after replay {s}")
+
+
+@pytest.mark.parametrize("mode", ["per_tensor", "approx"])
+def test_captured_sparsify_modes_replay(mode):
+    """Per-tensor selection and MSTopK: each mode's execution (its own
+    kernels and zeroed scratch) captured once and replayed on changing
+    gradients, every replay bitwise equal to eager execution."""
+    import torch
+    dev = need_gpu()
+    sizes = [300_007, 8192, 1, 77_777, 4096 * 3]
+    tmode = {"per_tensor": tk.PER_TENSOR, "approx": tk.APPROX}[mode]
+
+    def make():
+        g = [torch.empty(n, device=dev) for n in sizes]
+        r = [torch.zeros(n, device=dev) for n in sizes]
+        plan = tk.SparsifyPlan(sizes, rho=0.01, mode=tmode).bind(g, r)
+        idx = torch.empty(plan.k_total, dtype=torch.int32, device=dev)
+        val = torch.empty(plan.k_total, dtype=torch.float32, device=dev)
+        return g, r, plan, idx, val
+
+    def load(g, s):
+        for t, n in zip(g, sizes):
+            t.copy_(torch.from_numpy(gen.flat_normal(n, config=7, step=s)))
+
+    announce(f"graph {mode}: eager")
+    g, r, plan, idx, val = make()
+    ref = []
+    for s in range(3):
+        load(g, s)
+        plan.execute(idx, val)
+        torch.cuda.synchronize()
+        ref.append((idx.cpu().numpy().copy(), val.cpu().numpy().copy(),
+                    gen.concat(to_host(r))))
+    announce(f"graph {mode}: capture and replay")
+    g, r, plan, idx, val = make()
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        plan.execute(idx, val)
+    torch.cuda.synchronize()
+    for s in range(3):
+        load(g, s)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = (idx.cpu().numpy(), val.cpu().numpy(), gen.concat(to_host(r)))
+        for name, a, b in zip(("idx", "val", "residual"), got, ref[s]):
+            assert_bitwise(a, b, f"{mode} {name} after replay {s}")
