@@ -333,3 +333,28 @@ def test_static_entry_point_host_side():
                                          ctypes.byref(nb), None) == tk.OK
         worst = max(worst, nb.value)
     assert worst <= limit, worst
+
+
+def test_header_is_plain_c(tmp_path):
+    """include/tkef.h is a C header: a C11 program includes it, links the
+    library and calls it (version and error strings; nothing reaches a GPU)."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = tmp_path / "use.c"
+    src.write_text(
+        '#include <string.h>\n#include "tkef.h"\n'
+        "int main(void) {\n"
+        "  if (tkef_version() != TKEF_VERSION) return 1;\n"
+        "  if (strlen(tkef_strerror(TKEF_EWORKSPACE)) == 0) return 2;\n"
+        "  if (tkef_k_from_rho(1000, 0.01) != 10) return 3;\n"
+        "  return 0;\n}\n")
+    libdir = os.path.dirname(tk.LIB_PATH if os.path.isabs(tk.LIB_PATH)
+                             else os.path.join(ROOT, tk.LIB_PATH))
+    exe = tmp_path / "use"
+    subprocess.run(["gcc", "-std=c11", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                    "-I/opt/rocm/include", "-I" + os.path.join(ROOT, "include"), str(src),
+                    "-L" + libdir, "-ltkef", "-Wl,-rpath," + libdir, "-o", str(exe)],
+                   check=True, capture_output=True, timeout=120)
+    assert subprocess.run([str(exe)], timeout=120).returncode == 0
