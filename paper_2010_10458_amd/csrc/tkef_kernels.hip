@@ -782,7 +782,7 @@ static_assert(kSMaxGroups <= 65536, "region numbers fit 16 bits");
 // both cache lines of the argument block are fetched then, and later reloads
 // of the pointers hit.)
 template <int NT>
-__global__ __launch_bounds__(NT) void k_collect(
+__global__ __launch_bounds__(NT, 4) void k_collect(
     const TileDesc* __restrict__ tiles, const GroupDesc* __restrict__ groups,
     GroupState* __restrict__ st, const uint32_t* __restrict__ hist1,
     const uint16_t* __restrict__ summ, uint32_t* __restrict__ hist2,
@@ -888,8 +888,7 @@ __global__ __launch_bounds__(NT) void k_collect(
       }
       cw += tot;
     }
-    // the line list is refilled for the next chunk (a barrier also waits for
-    // this thread's global stores, so it is skipped when none follows)
+    // the line list is refilled for the next chunk (skipped after the last)
     if (c0 + (uint32_t)kFlCap < F) __syncthreads();
   }
 
@@ -915,7 +914,6 @@ __global__ __launch_bounds__(NT) void k_collect(
     above += cb[b];
   }
   __syncthreads();
-  // (global stores after the last barrier: a barrier waits for them)
 #pragma unroll
   for (int b = 0; b < kB2; ++b) {
     if (cb[b]) atomicAdd(&hist2[top - b], cb[b]);
@@ -994,8 +992,12 @@ __device__ __forceinline__ void for_class2(int wlim, uint32_t B2, uint32_t rcap,
   }
 }
 
+// (Four waves per SIMD: two 512-thread workgroups, or one of 1,024 threads,
+// per compute unit, so that up to 512 regions are all resident at once; at
+// 129 registers the 512-thread shape fitted one per compute unit and a
+// grid of 424 regions ran in two rounds.)
 template <int NT>
-__global__ __launch_bounds__(NT) void k_finish(
+__global__ __launch_bounds__(NT, 4) void k_finish(
     const TileDesc* __restrict__ tiles, const GroupDesc* __restrict__ groups,
     const GroupState* __restrict__ st, const uint16_t* __restrict__ summ, int64_t nlines,
     int lpt, uint32_t rcap, const uint32_t* __restrict__ hist2,
@@ -1034,13 +1036,18 @@ __global__ __launch_bounds__(NT) void k_finish(
   const uint2 mine = rcnt[w];
   const bool own_ov = (mine.x >> 31) != 0u;
   const uint4* __restrict__ mc = rcand + (size_t)w * rcap;
+  // A region with more stored candidates than threads (dense selections)
+  // takes them in rounds, candidate j on thread j % NT, so that a
+  // wavefront's loads and output stores fall on consecutive entries;
+  // otherwise each thread has at most one.
+  const bool rounds = !own_ov && mine.x > (uint32_t)NT;
   uint32_t cb = 0u, ce = 0u;
-  if (!own_ov) {
-    const uint32_t per = (mine.x + NT - 1) / NT;
-    cb = min(mine.x, tid * per);
-    ce = min(mine.x, cb + per);
+  if (!own_ov && !rounds) {
+    cb = min(mine.x, (uint32_t)tid);
+    ce = min(mine.x, cb + 1u);
   }
-  const uint4 v0 = (cb < ce) ? mc[cb] : make_uint4(0u, 0u, 0u, 0u);
+  const uint4 v0 = (cb < ce || rounds) ? mc[rounds ? (uint32_t)tid : cb]
+                                       : make_uint4(0u, 0u, 0u, 0u);
   uint2 cr[kRegPerThread];
 #pragma unroll
   for (int q = 0; q < kRegPerThread; ++q) {
@@ -1184,8 +1191,9 @@ __global__ __launch_bounds__(NT) void k_finish(
   }
   lines_class2(w, tally);
 
-  // this region: its stored candidates (a run per thread), or its lines.
-  // Counts of (key > T) and (key == T) in position order.
+  // this region: its stored candidate (at most one per thread), or its
+  // lines. Counts of (key > T) and (key == T) in position order (the rounds
+  // count theirs as they go).
   LineSpan ls;
   uint32_t mask = 0u;
   if (own_ov) {
@@ -1203,25 +1211,13 @@ __global__ __launch_bounds__(NT) void k_finish(
     walk_mask(ls, mask, at_least_T,
               [&](int, const TileDesc&, int, float x, uint32_t) { count(x); });
   } else if (cb < ce) {
-    // the run of candidates: the first was fetched at the start, the rest
-    // (dense selections) four loads in flight at a time (clamped indices)
-    count(__uint_as_float(v0.y));
-#pragma unroll 1
-    for (uint32_t j = cb + 1; j < ce; j += 4) {
-      uint4 q[4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) q[c] = mc[min(j + (uint32_t)c, ce - 1u)];
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (j + (uint32_t)c < ce) count(__uint_as_float(q[c].y));
-    }
+    count(__uint_as_float(v0.y));  // (fetched at the start)
   }
   const uint32_t sv[4] = {gt, eq, gtb, eqb};
   uint32_t pre[4], tot[4];
   block_scan4<NT>(sv, wsum, pre, tot);
   // clear the part of the zero-initialised scratch that only the earlier
   // kernels of this execution use (not read here), for the next execution
-  // (after the last barrier, which would wait for these stores)
 #pragma unroll 1
   for (int64_t i = (int64_t)w * NT + tid; i < clear_words; i += (int64_t)G * NT)
     clear_next[i] = 0u;
@@ -1230,7 +1226,7 @@ __global__ __launch_bounds__(NT) void k_finish(
   // zero its residuals here: it records its range of output slots, and the
   // last workgroup to finish zeroes the residuals at those slots' indices.
   const bool defer = (mine.y >> 31) != 0u;
-  if (defer && tid == 0) {
+  if (defer && tid == 0 && !rounds) {
     const uint32_t lo = tot[2] + min(tot[3], need3);
     const uint32_t hi = tot[2] + tot[0] + min(tot[3] + tot[1], need3);
     rzr[w] = (uint64_t)min(lo, k) | ((uint64_t)min(hi, k) << 32);
@@ -1255,26 +1251,48 @@ __global__ __launch_bounds__(NT) void k_finish(
       if (!defer) *gptr(rp) = 0.0f;
     }
   };
-  if (gt + eq == 0u) {
+  if (rounds) {
+    // elements above T and equal to T before the round (uniform); per
+    // round one scan of both counts, packed in 16-bit halves (a round
+    // holds at most NT of each)
+    uint32_t gtr_r = tot[2], eqr_r = tot[3];
+    uint4 cur = v0;
+#pragma unroll 1
+    for (uint32_t r0 = 0; r0 < mine.x; r0 += NT) {
+      const uint32_t j = r0 + (uint32_t)tid;
+      const uint4 nxt = mc[min(j + (uint32_t)NT, mine.x - 1u)];  // next round's (clamped)
+      const bool have = j < mine.x;
+      const float x = __uint_as_float(cur.y);
+      const uint32_t key = mag_key(x);
+      const bool isg = have && key > T, ise = have && key == T;
+      uint32_t rt;
+      const uint32_t rp = block_scan<NT>((isg ? 1u : 0u) | (ise ? 0x10000u : 0u), wsum, &rt);
+      const uint32_t gbef = gtr_r + (rp & 0xFFFFu), ebef = eqr_r + (rp >> 16);
+      uint32_t pos = 0xFFFFFFFFu;
+      if (isg) pos = gbef + min(ebef, need3);
+      else if (ise && ebef < need3) pos = gbef + ebef;
+      if (pos < k) {
+        idx_out[pos] = (int32_t)cur.x;
+        put_val(val_out, pos, x, val16);
+        if (!defer) *gptr(reinterpret_cast<float*>(((uint64_t)cur.w << 32) | cur.z)) = 0.0f;
+      }
+      gtr_r += rt & 0xFFFFu;
+      eqr_r += rt >> 16;
+      cur = nxt;
+    }
+    if (defer && tid == 0) {
+      const uint32_t lo = tot[2] + min(tot[3], need3);
+      const uint32_t hi = gtr_r + min(eqr_r, need3);
+      rzr[w] = (uint64_t)min(lo, k) | ((uint64_t)min(hi, k) << 32);
+    }
+  } else if (gt + eq == 0u) {
     // nothing to write
   } else if (own_ov) {
     walk_mask(ls, mask, at_least_T, [&](int, const TileDesc& t, int e, float x, uint32_t) {
       write((uint32_t)(t.gstart + e), t.r + e, x);
     });
   } else if (cb < ce) {
-    auto write_c = [&](const uint4& v) {
-      write(v.x, reinterpret_cast<float*>(((uint64_t)v.w << 32) | v.z), __uint_as_float(v.y));
-    };
-    write_c(v0);
-#pragma unroll 1
-    for (uint32_t j = cb + 1; j < ce; j += 4) {
-      uint4 q[4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) q[c] = mc[min(j + (uint32_t)c, ce - 1u)];
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (j + (uint32_t)c < ce) write_c(q[c]);
-    }
+    write(v0.x, reinterpret_cast<float*>(((uint64_t)v0.w << 32) | v0.z), __uint_as_float(v0.y));
   }
   if (!any_unstored) return;  // (uniform) the common case ends here
   // Every workgroup has read all it reads of the unstored regions' lines and
