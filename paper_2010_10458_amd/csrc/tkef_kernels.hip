@@ -1509,17 +1509,21 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
   __shared__ int32_t stage_code[kStage * kSBlock];  // [slot][thread]: (tile << 13) | e
   __shared__ float stage_x[kStage * kSBlock];
   __shared__ uint2 lbase[kEmitLdsGroups];
+  __shared__ uint4 lgrp[kEmitLdsGroups];  // per group: T, need, k, out_base
   const int tid = threadIdx.x;
   // With fold_ngroups > 0 (at most kEmitLdsGroups groups) every workgroup
   // forms the groups' bases itself (what k_groupscan writes into base[]):
-  // the groups' results are fetched now and scanned after pass 1.
+  // the groups' results are fetched now and scanned after pass 1, and what
+  // the writes need of each group is kept in LDS.
   uint32_t fgt = 0u, feq = 0u;
   if (tid < fold_ngroups) {
     const GroupState sg = st[tid];
-    const uint32_t kg = groups[tid].k;
-    fgt = (kg > sg.need) ? kg - sg.need : 0u;
+    const GroupDesc gd = groups[tid];
+    fgt = (gd.k > sg.need) ? gd.k - sg.need : 0u;
     feq = sg.need ? sg.n_eq : 0u;
+    lgrp[tid] = make_uint4(sg.T, sg.need, gd.k, gd.out_base);
   }
+  if (fold_ngroups > 0) __syncthreads();  // (uniform)
   // clear the part of the zero-initialised scratch that only the earlier
   // kernels of this execution use (not read here), for the next execution
 #pragma unroll 1
@@ -1527,7 +1531,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
        i += (int64_t)gridDim.x * kSBlock)
     clear_next[i] = 0u;
   const uint32_t ov = meta[0], C = meta[1];
-  auto T_of = [&](int g) -> uint32_t { return st[g].T; };
+  auto T_of = [&](int g) -> uint32_t { return fold_ngroups > 0 ? lgrp[g].x : st[g].T; };
   // this thread's elements: a run of candidates, or (after an overflow) lines
   LineSpan ls;
   uint32_t mask = 0u, cb = 0u, ce = 0u;
@@ -1575,12 +1579,26 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
   // pass 2: write
   auto write = [&](int, const TileDesc& t, int e, float x, uint32_t k) {
     const int g = t.group;
-    const uint32_t T = T_of(g);
+    uint32_t T, need, gk, gob, bg, be;
+    if (fold_ngroups > 0) {
+      const uint4 q = lgrp[g];
+      T = q.x;
+      need = q.y;
+      gk = q.z;
+      gob = q.w;
+      bg = lbase[g].x;
+      be = lbase[g].y;
+    } else {
+      const GroupState sg = st[g];
+      const GroupDesc gd = groups[g];
+      T = sg.T;
+      need = sg.need;
+      gk = gd.k;
+      gob = gd.out_base;
+      bg = base[2 * g];
+      be = base[2 * g + 1];
+    }
     if (k < T) return;
-    const GroupDesc gd = groups[g];
-    const uint32_t need = st[g].need;
-    const uint32_t bg = fold_ngroups > 0 ? lbase[g].x : base[2 * g];
-    const uint32_t be = fold_ngroups > 0 ? lbase[g].y : base[2 * g + 1];
     uint32_t pos = 0xFFFFFFFFu;
     if (k > T) {
       pos = (gtr - bg) + min(eqr - be, need);
@@ -1589,20 +1607,26 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
       if (eqr - be < need) pos = (gtr - bg) + (eqr - be);
       ++eqr;
     }
-    if (pos < gd.k) {
-      idx_out[gd.out_base + pos] = t.gstart + e;
-      put_val(val_out, (size_t)gd.out_base + pos, x, val16);
+    if (pos < gk) {
+      idx_out[gob + pos] = t.gstart + e;
+      put_val(val_out, (size_t)gob + pos, x, val16);
       gptr(t.r)[e] = 0.0f;
     }
   };
   if (nst <= (uint32_t)kStage) {
-#pragma unroll 1
-    for (uint32_t q = 0; q < nst; ++q) {
-      const uint32_t code = (uint32_t)stage_code[q * kSBlock + tid];
-      const int tile = (int)(code >> kCandShift);
-      const TileDesc t = tiles[tile];
-      const float x = stage_x[q * kSBlock + tid];
-      write(tile, t, (int)(code & (kTile - 1)), x, mag_key(x));
+    // the staged elements' tile descriptors are all requested before the
+    // first write
+    TileDesc td[kStage];
+#pragma unroll
+    for (int q = 0; q < kStage; ++q)
+      if ((uint32_t)q < nst) td[q] = tiles[(uint32_t)stage_code[q * kSBlock + tid] >> kCandShift];
+#pragma unroll
+    for (int q = 0; q < kStage; ++q) {
+      if ((uint32_t)q < nst) {
+        const uint32_t code = (uint32_t)stage_code[q * kSBlock + tid];
+        const float x = stage_x[q * kSBlock + tid];
+        write((int)(code >> kCandShift), td[q], (int)(code & (kTile - 1)), x, mag_key(x));
+      }
     }
   } else if (ov) {
     walk_mask(ls, mask, at_least_T, write);
