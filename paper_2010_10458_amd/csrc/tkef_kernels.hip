@@ -1489,6 +1489,7 @@ __global__ __launch_bounds__(kSBlock) void k_groupscan(const GroupDesc* __restri
 // need_g); an element with key == T_g is kept while fewer than need_g equal
 // keys precede it in g. Counts before an element are global prefixes (over
 // the candidate list, in position order) minus the group's base.
+template <bool kFold>
 __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ tiles,
                                                   int32_t ntiles,
                                                   const GroupDesc* __restrict__ groups,
@@ -1511,7 +1512,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
   __shared__ uint2 lbase[kEmitLdsGroups];
   __shared__ uint4 lgrp[kEmitLdsGroups];  // per group: T, need, k, out_base
   const int tid = threadIdx.x;
-  // With fold_ngroups > 0 (at most kEmitLdsGroups groups) every workgroup
+  // With kFold (fold_ngroups, at most kEmitLdsGroups, groups) every workgroup
   // forms the groups' bases itself (what k_groupscan writes into base[]):
   // the groups' results are fetched now and scanned after pass 1, and what
   // the writes need of each group is kept in LDS.
@@ -1523,7 +1524,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
     feq = sg.need ? sg.n_eq : 0u;
     lgrp[tid] = make_uint4(sg.T, sg.need, gd.k, gd.out_base);
   }
-  if (fold_ngroups > 0) __syncthreads();  // (uniform)
+  if constexpr (kFold) __syncthreads();
   // clear the part of the zero-initialised scratch that only the earlier
   // kernels of this execution use (not read here), for the next execution
 #pragma unroll 1
@@ -1531,7 +1532,10 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
        i += (int64_t)gridDim.x * kSBlock)
     clear_next[i] = 0u;
   const uint32_t ov = meta[0], C = meta[1];
-  auto T_of = [&](int g) -> uint32_t { return fold_ngroups > 0 ? lgrp[g].x : st[g].T; };
+  auto T_of = [&](int g) -> uint32_t {
+    if constexpr (kFold) return lgrp[g].x;
+    else return st[g].T;
+  };
   // this thread's elements: a run of candidates, or (after an overflow) lines
   LineSpan ls;
   uint32_t mask = 0u, cb = 0u, ce = 0u;
@@ -1563,7 +1567,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
   auto at_least_T = [&](int g, uint32_t k) -> bool { return k >= T_of(g); };
   if (ov) walk_mask(ls, mask, at_least_T, count);
   else walk_cands(tiles, ntiles, cand, cb, ce, count);
-  if (fold_ngroups > 0) {  // (uniform; its barriers also order lbase for the writes)
+  if constexpr (kFold) {  // (its barriers also order lbase for the writes)
     uint2 gtot;
     const uint2 gx = block_scan2<kSBlock>(fgt, feq, wsum, &gtot);
     if (tid < fold_ngroups) lbase[tid] = gx;
@@ -1580,7 +1584,7 @@ __global__ __launch_bounds__(kSBlock) void k_emit(const TileDesc* __restrict__ t
   auto write = [&](int, const TileDesc& t, int e, float x, uint32_t k) {
     const int g = t.group;
     uint32_t T, need, gk, gob, bg, be;
-    if (fold_ngroups > 0) {
+    if constexpr (kFold) {
       const uint4 q = lgrp[g];
       T = q.x;
       need = q.y;
@@ -3043,7 +3047,10 @@ hipError_t launch_emit(const TileDesc* tiles, int32_t ntiles, const GroupDesc* g
                        int val16, uint32_t* status, uint32_t* clear_next, int64_t clear_words,
                        int32_t fold_ngroups, hipStream_t s, const Ev& ev) {
   if (fold_ngroups > kEmitLdsGroups) return hipErrorInvalidValue;
-  return launch(k_emit, dim3(grid), dim3(kSBlock), s, ev, tiles, ntiles, groups, st, summ, nlines,
+  // (one instantiation per case, so that no load picks between an LDS and a
+  // global address at run time: that would be a flat load)
+  return launch(fold_ngroups > 0 ? k_emit<true> : k_emit<false>, dim3(grid), dim3(kSBlock), s, ev,
+                tiles, ntiles, groups, st, summ, nlines,
                 lpt, reinterpret_cast<const uint2*>(cand), meta, base, flags, idx_out, val_out,
                 val16, status, clear_next, clear_words, fold_ngroups);
 }
