@@ -412,3 +412,47 @@ def test_band_beyond_region_capacity(case):
         k = 3500
     r = np.zeros(n, np.float32)
     compare_with_oracle([g], [r], k=k, label=f"band beyond region capacity ({case})")
+
+
+@pytest.mark.parametrize("levels", [3, 50])
+def test_dense_regions_with_ties_across_rounds(levels):
+    """2^21 elements whose magnitudes take only `levels` values, k = 150,000:
+    each of the 32 selection regions stores several thousand candidates,
+    taken by the finish kernel in rounds of one candidate per thread, and the
+    threshold class (tens of thousands of equal magnitudes, split by
+    position) runs through many rounds of every region."""
+    rng = np.random.default_rng(9100 + levels)
+    n = 1 << 21
+    mags = np.sort(rng.random(levels).astype(np.float32) + np.float32(0.5))
+    g = (mags[rng.integers(0, levels, n)] * rng.choice([-1, 1], n)).astype(np.float32)
+    r = np.zeros(n, np.float32)
+    idx, val, _ = compare_with_oracle([g], [r], k=150_000,
+                                      label=f"dense ties across rounds ({levels} levels)")
+    # the threshold class is split: some of its members are taken, some not
+    T = np.abs(val).min()
+    taken = np.count_nonzero(np.abs(val) == T)
+    assert 0 < taken < np.count_nonzero(np.abs(g) == T)
+
+
+def test_large_regions_with_ties_across_rounds():
+    """40 M elements, k = 200,000, values N(0, 1) rounded to multiples of
+    1/64: above 2^20 summary lines and with k < d / 160 the selection runs
+    1,024-thread workgroups (153 regions), each storing about 1,500
+    candidates, which the finish kernel takes in two rounds; the threshold
+    class (thousands of equal magnitudes) is split by position. Checked
+    through the exact selection properties against the oracle's x."""
+    import torch
+    dev = need_gpu()
+    rng = np.random.default_rng(9200)
+    n = 40_000_000
+    g = (np.round(rng.standard_normal(n) * 64) / 64).astype(np.float32)
+    announce("sparsify 40M quantized k=200000")
+    gd, rd = torch.from_numpy(g).to(dev), torch.zeros(n, device=dev)
+    plan = tk.SparsifyPlan([n], k=200_000).bind([gd], [rd])
+    idx, val = plan.execute()
+    torch.cuda.synchronize()
+    idx, val = idx.cpu().numpy(), val.cpu().numpy()
+    x = orc().ef_add(g, np.zeros(n, np.float32))
+    check_selection(x, idx, val, rd.cpu().numpy(), 200_000)
+    T = np.abs(val).min()
+    assert 0 < np.count_nonzero(np.abs(val) == T) < np.count_nonzero(np.abs(x) == T)
