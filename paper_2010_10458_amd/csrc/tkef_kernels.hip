@@ -2414,6 +2414,49 @@ __device__ __forceinline__ int ms_bin_big(const uint32_t* K, uint32_t key) {
   return base;
 }
 
+// The thresholds of a pass are evenly spaced in value: threshold j is
+// abar + (l + j step)(u - abar). So the bin of a magnitude a is
+// floor(((a - abar) / (u - abar) - l) / step) up to the roundings of that
+// expression and of the thresholds' keys; ms_bin_est computes it in double
+// and keeps it when its two keys bracket the element's key (one LDS round
+// trip), else searches. Thresholds that round to one key (a narrow interval
+// after a few passes) fail the check and are searched, so the result is
+// always the search's.
+struct MsEst {
+  double c0, c1, c2;  // abar, 1 / ((u - abar) step), l / step
+};
+__device__ __forceinline__ MsEst ms_est(const MsState& s, int nb) {
+  const double step = ms_step(s, nb);
+  MsEst e;
+  e.c0 = s.abar;
+  e.c1 = 1.0 / ((s.u - s.abar) * step);  // (inf or NaN when u == abar: the check fails)
+  e.c2 = s.l / step;
+  return e;
+}
+__device__ __forceinline__ int ms_bin_est(const uint32_t* K, uint32_t key, const MsEst& e) {
+  constexpr int NB = kMsRefineKeys;
+  const double a = (double)__uint_as_float(key);
+  double jd = floor((a - e.c0) * e.c1 - e.c2);
+  jd = fmin(fmax(jd, 1.0), (double)(NB - 1));  // (fmax takes 1 over a NaN)
+  const int j = (int)jd;
+  const uint32_t lo = K[j];
+  const uint32_t hi = (j + 1 < NB) ? K[j + 1] : 0xFFFFFFFFu;
+  if (lo <= key && key < hi) return j;
+  return ms_bin_big(K, key);
+}
+// The first pass: l = 0 and step = 1 / 64, so the bin is
+// floor((a - abar) * 64 / (u - abar)); in binary32 (c0 = abar, c1 = 64 /
+// (u - abar), both rounded), which the check makes exact all the same.
+__device__ __forceinline__ int ms_bin_est64(const uint32_t* K, uint32_t key, float c0, float c1) {
+  float jf = floorf((__uint_as_float(key) - c0) * c1);
+  jf = fminf(fmaxf(jf, 1.0f), (float)(kMsKeys - 1));  // (fmaxf takes 1 over a NaN)
+  const int j = (int)jf;
+  const uint32_t lo = K[j];
+  const uint32_t hi = (j + 1 < kMsKeys) ? K[j + 1] : 0xFFFFFFFFu;
+  if (lo <= key && key < hi) return j;
+  return ms_bin(K, key);
+}
+
 // The state before the first pass, from the stream's partial sums: nslots
 // copies of the digits (kMsDigitStride words apart) and of the largest key.
 // Whole workgroup (>= kMsDigits threads).
@@ -2680,6 +2723,8 @@ __global__ __launch_bounds__(kBlock) void k_ms_count(
   }
   if (tid < kMsKeys) h[tid] = 0u;
   ms_keys(s, K, kMsKeys);
+  // (the first pass brackets the ratio in [0, 1])
+  const float c0 = (float)s.abar, c1 = (float)(64.0 / (s.u - s.abar));
   const uint32_t kmin = K[1];
   const uint32_t smin = kmin >> 16;  // a line is read if its summary reaches this
   const int per_tile = kTile / kQuarter;
@@ -2742,14 +2787,14 @@ __global__ __launch_bounds__(kBlock) void k_ms_count(
       uint32_t key = 0u;
 #pragma unroll
       for (int c = 0; c < kSlots; ++c) key = (c == j) ? keys[c] : key;
-      atomicAdd(&h[ms_bin(K, key)], 1u);
+      atomicAdd(&h[ms_bin_est64(K, key, c0, c1)], 1u);
     }
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       if (!full[q] && len[q] > 0) {
         for (int e = tid; e < len[q]; e += kBlock) {
           const uint32_t key = mag_key(gptr(xs[q])[e]);
-          if (key >= kmin) atomicAdd(&h[ms_bin(K, key)], 1u);
+          if (key >= kmin) atomicAdd(&h[ms_bin_est64(K, key, c0, c1)], 1u);
         }
       }
     }
@@ -2783,11 +2828,12 @@ __global__ __launch_bounds__(kSBlock) void k_ms_refine(
   if (blockIdx.x == 0 && tid == 0) *st_out = s;
   for (int i = tid; i < kMsRefineKeys; i += kSBlock) h[i] = 0u;
   ms_keys(s, K, kMsRefineKeys);
+  const MsEst est = ms_est(s, kMsRefineKeys);
   const uint32_t kmin = K[1];
   const uint32_t mask = ls.flagged([&](int) -> uint32_t { return kmin; });
   walk_mask(ls, mask, [&](int, uint32_t key) -> bool { return key >= kmin; },
             [&](int, const TileDesc&, int, float, uint32_t key) {
-              atomicAdd(&h[ms_bin_big(K, key)], 1u);
+              atomicAdd(&h[ms_bin_est(K, key, est)], 1u);
             });
   __syncthreads();
   for (int i = tid; i < kMsRefineKeys; i += kSBlock)
