@@ -7,7 +7,8 @@ captured once and replayed. The step is captured on fixed buffers; between
 replays the program copies the next gradient and the other workers' lists
 into them eagerly and synchronizes. Every replay is compared bit for bit with
 the same step run eagerly (the update in deterministic mode, so that both
-runs sum in the same order).
+runs sum in the same order). The per-tensor and MSTopK selections and the
+LARS step are captured and replayed the same way.
 """
 import numpy as np
 import pytest
@@ -143,3 +144,56 @@ def test_captured_sparsify_modes_replay(mode):
         got = (idx.cpu().numpy(), val.cpu().numpy(), gen.concat(to_host(r)))
         for name, a, b in zip(("idx", "val", "residual"), got, ref[s]):
             assert_bitwise(a, b, f"{mode} {name} after replay {s}")
+
+
+def test_captured_lars_step_replays():
+    """The LARS step fused with the aggregate (segment table, norm pass,
+    rates, step pass) captured once and replayed on changing lists, with
+    momentum: every replay's parameters, momentum and rates bitwise equal to
+    the same step run eagerly (deterministic sums; the rates' double sums
+    run in a fixed order)."""
+    import torch
+    dev = need_gpu()
+    sizes = [300_007, 8192, 1, 77_777, 4096 * 3]
+    d, P, K = sum(sizes), 6, 20_000
+    gamma, eta, eps, mu = 1e-3, 0.1, 5e-5, 0.9
+
+    def make():
+        w = to_dev(gen.params_like(sizes, config=11), dev)
+        b = to_dev([np.zeros(n, np.float32) for n in sizes], dev)
+        plan = tk.UpdatePlan(sizes, P=P, stride=K, deterministic=True).bind(w, b)
+        idx = torch.zeros((P, K), dtype=torch.int32, device=dev)
+        val = torch.zeros((P, K), dtype=torch.float32, device=dev)
+        rates = torch.zeros(len(sizes), dtype=torch.float64, device=dev)
+        return w, b, plan, idx, val, rates
+
+    def load(idx, val, s):
+        li, lv = gen.sparse_lists(d, P, K, config=11, step=s)
+        idx.copy_(torch.from_numpy(li))
+        val.copy_(torch.from_numpy(lv))
+
+    def state(w, b, rates):
+        return (gen.concat(to_host(w)), gen.concat(to_host(b)), rates.cpu().numpy().copy())
+
+    announce("graph lars: eager")
+    w, b, plan, idx, val, rates = make()
+    ref = []
+    for s in range(3):
+        load(idx, val, s)
+        plan.lars_execute(idx, val, gamma, eta, eps, mu=mu, rates=rates)
+        torch.cuda.synchronize()
+        ref.append(state(w, b, rates))
+    announce("graph lars: capture and replay")
+    w, b, plan, idx, val, rates = make()
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        plan.lars_execute(idx, val, gamma, eta, eps, mu=mu, rates=rates)
+    torch.cuda.synchronize()
+    for s in range(3):
+        load(idx, val, s)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, a, r in zip(("w", "b", "rates"), state(w, b, rates), ref[s]):
+            assert_bitwise(a, r, f"lars {name} after replay {s}")
