@@ -194,6 +194,21 @@ def test_fp16_values_edge_magnitudes():
         compare16([g], [r], k=k, label=f"edge k={k}")
 
 
+def test_fp16_values_dense_regions():
+    """A dense selection with binary16 values: 2^21 elements on a grid of
+    1/256 (ties), k = 150,000, so every selection region stores thousands of
+    candidates and the finish kernel writes them in rounds of one per
+    thread; globally and per tensor (two tensors)."""
+    rng = np.random.default_rng(53)
+    n = 1 << 21
+    g = (np.round(rng.standard_normal(n) * 256) / 256).astype(np.float32)
+    r = np.zeros(n, np.float32)
+    compare16([g], [r], k=150_000, label="dense fp16")
+    h = n // 2
+    compare16([g[:h], g[h:]], [r[:h], r[h:]], rho=0.07, mode=tk.PER_TENSOR,
+              label="dense fp16 per tensor")
+
+
 @pytest.mark.parametrize("mode", [tk.GLOBAL, tk.PER_TENSOR])
 def test_fp16_values_resnet_step(mode):
     sizes = gen.numels(gen.resnet50_shapes())
