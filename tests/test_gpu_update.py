@@ -253,3 +253,42 @@ def test_c5_resnet50_p128_momentum_3_steps():
         assert np.all(np.abs(bg.astype(np.float64) - b_ref) <= 1e-6 * (np.abs(b_ref) + S / 0.1))
         # carry the GPU state forward so later steps test one step at a time
         w_ref, b_ref = wg, bg
+
+
+@pytest.mark.parametrize("mu,wd", [(0.0, 0.0), (0.9, 5e-5)])
+def test_update_worker_order_permuted(mu, wd):
+    """The same 24 overlapping lists in a permuted worker order: each
+    position's sum then runs in another order, so the result must agree with
+    the oracle's original-order result within the bound that covers any
+    order, and bit for bit where a position has at most two contributions."""
+    rng = np.random.default_rng(808 + int(mu * 10))
+    sizes = [100_003, 4097]
+    d = sum(sizes)
+    P, k = 24, 3000
+    idx, val = _lists(rng, d, P, k, std=0.1, overlap=True)
+    perm = rng.permutation(P)
+    assert not np.array_equal(perm, np.arange(P))
+    w0 = [(rng.standard_normal(n) * 0.1).astype(np.float32) for n in sizes]
+    b0 = [(rng.standard_normal(n) * 0.01).astype(np.float32) for n in sizes] if mu else None
+    lr = 0.05
+    announce(f"update worker order permuted mu={mu}")
+    w_gpu, b_gpu, status = gpu_update(sizes, w0, b0, idx[perm], val[perm], lr, mu, wd)
+    assert status == 0
+    w_ref, b_ref = orc().update(gen.concat(w0), None if b0 is None else gen.concat(b0), idx, val,
+                                lr=lr, mu=mu, wd=wd)
+    wg = gen.concat(w_gpu)
+    cnt = np.bincount(idx.ravel().astype(np.int64), minlength=d)
+    assert (cnt >= 3).sum() > 1000  # the overlap makes many positions order-sensitive
+    le2 = cnt <= 2
+    assert_bitwise(wg[le2], w_ref[le2], "w (<= 2 contributions)")
+    A = np.zeros(d)
+    np.add.at(A, idx.ravel().astype(np.int64), np.abs(val.ravel().astype(np.float64)))
+    w0c = np.abs(gen.concat(w0)).astype(np.float64)
+    b0c = np.abs(gen.concat(b0)).astype(np.float64) if b0 is not None else 0.0
+    S = lr * (A + wd * w0c + mu * b0c)
+    assert np.all(np.abs(wg.astype(np.float64) - w_ref) <= 1e-6 * (np.abs(w_ref) + S))
+    if b_ref is not None:
+        bg = gen.concat(b_gpu)
+        assert_bitwise(bg[le2], b_ref[le2], "b (<= 2 contributions)")
+        Sb = A + wd * w0c + mu * b0c
+        assert np.all(np.abs(bg.astype(np.float64) - b_ref) <= 1e-6 * (np.abs(b_ref) + Sb))
