@@ -1039,7 +1039,9 @@ __global__ __launch_bounds__(NT, 4) void k_finish(
   // A region with more stored candidates than threads (dense selections)
   // takes them in rounds, candidate j on thread j % NT, so that a
   // wavefront's loads and output stores fall on consecutive entries;
-  // otherwise each thread has at most one.
+  // otherwise each thread has at most one. (A region that stored its
+  // candidates also stored its band, which they include: it never defers
+  // its residual zeros, below.)
   const bool rounds = !own_ov && mine.x > (uint32_t)NT;
   uint32_t cb = 0u, ce = 0u;
   if (!own_ov && !rounds) {
@@ -1226,7 +1228,7 @@ __global__ __launch_bounds__(NT, 4) void k_finish(
   // zero its residuals here: it records its range of output slots, and the
   // last workgroup to finish zeroes the residuals at those slots' indices.
   const bool defer = (mine.y >> 31) != 0u;
-  if (defer && tid == 0 && !rounds) {
+  if (defer && tid == 0) {
     const uint32_t lo = tot[2] + min(tot[3], need3);
     const uint32_t hi = tot[2] + tot[0] + min(tot[3] + tot[1], need3);
     rzr[w] = (uint64_t)min(lo, k) | ((uint64_t)min(hi, k) << 32);
@@ -1274,16 +1276,11 @@ __global__ __launch_bounds__(NT, 4) void k_finish(
       if (pos < k) {
         idx_out[pos] = (int32_t)cur.x;
         put_val(val_out, pos, x, val16);
-        if (!defer) *gptr(reinterpret_cast<float*>(((uint64_t)cur.w << 32) | cur.z)) = 0.0f;
+        *gptr(reinterpret_cast<float*>(((uint64_t)cur.w << 32) | cur.z)) = 0.0f;
       }
       gtr_r += rt & 0xFFFFu;
       eqr_r += rt >> 16;
       cur = nxt;
-    }
-    if (defer && tid == 0) {
-      const uint32_t lo = tot[2] + min(tot[3], need3);
-      const uint32_t hi = gtr_r + min(eqr_r, need3);
-      rzr[w] = (uint64_t)min(lo, k) | ((uint64_t)min(hi, k) << 32);
     }
   } else if (gt + eq == 0u) {
     // nothing to write
